@@ -1,0 +1,292 @@
+"""Seeded synthetic workloads for GRAFT's per-round draft-tree construction.
+
+This module only draws inputs.  It holds none of the method's arithmetic (no
+softmax, top-K, edge scoring, budget choice, selection or acceptance): both the
+CPU oracle and the HIP library receive exactly the arrays produced here.
+
+Workloads (shapes from the five benchmark configurations of the hot path):
+
+  id  batch  L   V       K   N_max  budget                         scorer d/rank
+  0   1      8   32000   4   32     fixed 32                       64/16
+  1   1      16  151936  8   64     fixed 64                       64/16
+  2   16     16  151936  8   256    SABA {16,32,64,128,256}        64/16
+  3   64     16  128256  16  512    SABA 32..512 step 16           128/32
+  4   128    32  151936  32  1024   SABA 32..1024 step 16          128/32
+
+Drafter logits (one row per future position): z ~ N(0,1) per entry, divided by
+a per-row temperature T ~ U(0.5, 1.5) in workloads 3 and 4, then n_boost
+distinct uniformly drawn token ids get +6 * r**-1.2 for rank r = 1..n_boost
+(n_boost = L), rounded to bf16 with round-to-nearest-even.  The vocabulary
+sizes are those of the Qwen3 family (151936) and a 128256-entry vocabulary.
+
+Every random stream is keyed by (workload seed, round, sequence, attempt,
+stream id) through numpy's SeedSequence, so one sequence can be re-drawn
+(attempt + 1) without touching the others.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = [
+    "Workload", "WORKLOADS", "workload", "bf16_from_f32", "f32_from_bf16",
+    "gen_sequence_logits", "gen_round", "gen_scorer", "saba_params",
+    "hist_ring_init", "node_targets", "splitmix64", "NODE_TARGET_P_NUM",
+]
+
+HIST_WINDOW = 4
+
+
+@dataclass(frozen=True)
+class Workload:
+    wid: int
+    batch: int
+    L: int
+    V: int
+    K: int
+    n_max: int
+    budget_mode: str              # "fixed" or "saba"
+    fixed_budget: int = 0
+    grid: tuple = ()
+    c1: float = 0.0
+    c2: float = 0.0
+    emb_dim: int = 64
+    rank: int = 16
+    temperature: bool = False
+    targets: str = "depth"        # "depth" (second logit tensor) or "node" (counter hash)
+    rounds: int = 1
+    phi: tuple = (0.0, 0.0, 0.0, 0.0)
+    seed: int = 0
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def n_boost(self) -> int:
+        return self.L
+
+
+WORKLOADS = {
+    0: Workload(0, 1, 8, 32000, 4, 32, "fixed", fixed_budget=32, emb_dim=64, rank=16,
+                seed=1000),
+    1: Workload(1, 1, 16, 151936, 8, 64, "fixed", fixed_budget=64, emb_dim=64, rank=16,
+                seed=1001),
+    2: Workload(2, 16, 16, 151936, 8, 256, "saba", grid=(16, 32, 64, 128, 256),
+                c1=1.0 / 128, c2=0.0, emb_dim=64, rank=16,
+                phi=(6.0, 2000.0, 0.5, 14.0), seed=1002),
+    3: Workload(3, 64, 16, 128256, 16, 512, "saba", grid=tuple(range(32, 513, 16)),
+                c1=1.0 / 256, c2=2e-7, emb_dim=128, rank=32, temperature=True,
+                phi=(6.0, 2000.0, 0.5, 18.0), seed=1003),
+    4: Workload(4, 128, 32, 151936, 32, 1024, "saba", grid=tuple(range(32, 1025, 16)),
+                c1=1.0 / 512, c2=2e-7, emb_dim=128, rank=32, temperature=True,
+                targets="node", rounds=50, phi=(6.0, 2000.0, 0.5, 40.0), seed=1004),
+}
+
+
+def workload(wid: int, **overrides) -> Workload:
+    """The named workload, optionally with fields replaced (smaller test shapes)."""
+    w = WORKLOADS[wid]
+    if overrides:
+        d = dict(w.__dict__)
+        d.update(overrides)
+        w = Workload(**d)
+    return w
+
+
+def _rng(w: Workload, rnd: int, b: int, attempt: int, stream: int) -> np.random.Generator:
+    return np.random.default_rng([w.seed, w.wid, rnd, b, attempt, stream])
+
+
+def bf16_from_f32(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round-to-nearest-even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def f32_from_bf16(h: np.ndarray) -> np.ndarray:
+    return (np.asarray(h, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _boost_weights(n: int) -> np.ndarray:
+    r = np.arange(1, n + 1, dtype=np.float64)
+    return (6.0 * r ** -1.2).astype(np.float32)
+
+
+def gen_sequence_logits(w: Workload, rnd: int, b: int, attempt: int = 0):
+    """Drafter logits of one sequence: (bf16 bits [L, V], boosted ids [L, n_boost])."""
+    g = _rng(w, rnd, b, attempt, 0)
+    out = np.empty((w.L, w.V), dtype=np.uint16)
+    boost_ids = np.empty((w.L, w.n_boost), dtype=np.int64)
+    wts = _boost_weights(w.n_boost)
+    for l in range(w.L):
+        z = g.standard_normal(w.V, dtype=np.float32)
+        if w.temperature:
+            t = np.float32(g.uniform(0.5, 1.5))
+            z = z / t
+        ids = g.choice(w.V, size=w.n_boost, replace=False)
+        z[ids] += wts
+        boost_ids[l] = ids
+        out[l] = bf16_from_f32(z)
+    return out, boost_ids
+
+
+def _depth_targets(w: Workload, rnd: int, b: int, attempt: int, boost_ids: np.ndarray) -> np.ndarray:
+    """Per-depth target tokens [L + 1] of one sequence.
+
+    Entry j is the token the (synthetic) target model wants at draft depth j+1:
+    the argmax of a second seeded bf16 logit row that boosts the same ids as
+    the drafter row, with their ranks perturbed by adjacent swaps (p = 0.3).
+    Entry L (the bonus after a fully accepted chain) is uniform over V.
+    """
+    g = _rng(w, rnd, b, attempt, 1)
+    wts = _boost_weights(w.n_boost)
+    tgt = np.empty(w.L + 1, dtype=np.int32)
+    for l in range(w.L):
+        z = g.standard_normal(w.V, dtype=np.float32)
+        perm = np.arange(w.n_boost)
+        swaps = g.random(w.n_boost - 1) < 0.3
+        for i in range(w.n_boost - 1):
+            if swaps[i]:
+                perm[i], perm[i + 1] = perm[i + 1], perm[i]
+        z[boost_ids[l][perm]] += wts
+        zb = f32_from_bf16(bf16_from_f32(z))
+        tgt[l] = int(np.argmax(zb))       # first maximum: ties go to the lower id
+    tgt[w.L] = int(g.integers(0, w.V))
+    return tgt
+
+
+def hist_ring_init(w: Workload, rnd: int = 0, attempts=None) -> np.ndarray:
+    """Initial acceptance-history window [batch, HIST_WINDOW], entries ~ U{0..16}."""
+    out = np.empty((w.batch, HIST_WINDOW), dtype=np.int32)
+    for b in range(w.batch):
+        a = 0 if attempts is None else int(attempts[b])
+        out[b] = _rng(w, rnd, b, a, 2).integers(0, 17, size=HIST_WINDOW)
+    return out
+
+
+def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = True,
+              seqs=None) -> dict:
+    """All per-round inputs for the batch (numpy, host memory).
+
+    attempts[b] selects the re-draw index of sequence b (default 0).  seqs, if
+    given, restricts generation to those sequence indices (others left zero);
+    useful when only a sample of a large batch is compared against the oracle.
+    """
+    B = w.batch
+    attempts = np.zeros(B, dtype=np.int64) if attempts is None else np.asarray(attempts)
+    seqs = range(B) if seqs is None else seqs
+    logits = np.zeros((B, w.L, w.V), dtype=np.uint16)
+    boost = np.zeros((B, w.L, w.n_boost), dtype=np.int64)
+    root = np.zeros(B, dtype=np.int32)
+    prefix = np.zeros(B, dtype=np.int32)
+    tdepth = np.zeros((B, w.L + 1), dtype=np.int32)
+    ring = hist_ring_init(w, rnd, attempts)
+    for b in seqs:
+        a = int(attempts[b])
+        logits[b], boost[b] = gen_sequence_logits(w, rnd, b, a)
+        g = _rng(w, rnd, b, a, 3)
+        root[b] = g.integers(0, w.V)
+        prefix[b] = g.integers(64, 4097)
+        if with_targets and w.targets == "depth":
+            tdepth[b] = _depth_targets(w, rnd, b, a, boost[b])
+    hist = ring.astype(np.float64).mean(axis=1).astype(np.float32)
+    out = dict(logits=logits, boost_ids=boost, root_token=root, prefix_len=prefix,
+               base_pos=(prefix - 1).astype(np.int32), hist=hist, hist_ring=ring,
+               attempts=attempts)
+    if w.budget_mode == "fixed":
+        out["fixed_budget"] = np.full(B, w.fixed_budget, dtype=np.int32)
+    if w.targets == "depth":
+        out["target_depth"] = tdepth
+    return out
+
+
+def gen_scorer(w: Workload, mode: str = "literal") -> dict:
+    """Edge-scorer parameters.
+
+    literal: the benchmark stand-in score log q(c) + e_p^T W e_c with W = U V^T,
+      U, V in R^{d x rank} ~ N(0, 0.05^2), embeddings E in R^{V x d} ~ N(0, 0.1^2).
+      Expressed as the bi-tower with g_p = U, g_c = V, scale = sqrt(m), no depth
+      embedding, beta = 1 and no centering.
+    paper: the same projections with a depth embedding u ~ N(0, 0.05^2) [L, m],
+      scale 1.5, beta = 0.2 and centering on.
+    """
+    g = np.random.default_rng([w.seed, w.wid, 77])
+    emb = (g.standard_normal((w.V, w.emb_dim), dtype=np.float32) * np.float32(0.1))
+    U = (g.standard_normal((w.emb_dim, w.rank), dtype=np.float32) * np.float32(0.05))
+    Vm = (g.standard_normal((w.emb_dim, w.rank), dtype=np.float32) * np.float32(0.05))
+    u = (g.standard_normal((w.L, w.rank), dtype=np.float32) * np.float32(0.05))
+    if mode == "literal":
+        return dict(emb=emb, g_parent=U, g_child=Vm, depth_emb=None,
+                    scale=float(np.float32(math.sqrt(w.rank))), beta=1.0, center=0)
+    if mode == "paper":
+        return dict(emb=emb, g_parent=U, g_child=Vm, depth_emb=u,
+                    scale=1.5, beta=0.2, center=1)
+    raise ValueError(mode)
+
+
+def saba_params(w: Workload) -> dict:
+    """SABA constants: utility (1 - exp(-B/tau)) / (c0 + c1 B + c2 B prefix),
+    tau = max(phi . [1, conf, ent, hist], tau_min)."""
+    return dict(grid=np.asarray(w.grid, dtype=np.int32), phi=np.asarray(w.phi, dtype=np.float32),
+                tau_min=1.0, c0=1.0, c1=float(w.c1), c2=float(w.c2))
+
+
+# ---------------------------------------------------------------------------
+# Synthetic verifier for per-node targets (workload 4).
+#
+# The target model's greedy token after a draft node is replaced by a
+# counter-based draw keyed on the node's identity (sequence, depth, parent
+# token, token).  splitmix64 is Steele, Lea and Flood's published mixer
+# ("Fast splittable pseudorandom number generators", OOPSLA 2014).  With
+# probability 0.8 (an integer threshold on 24 hash bits) the target is the
+# drafter's candidate of geometric(1/2) rank at the next depth; otherwise, and
+# always at depth L, it is a hash of the identity modulo V.
+# ---------------------------------------------------------------------------
+
+_M64 = (1 << 64) - 1
+NODE_TARGET_P_NUM = 13421773      # round(0.8 * 2**24)
+
+
+def splitmix64(x):
+    x = np.asarray(x, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        z = x + np.uint64(0x9E3779B97F4A7C15)
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+def node_targets(seed: int, b, depth, parent_tok, tok, topk_ids_seq, V: int, L: int, K: int):
+    """Target token of each node (vectorised over nodes of one sequence).
+
+    depth: 0 for the root, 1..L for draft nodes.  parent_tok is -1 for the root
+    and for depth-1 nodes' parent use the root token.  topk_ids_seq [L, K] holds
+    the drafter candidates (rank order) of this sequence.
+    """
+    depth = np.asarray(depth, dtype=np.int64)
+    enc = lambda t: (np.asarray(t, dtype=np.int64) + 1).astype(np.uint64)
+    h = splitmix64(np.uint64(seed))
+    h = splitmix64(h ^ np.uint64(b))
+    h = splitmix64(h ^ depth.astype(np.uint64))
+    h = splitmix64(h ^ enc(parent_tok))
+    h = splitmix64(h ^ enc(tok))
+    pick = (splitmix64(h ^ np.uint64(1)) >> np.uint64(40)) < np.uint64(NODE_TARGET_P_NUM)
+    h2 = splitmix64(h ^ np.uint64(2))
+    # count trailing zeros of h2 (64 when zero), capped at K-1
+    r = np.zeros(h2.shape, dtype=np.int64)
+    x = h2.copy()
+    alive = np.ones(h2.shape, dtype=bool)
+    for i in range(min(K - 1, 64)):
+        bit = (x & np.uint64(1)) == np.uint64(0)
+        alive &= bit
+        r += alive
+        x = x >> np.uint64(1)
+    r = np.minimum(r, K - 1)
+    h3 = splitmix64(h ^ np.uint64(3))
+    hashed = (h3 % np.uint64(V)).astype(np.int64)
+    topk = np.asarray(topk_ids_seq)
+    nd = np.minimum(depth, L - 1)
+    from_cand = topk[nd, r]
+    use = pick & (depth < L)
+    return np.where(use, from_cand, hashed).astype(np.int32)
