@@ -1,0 +1,229 @@
+/*
+ * graft.h -- C ABI of the MI355X (gfx950) implementation of GRAFT's per-round
+ * draft-tree construction (arXiv 2608.20375).
+ *
+ * One decoding round of a diffusion-LM drafter (DFlash) gives, for every
+ * future depth d = 1..L, a full-vocabulary distribution q_{t,d} (the paper's
+ * Preliminaries, "DFlash one-pass marginals").  graft_build_tree turns the
+ * drafter logits of a batch of independent sequences into draft trees:
+ *
+ *   1. log-softmax statistics and the top-K candidate tokens of every depth
+ *      (candidates = highest-probability tokens per position, DDTree paragraph);
+ *   2. TDES edge scores of every parent -> child candidate pair between
+ *      consecutive depths (Sec. "Target-Distilled Edge Scoring", eqs.
+ *      tdes-score, tdes-center, tdes-bitower);
+ *   3. the SABA budget B_t of every sequence (Sec. "State-Aware Budget
+ *      Allocation", eqs. saba-objective, saba-gain, saba-cost);
+ *   4. budgeted best-first selection of candidate prefixes ranked by their
+ *      path score (DDTree paragraph and eq. ddtree-path-score; TDES
+ *      "Inference", eq. tdes-path-score);
+ *   5. emission of token ids, parent indices, depth position ids and the
+ *      ancestor tree-attention mask (Preliminaries, tree-based speculative
+ *      decoding).
+ * graft_accept then performs the greedy acceptance walk against the target
+ * model's tokens (same paragraph: commit the longest accepted draft path).
+ *
+ * Conventions
+ *   - Every pointer is DEVICE memory unless its comment says (host).
+ *   - Calls that take a stream enqueue work on it and return without
+ *     synchronizing, except where stated.  All calls of one context must be
+ *     ordered (one stream at a time); there is no internal locking.
+ *   - The library never keeps a caller pointer past stream-ordered use.
+ *   - Return values are graft_status codes.  Host-side validation happens
+ *     before anything is enqueued: on an error the outputs are untouched and
+ *     graft_last_error() (thread-local) describes it.  Nothing is thrown.
+ *
+ * Semantics fixed where the paper is silent (the CPU oracle uses the same):
+ *   - The root (last committed token) is implicit: it is neither a node nor a
+ *     mask row/column, and the budget counts draft nodes only.  A tree holds
+ *     N = min(B_t, max_nodes, number of distinct prefixes) nodes.
+ *   - Depth-1 edges have the root token as parent; every parent's children
+ *     set C_{p,d} is all K candidates of depth d.
+ *   - Prefix order (the heap order): higher path score, then smaller depth,
+ *     then the lexicographically smaller token-id path from the root.  Path
+ *     scores are fp64 sums, root to leaf, of fp32 edge scores.
+ *   - Candidates of a depth are ordered by (logit descending, token id
+ *     ascending); logits must be finite.
+ *   - Nodes are numbered canonically: depth ascending, then token-id path
+ *     lexicographically ascending.  parents[i] < i; parents[i] = -1 marks a
+ *     child of the root.  pos_ids[i] = base_pos + depth(i).
+ *   - mask row i has bit j set iff node j is node i or an ancestor of it;
+ *     bit j of row i is bit (j & 63) of word (j >> 6).
+ *   - acc_len counts accepted draft nodes and excludes the bonus token.
+ */
+#ifndef GRAFT_H
+#define GRAFT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define GRAFT_API __attribute__((visibility("default")))
+#else
+#define GRAFT_API
+#endif
+
+/* Same type as HIP's hipStream_t; NULL is the default stream. */
+typedef struct ihipStream_t *graft_stream_t;
+
+typedef enum {
+    GRAFT_OK = 0,
+    GRAFT_ERR_INVALID_ARG = 1,   /* NULL where required, bad sizes, unsorted grid ... */
+    GRAFT_ERR_UNSUPPORTED = 2,   /* a size beyond the limits below */
+    GRAFT_ERR_OUT_OF_MEMORY = 3,
+    GRAFT_ERR_HIP = 4,           /* a HIP runtime call or launch failed */
+    GRAFT_ERR_DEVICE_DATA = 5    /* graft_get_device_status: kernels saw invalid data */
+} graft_status;
+
+typedef struct graft_ctx graft_ctx;
+
+/* Problem sizes fixed for the life of a context. */
+typedef struct {
+    int32_t max_batch;   /* sequences per call, >= 1 */
+    int32_t num_pos;     /* L: drafter block depth, 1..64 */
+    int32_t vocab;       /* V: vocabulary size, >= top_k */
+    int32_t top_k;       /* K: candidates per depth, 1..64 */
+    int32_t max_nodes;   /* N_max: tree capacity, 1..1024 (mask row = ceil(N_max/64) words) */
+    int32_t hist_window; /* w: acceptance-history window of the device ring, 1..64 (0 -> 4) */
+} graft_dims;
+
+/* TDES scorer, eq. tdes-bitower:
+ *   f(p,c,d) = scale * (g_p(e_p) + u_d)^T (g_c(e_c) + u_d) / sqrt(score_dim),
+ * g_p(e) = e^T g_parent, g_c(e) = e^T g_child (row-major, fp32);
+ * edge score = log q_d(c) + beta * f~ where f~ is f minus its mean over the
+ * K children of the same parent when center != 0 (eq. tdes-center), else f.
+ * The benchmark stand-in score log q(c) + e_p^T U V^T e_c is
+ * {emb, U, V, NULL, E, rank, sqrt(rank), 1, 0}. */
+typedef struct {
+    const float *emb;        /* [vocab, emb_dim] frozen token embeddings */
+    const float *g_parent;   /* [emb_dim, score_dim] */
+    const float *g_child;    /* [emb_dim, score_dim] */
+    const float *depth_emb;  /* [num_pos, score_dim] u_d, or NULL for u = 0 */
+    int32_t emb_dim;         /* E >= 1 */
+    int32_t score_dim;       /* m, 1..64 */
+    float scale;             /* s */
+    float beta;              /* residual strength (the paper's default is 0.2) */
+    int32_t center;          /* nonzero: subtract the per-parent mean */
+} graft_scorer_desc;
+
+/* SABA, eqs. saba-objective/gain/cost (host memory; copied into the context):
+ *   tau = max(phi[0] + phi[1] conf + phi[2] ent + phi[3] hist, tau_min)
+ *   U(B) = (1 - exp(-B / tau)) / (c0 + c1 B + c2 B prefix)
+ *   B_t = the smallest budget of the grid with the largest U.
+ * conf = mean over depths of the top-1 probability, ent = mean per-depth
+ * entropy (standing in for the representation-degeneration signal, which
+ * needs drafter hidden states), hist = mean accepted length over the window. */
+typedef struct {
+    const int32_t *budgets;  /* (host) strictly ascending, each in 1..max_nodes */
+    int32_t n_budgets;       /* 1..64 */
+    float phi[4];
+    float tau_min;           /* > 0 */
+    float c0, c1, c2;
+} graft_saba_desc;
+
+/* Per-round inputs. */
+typedef struct {
+    int32_t batch;               /* 1..max_batch */
+    const uint16_t *logits;      /* [batch, L, V] bf16 bit patterns, contiguous,
+                                    16-byte aligned base; finite values */
+    const int32_t *root_token;   /* [batch] last committed token, in [0, V) */
+    const int32_t *base_pos;     /* [batch] position id of the root */
+    const int32_t *prefix_len;   /* [batch] prefix_t of eq. saba-cost, or NULL (0) */
+    const float *hist;           /* [batch] hist_t, or NULL: mean of the context's ring */
+    const int32_t *fixed_budget; /* [batch] fixed budgets (DDTree-style), or NULL: SABA */
+} graft_round_in;
+
+/* Per-round outputs, caller-allocated.  Required: budget, n_nodes, tokens,
+ * parents, pos_ids.  Every other field may be NULL. */
+typedef struct {
+    int32_t *budget;        /* [batch] B_t */
+    int32_t *n_nodes;       /* [batch] N */
+    int32_t *tokens;        /* [batch, max_nodes] canonical order, -1 padded */
+    int32_t *parents;       /* [batch, max_nodes] -1 for root children and padding */
+    int32_t *pos_ids;       /* [batch, max_nodes] -1 padded */
+    uint64_t *mask;         /* [batch, max_nodes, ceil(max_nodes/64)] zero padded */
+    int32_t *topk_ids;      /* [batch, L, K] candidates, rank order */
+    float *topk_logq;       /* [batch, L, K] log q of the candidates */
+    float *row_lse;         /* [batch, L] log-sum-exp of each logit row */
+    float *row_maxprob;     /* [batch, L] top-1 probability */
+    float *row_entropy;     /* [batch, L] entropy of q */
+    float *edge_scores;     /* [batch, L, K, K] [depth-1][parent rank][child rank];
+                               depth 1 uses parent row 0 only (others 0) */
+    double *node_scores;    /* [batch, max_nodes] path score of each node, 0 padded */
+    float *saba_state;      /* [batch, 4] conf, ent, hist, tau (tau = 0 for fixed budgets) */
+} graft_tree_out;
+
+/* Targets of the acceptance walk: exactly one of target_node / target_depth.
+ *   per-node:  target(root) = target_root[b], target(node i) = target_node[b, i]
+ *   per-depth: target(node at depth l) = target_depth[b, l], l = 0 (root) .. L */
+typedef struct {
+    const int32_t *target_root;   /* [batch] (per-node mode) */
+    const int32_t *target_node;   /* [batch, max_nodes] or NULL */
+    const int32_t *target_depth;  /* [batch, L + 1] or NULL */
+} graft_targets;
+
+/* Creates a context and allocates its workspace for `dims` (synchronous). */
+GRAFT_API int graft_create(const graft_dims *dims /* host */, graft_ctx **out /* host */);
+
+/* Destroys the context after synchronizing the device; NULL is a no-op. */
+GRAFT_API void graft_destroy(graft_ctx *ctx);
+
+/* Installs a TDES scorer: computes the cached projections g_p(e), g_c(e) of
+ * every token once (the paper notes they depend only on the token id), on
+ * `stream`.  The descriptor's arrays must stay valid until that work is done.
+ * Must be called before the first graft_build_tree. */
+GRAFT_API int graft_set_scorer(graft_ctx *ctx, const graft_scorer_desc *desc /* host */,
+                     graft_stream_t stream);
+
+/* Installs SABA parameters (host only, no device work). */
+GRAFT_API int graft_set_saba(graft_ctx *ctx, const graft_saba_desc *desc /* host */);
+
+/* Fills the device acceptance-history ring: init[b, i], i < hist_window,
+ * are the accepted lengths of the previous rounds of sequence b. */
+GRAFT_API int graft_set_history(graft_ctx *ctx, int32_t batch, const int32_t *init, graft_stream_t stream);
+
+/* One round of draft-tree construction for the batch (steps 1-5 above). */
+GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host */,
+                     const graft_tree_out *out /* host */, graft_stream_t stream);
+
+/* Greedy acceptance walk over the trees of the batch.
+ *   n_nodes [batch], tokens/parents [batch, max_nodes] as written by
+ *   graft_build_tree; acc_len [batch], acc_nodes [batch, L] (canonical node
+ *   indices along the accepted path, -1 padded) and bonus [batch] (the target
+ *   token after the last accepted node) are written.  With update_history
+ *   nonzero, acc_len is pushed into the context's history ring. */
+GRAFT_API int graft_accept(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes, const int32_t *tokens,
+                 const int32_t *parents, const graft_targets *targets /* host */,
+                 int32_t *acc_len, int32_t *acc_nodes, int32_t *bonus,
+                 int32_t update_history, graft_stream_t stream);
+
+/* Synchronizes `stream` and reports data errors the kernels detected since
+ * the last call (token ids outside [0, V), for example): GRAFT_OK or
+ * GRAFT_ERR_DEVICE_DATA; the flag is then cleared. */
+GRAFT_API int graft_get_device_status(graft_ctx *ctx, graft_stream_t stream);
+
+/* Synthetic stand-in for the target model, for tests and benchmarks only: the
+ * per-node targets of a counter-based draw keyed on each node's identity
+ * (sequence, depth, parent token, token) with splitmix64.  With probability
+ * 0.8 (24 hash bits under 13421773) the target is the candidate of
+ * geometric(1/2) rank (capped at K-1) at the next depth, else, and always at
+ * depth L, the identity hash modulo V.  topk_ids [batch, L, K] are the
+ * candidates of the round; target_root [batch], target_node [batch, max_nodes]
+ * are written (-1 padded). */
+GRAFT_API int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t seed,
+                             const int32_t *root_token, const int32_t *n_nodes,
+                             const int32_t *tokens, const int32_t *parents,
+                             const int32_t *topk_ids, int32_t *target_root,
+                             int32_t *target_node, graft_stream_t stream);
+
+GRAFT_API const char *graft_status_string(int status);
+GRAFT_API const char *graft_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRAFT_H */

@@ -1,0 +1,258 @@
+"""Python binding of libgraft (include/graft.h): argument marshalling only.
+
+Every step of GRAFT's per-round draft-tree construction runs in the HIP
+kernels of libgraft.so; this module passes torch tensors' device pointers and
+the current HIP stream through ctypes.  If the library is not built, importing
+works but creating a Context raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+__all__ = ["Context", "TreeBuffers", "lib", "library_path", "GraftError", "EXPORTED_SYMBOLS"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libgraft.so")
+_lib = None
+
+EXPORTED_SYMBOLS = (
+    "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
+    "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
+    "graft_status_string", "graft_last_error",
+)
+
+
+class GraftError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        L = lib()
+        super().__init__("%s: %s (%s)" % (where, L.graft_status_string(status).decode(),
+                                          L.graft_last_error().decode()))
+
+
+class Dims(C.Structure):
+    _fields_ = [("max_batch", C.c_int32), ("num_pos", C.c_int32), ("vocab", C.c_int32),
+                ("top_k", C.c_int32), ("max_nodes", C.c_int32), ("hist_window", C.c_int32)]
+
+
+class ScorerDesc(C.Structure):
+    _fields_ = [("emb", C.c_void_p), ("g_parent", C.c_void_p), ("g_child", C.c_void_p),
+                ("depth_emb", C.c_void_p), ("emb_dim", C.c_int32), ("score_dim", C.c_int32),
+                ("scale", C.c_float), ("beta", C.c_float), ("center", C.c_int32)]
+
+
+class SabaDesc(C.Structure):
+    _fields_ = [("budgets", C.c_void_p), ("n_budgets", C.c_int32), ("phi", C.c_float * 4),
+                ("tau_min", C.c_float), ("c0", C.c_float), ("c1", C.c_float), ("c2", C.c_float)]
+
+
+class RoundIn(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("logits", C.c_void_p), ("root_token", C.c_void_p),
+                ("base_pos", C.c_void_p), ("prefix_len", C.c_void_p), ("hist", C.c_void_p),
+                ("fixed_budget", C.c_void_p)]
+
+
+class TreeOut(C.Structure):
+    _fields_ = [("budget", C.c_void_p), ("n_nodes", C.c_void_p), ("tokens", C.c_void_p),
+                ("parents", C.c_void_p), ("pos_ids", C.c_void_p), ("mask", C.c_void_p),
+                ("topk_ids", C.c_void_p), ("topk_logq", C.c_void_p), ("row_lse", C.c_void_p),
+                ("row_maxprob", C.c_void_p), ("row_entropy", C.c_void_p),
+                ("edge_scores", C.c_void_p), ("node_scores", C.c_void_p),
+                ("saba_state", C.c_void_p)]
+
+
+class Targets(C.Structure):
+    _fields_ = [("target_root", C.c_void_p), ("target_node", C.c_void_p),
+                ("target_depth", C.c_void_p)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """The loaded libgraft.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError("libgraft.so is not built (python -m paper_2608_20375_amd.build); "
+                               "this package has no non-HIP path")
+        L = C.CDLL(_LIB_PATH)
+        vp, i32 = C.c_void_p, C.c_int32
+        L.graft_create.argtypes = [C.POINTER(Dims), C.POINTER(vp)]
+        L.graft_destroy.argtypes = [vp]
+        L.graft_destroy.restype = None
+        L.graft_set_scorer.argtypes = [vp, C.POINTER(ScorerDesc), vp]
+        L.graft_set_saba.argtypes = [vp, C.POINTER(SabaDesc)]
+        L.graft_set_history.argtypes = [vp, i32, vp, vp]
+        L.graft_build_tree.argtypes = [vp, C.POINTER(RoundIn), C.POINTER(TreeOut), vp]
+        L.graft_accept.argtypes = [vp, i32, vp, vp, vp, C.POINTER(Targets), vp, vp, vp, i32, vp]
+        L.graft_get_device_status.argtypes = [vp, vp]
+        L.graft_synth_node_targets.argtypes = [vp, i32, C.c_uint64, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.graft_status_string.argtypes = [C.c_int]
+        L.graft_status_string.restype = C.c_char_p
+        L.graft_last_error.argtypes = []
+        L.graft_last_error.restype = C.c_char_p
+        for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
+                  "graft_build_tree", "graft_accept", "graft_get_device_status",
+                  "graft_synth_node_targets"):
+            getattr(L, n).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(t, dtype=None, name="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise GraftError(status, where)
+
+
+class TreeBuffers:
+    """Preallocated outputs of one build_tree call (torch tensors on the device)."""
+
+    def __init__(self, ctx: "Context", batch: int, mask=True, topk=True, stats=True, edges=False,
+                 node_scores=True, saba_state=True, device=None):
+        d = ctx.dims
+        dev = device or torch.device("cuda", torch.cuda.current_device())
+        L, K, N = d.num_pos, d.top_k, d.max_nodes
+        W = (N + 63) // 64
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.batch = batch
+        self.budget = torch.empty(batch, **i32)
+        self.n_nodes = torch.empty(batch, **i32)
+        self.tokens = torch.empty(batch, N, **i32)
+        self.parents = torch.empty(batch, N, **i32)
+        self.pos_ids = torch.empty(batch, N, **i32)
+        # uint64 words of the ancestor bitset, held as int64 (same bits)
+        self.mask = torch.empty(batch, N, W, dtype=torch.int64, device=dev) if mask else None
+        self.topk_ids = torch.empty(batch, L, K, **i32) if topk else None
+        self.topk_logq = torch.empty(batch, L, K, **f32) if topk else None
+        self.row_lse = torch.empty(batch, L, **f32) if stats else None
+        self.row_maxprob = torch.empty(batch, L, **f32) if stats else None
+        self.row_entropy = torch.empty(batch, L, **f32) if stats else None
+        self.edge_scores = torch.empty(batch, L, K, K, **f32) if edges else None
+        self.node_scores = (torch.empty(batch, N, dtype=torch.float64, device=dev)
+                            if node_scores else None)
+        self.saba_state = torch.empty(batch, 4, **f32) if saba_state else None
+        t = TreeOut()
+        for name, _ in TreeOut._fields_:
+            setattr(t, name, _ptr(getattr(self, name), name=name))
+        self._struct = t
+
+    def as_dict(self) -> dict:
+        return {n: getattr(self, n) for n, _ in TreeOut._fields_ if getattr(self, n) is not None}
+
+
+class Context:
+    """A graft_ctx: sizes fixed at creation, workspace owned by the library."""
+
+    def __init__(self, max_batch: int, num_pos: int, vocab: int, top_k: int, max_nodes: int,
+                 hist_window: int = 4):
+        L = lib()
+        self.dims = Dims(max_batch, num_pos, vocab, top_k, max_nodes, hist_window)
+        h = C.c_void_p()
+        _check(L.graft_create(C.byref(self.dims), C.byref(h)), "graft_create")
+        self._h = h
+        self._keep = []
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().graft_destroy(self._h)
+            self._h = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_scorer(self, emb, g_parent, g_child, depth_emb=None, scale=1.0, beta=1.0, center=0):
+        d = ScorerDesc(_ptr(emb, torch.float32, "emb"), _ptr(g_parent, torch.float32, "g_parent"),
+                       _ptr(g_child, torch.float32, "g_child"),
+                       _ptr(depth_emb, torch.float32, "depth_emb"), emb.shape[1],
+                       g_parent.shape[1], float(scale), float(beta), int(center))
+        self._keep = [emb, g_parent, g_child, depth_emb]
+        _check(lib().graft_set_scorer(self._h, C.byref(d), _stream()), "graft_set_scorer")
+
+    def set_saba(self, budgets, phi, tau_min=1.0, c0=1.0, c1=0.0, c2=0.0):
+        arr = (C.c_int32 * len(budgets))(*[int(b) for b in budgets])
+        d = SabaDesc(C.cast(arr, C.c_void_p), len(budgets), (C.c_float * 4)(*map(float, phi)),
+                     float(tau_min), float(c0), float(c1), float(c2))
+        _check(lib().graft_set_saba(self._h, C.byref(d)), "graft_set_saba")
+
+    def set_history(self, init):
+        _check(lib().graft_set_history(self._h, init.shape[0], _ptr(init, torch.int32, "init"),
+                                       _stream()), "graft_set_history")
+
+    def build_tree(self, logits, root_token, base_pos, prefix_len=None, hist=None,
+                   fixed_budget=None, out: TreeBuffers | None = None, **want) -> TreeBuffers:
+        batch = logits.shape[0]
+        if out is None:
+            out = TreeBuffers(self, batch, **want)
+        r = RoundIn(batch, _ptr(logits, None, "logits"), _ptr(root_token, torch.int32, "root_token"),
+                    _ptr(base_pos, torch.int32, "base_pos"),
+                    _ptr(prefix_len, torch.int32, "prefix_len"), _ptr(hist, torch.float32, "hist"),
+                    _ptr(fixed_budget, torch.int32, "fixed_budget"))
+        if logits.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+            raise TypeError("logits must hold bf16 bit patterns")
+        _check(lib().graft_build_tree(self._h, C.byref(r), C.byref(out._struct), _stream()),
+               "graft_build_tree")
+        return out
+
+    def accept(self, n_nodes, tokens, parents, target_root=None, target_node=None,
+               target_depth=None, update_history=False, acc_len=None, acc_nodes=None, bonus=None):
+        batch = n_nodes.shape[0]
+        dev = n_nodes.device
+        acc_len = torch.empty(batch, dtype=torch.int32, device=dev) if acc_len is None else acc_len
+        acc_nodes = (torch.empty(batch, self.dims.num_pos, dtype=torch.int32, device=dev)
+                     if acc_nodes is None else acc_nodes)
+        bonus = torch.empty(batch, dtype=torch.int32, device=dev) if bonus is None else bonus
+        t = Targets(_ptr(target_root, torch.int32, "target_root"),
+                    _ptr(target_node, torch.int32, "target_node"),
+                    _ptr(target_depth, torch.int32, "target_depth"))
+        _check(lib().graft_accept(self._h, batch, _ptr(n_nodes, torch.int32, "n_nodes"),
+                                  _ptr(tokens, torch.int32, "tokens"),
+                                  _ptr(parents, torch.int32, "parents"), C.byref(t),
+                                  _ptr(acc_len, torch.int32, "acc_len"),
+                                  _ptr(acc_nodes, torch.int32, "acc_nodes"),
+                                  _ptr(bonus, torch.int32, "bonus"), int(bool(update_history)),
+                                  _stream()), "graft_accept")
+        return acc_len, acc_nodes, bonus
+
+    def synth_node_targets(self, seed, root_token, n_nodes, tokens, parents, topk_ids,
+                           target_root=None, target_node=None):
+        batch = n_nodes.shape[0]
+        dev = n_nodes.device
+        if target_root is None:
+            target_root = torch.empty(batch, dtype=torch.int32, device=dev)
+        if target_node is None:
+            target_node = torch.empty(batch, self.dims.max_nodes, dtype=torch.int32, device=dev)
+        _check(lib().graft_synth_node_targets(
+            self._h, batch, C.c_uint64(int(seed) & ((1 << 64) - 1)),
+            _ptr(root_token, torch.int32, "root_token"), _ptr(n_nodes, torch.int32, "n_nodes"),
+            _ptr(tokens, torch.int32, "tokens"), _ptr(parents, torch.int32, "parents"),
+            _ptr(topk_ids, torch.int32, "topk_ids"), _ptr(target_root, torch.int32, "target_root"),
+            _ptr(target_node, torch.int32, "target_node"), _stream()), "graft_synth_node_targets")
+        return target_root, target_node
+
+    def device_status(self) -> int:
+        return lib().graft_get_device_status(self._h, _stream())

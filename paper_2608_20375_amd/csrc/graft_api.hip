@@ -1,0 +1,318 @@
+// graft_api.hip -- host side of the C ABI declared in include/graft.h:
+// validation, context and workspace ownership, kernel launches on the
+// caller's stream.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "graft_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+  return fail(GRAFT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+template <typename T>
+hipError_t dalloc(T **p, size_t n) {
+  *p = nullptr;
+  if (n == 0) n = 1;
+  return hipMalloc(reinterpret_cast<void **>(p), n * sizeof(T));
+}
+
+void free_ctx(graft_ctx *c) {
+  if (!c) return;
+  (void)hipFree(c->part_stats);
+  (void)hipFree(c->part_keys);
+  (void)hipFree(c->row_counters);
+  (void)hipFree(c->topk_ids);
+  (void)hipFree(c->topk_logq);
+  (void)hipFree(c->row_stats);
+  (void)hipFree(c->sorted_score);
+  (void)hipFree(c->sorted_child);
+  (void)hipFree(c->sel_nodes);
+  (void)hipFree(c->sel_scores);
+  (void)hipFree(c->heap);
+  (void)hipFree(c->proj_parent);
+  (void)hipFree(c->proj_child);
+  (void)hipFree(c->depth_emb);
+  (void)hipFree(c->hist_ring);
+  (void)hipFree(c->hist_pos);
+  (void)hipFree(c->error_flag);
+  delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *graft_status_string(int s) {
+  switch (s) {
+    case GRAFT_OK: return "ok";
+    case GRAFT_ERR_INVALID_ARG: return "invalid argument";
+    case GRAFT_ERR_UNSUPPORTED: return "unsupported size";
+    case GRAFT_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case GRAFT_ERR_HIP: return "HIP runtime error";
+    case GRAFT_ERR_DEVICE_DATA: return "invalid data seen on the device";
+    default: return "unknown status";
+  }
+}
+
+const char *graft_last_error(void) { return g_err; }
+
+int graft_create(const graft_dims *dims, graft_ctx **out) {
+  if (!dims || !out) return fail(GRAFT_ERR_INVALID_ARG, "graft_create: NULL argument");
+  *out = nullptr;
+  graft_dims d = *dims;
+  if (d.hist_window == 0) d.hist_window = 4;
+  if (d.max_batch < 1 || d.num_pos < 1 || d.vocab < 1 || d.top_k < 1 || d.max_nodes < 1 ||
+      d.hist_window < 1)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_create: sizes must be positive");
+  if (d.num_pos > graft::kMaxL)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_create: num_pos %d > %d", d.num_pos, graft::kMaxL);
+  if (d.top_k > graft::kMaxK)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_create: top_k %d > %d", d.top_k, graft::kMaxK);
+  if (d.top_k > d.vocab)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_create: top_k %d > vocab %d", d.top_k, d.vocab);
+  if (d.max_nodes > graft::kMaxNodes)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_create: max_nodes %d > %d", d.max_nodes,
+                graft::kMaxNodes);
+  if (d.hist_window > 64)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_create: hist_window %d > 64", d.hist_window);
+  if (static_cast<int64_t>(d.max_batch) * d.num_pos > (1 << 24))
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_create: max_batch * num_pos too large");
+
+  graft_ctx *c = new (std::nothrow) graft_ctx();
+  if (!c) return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_create: host allocation failed");
+  c->dims = d;
+  (void)hipGetDevice(&c->device);
+  const size_t B = d.max_batch, L = d.num_pos, K = d.top_k, N = d.max_nodes;
+  c->part_slots = graft::logits_part_slots(d);
+  hipError_t e = hipSuccess;
+#define GRAFT_ALLOC(ptr, n)              \
+  if (e == hipSuccess) e = dalloc(&(ptr), (n));
+  GRAFT_ALLOC(c->part_stats, static_cast<size_t>(c->part_slots) * 3);
+  GRAFT_ALLOC(c->part_keys, static_cast<size_t>(c->part_slots) * K);
+  GRAFT_ALLOC(c->row_counters, B * L);
+  GRAFT_ALLOC(c->topk_ids, B * L * K);
+  GRAFT_ALLOC(c->topk_logq, B * L * K);
+  GRAFT_ALLOC(c->row_stats, B * L * 3);
+  GRAFT_ALLOC(c->sorted_score, B * L * K * K);
+  GRAFT_ALLOC(c->sorted_child, B * L * K * K);
+  GRAFT_ALLOC(c->sel_nodes, B * N);
+  GRAFT_ALLOC(c->sel_scores, B * N);
+  GRAFT_ALLOC(c->heap, B * (N + 1));
+  GRAFT_ALLOC(c->hist_ring, B * d.hist_window);
+  GRAFT_ALLOC(c->hist_pos, B);
+  GRAFT_ALLOC(c->error_flag, 1);
+#undef GRAFT_ALLOC
+  if (e == hipSuccess) e = hipMemset(c->row_counters, 0, B * L * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(c->error_flag, 0, sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(c->hist_ring, 0, B * d.hist_window * sizeof(int32_t));
+  if (e == hipSuccess) e = hipMemset(c->hist_pos, 0, B * sizeof(int32_t));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    free_ctx(c);
+    return e == hipErrorOutOfMemory ? fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_create: %s",
+                                           hipGetErrorString(e))
+                                    : hip_fail(e, "graft_create");
+  }
+  *out = c;
+  return GRAFT_OK;
+}
+
+void graft_destroy(graft_ctx *ctx) {
+  if (!ctx) return;
+  (void)hipDeviceSynchronize();
+  free_ctx(ctx);
+}
+
+int graft_set_scorer(graft_ctx *ctx, const graft_scorer_desc *desc, graft_stream_t stream) {
+  if (!ctx || !desc) return fail(GRAFT_ERR_INVALID_ARG, "graft_set_scorer: NULL argument");
+  if (!desc->emb || !desc->g_parent || !desc->g_child)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_scorer: emb, g_parent and g_child are required");
+  if (desc->emb_dim < 1 || desc->score_dim < 1)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_scorer: emb_dim and score_dim must be positive");
+  if (desc->score_dim > graft::kMaxScoreDim)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_set_scorer: score_dim %d > %d", desc->score_dim,
+                graft::kMaxScoreDim);
+  if (!std::isfinite(desc->scale) || !std::isfinite(desc->beta))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_scorer: scale and beta must be finite");
+  const size_t V = ctx->dims.vocab, m = desc->score_dim, L = ctx->dims.num_pos;
+  hipError_t e = hipSuccess;
+  if (ctx->scorer.score_dim != desc->score_dim || !ctx->proj_parent) {
+    (void)hipStreamSynchronize(reinterpret_cast<hipStream_t>(stream));
+    (void)hipFree(ctx->proj_parent);
+    (void)hipFree(ctx->proj_child);
+    (void)hipFree(ctx->depth_emb);
+    ctx->proj_parent = ctx->proj_child = ctx->depth_emb = nullptr;
+    ctx->has_scorer = false;
+    e = dalloc(&ctx->proj_parent, V * m);
+    if (e == hipSuccess) e = dalloc(&ctx->proj_child, V * m);
+    if (e == hipSuccess) e = dalloc(&ctx->depth_emb, L * m);
+    if (e != hipSuccess) return hip_fail(e, "graft_set_scorer: allocation");
+  }
+  ctx->scorer.scale = desc->scale;
+  ctx->scorer.beta = desc->beta;
+  ctx->scorer.center = desc->center != 0;
+  ctx->scorer.score_dim = desc->score_dim;
+  ctx->scorer.has_depth_emb = desc->depth_emb != nullptr;
+  if (desc->depth_emb) {
+    e = hipMemcpyAsync(ctx->depth_emb, desc->depth_emb, L * m * sizeof(float),
+                       hipMemcpyDeviceToDevice, stream);
+    if (e != hipSuccess) return hip_fail(e, "graft_set_scorer: depth embedding copy");
+  }
+  e = graft::launch_projection(ctx, desc, stream);
+  if (e != hipSuccess) return hip_fail(e, "graft_set_scorer: projection launch");
+  ctx->has_scorer = true;
+  return GRAFT_OK;
+}
+
+int graft_set_saba(graft_ctx *ctx, const graft_saba_desc *desc) {
+  if (!ctx || !desc || !desc->budgets)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_saba: NULL argument");
+  if (desc->n_budgets < 1 || desc->n_budgets > graft::kMaxGrid)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_set_saba: n_budgets must be in 1..%d",
+                graft::kMaxGrid);
+  for (int i = 0; i < desc->n_budgets; ++i) {
+    const int v = desc->budgets[i];
+    if (v < 1 || v > ctx->dims.max_nodes)
+      return fail(GRAFT_ERR_INVALID_ARG, "graft_set_saba: budget %d outside 1..max_nodes", v);
+    if (i > 0 && v <= desc->budgets[i - 1])
+      return fail(GRAFT_ERR_INVALID_ARG, "graft_set_saba: budgets must be strictly ascending");
+  }
+  if (!(desc->tau_min > 0.f) || !std::isfinite(desc->tau_min))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_saba: tau_min must be positive and finite");
+  for (int i = 0; i < 4; ++i)
+    if (!std::isfinite(desc->phi[i]))
+      return fail(GRAFT_ERR_INVALID_ARG, "graft_set_saba: phi must be finite");
+  if (!std::isfinite(desc->c0) || !std::isfinite(desc->c1) || !std::isfinite(desc->c2))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_saba: cost coefficients must be finite");
+  graft::SabaParams p{};
+  for (int i = 0; i < desc->n_budgets; ++i) p.grid[i] = desc->budgets[i];
+  p.n_grid = desc->n_budgets;
+  for (int i = 0; i < 4; ++i) p.phi[i] = desc->phi[i];
+  p.tau_min = desc->tau_min;
+  p.c0 = desc->c0;
+  p.c1 = desc->c1;
+  p.c2 = desc->c2;
+  ctx->saba = p;
+  ctx->has_saba = true;
+  return GRAFT_OK;
+}
+
+int graft_set_history(graft_ctx *ctx, int32_t batch, const int32_t *init, graft_stream_t stream) {
+  if (!ctx || !init) return fail(GRAFT_ERR_INVALID_ARG, "graft_set_history: NULL argument");
+  if (batch < 1 || batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_set_history: batch %d outside 1..%d", batch,
+                ctx->dims.max_batch);
+  hipError_t e = graft::launch_set_history(ctx, batch, init, stream);
+  if (e != hipSuccess) return hip_fail(e, "graft_set_history");
+  ctx->has_history = true;
+  return GRAFT_OK;
+}
+
+int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+                     graft_stream_t stream) {
+  if (!ctx || !in || !out) return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: NULL argument");
+  const graft_dims &d = ctx->dims;
+  if (in->batch < 1 || in->batch > d.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: batch %d outside 1..%d", in->batch,
+                d.max_batch);
+  if (!in->logits || !in->root_token || !in->base_pos)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: logits, root_token and base_pos are required");
+  if ((reinterpret_cast<uintptr_t>(in->logits) & 15u) != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: logits must be 16-byte aligned");
+  if (!out->budget || !out->n_nodes || !out->tokens || !out->parents || !out->pos_ids)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "graft_build_tree: budget, n_nodes, tokens, parents and pos_ids are required");
+  if (!ctx->has_scorer)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: no scorer installed (graft_set_scorer)");
+  if (!in->fixed_budget && !ctx->has_saba)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "graft_build_tree: no fixed budgets and no SABA parameters (graft_set_saba)");
+  if (!in->hist && !in->fixed_budget && !ctx->has_history)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "graft_build_tree: no hist input and no history ring (graft_set_history)");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = graft::launch_logits_pass(ctx, in->batch, in->logits, out, s);
+  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: logits pass");
+  e = graft::launch_edge_scores(ctx, in->batch, in->root_token, out->edge_scores, s);
+  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: edge scores");
+  e = graft::launch_select(ctx, in, out, s);
+  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: selection");
+  return GRAFT_OK;
+}
+
+int graft_accept(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes, const int32_t *tokens,
+                 const int32_t *parents, const graft_targets *targets, int32_t *acc_len,
+                 int32_t *acc_nodes, int32_t *bonus, int32_t update_history,
+                 graft_stream_t stream) {
+  if (!ctx || !targets || !n_nodes || !tokens || !parents || !acc_len || !acc_nodes || !bonus)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_accept: NULL argument");
+  if (batch < 1 || batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_accept: batch %d outside 1..%d", batch,
+                ctx->dims.max_batch);
+  const bool per_node = targets->target_node != nullptr;
+  const bool per_depth = targets->target_depth != nullptr;
+  if (per_node == per_depth)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "graft_accept: give exactly one of target_node and target_depth");
+  if (per_node && !targets->target_root)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_accept: per-node targets need target_root");
+  if (update_history && !ctx->has_history)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_accept: no history ring (graft_set_history)");
+  hipError_t e = graft::launch_accept(ctx, batch, n_nodes, tokens, parents, targets, acc_len,
+                                      acc_nodes, bonus, update_history,
+                                      reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graft_accept");
+  return GRAFT_OK;
+}
+
+int graft_get_device_status(graft_ctx *ctx, graft_stream_t stream) {
+  if (!ctx) return fail(GRAFT_ERR_INVALID_ARG, "graft_get_device_status: NULL context");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint32_t flag = 0;
+  hipError_t e = hipMemcpyAsync(&flag, ctx->error_flag, sizeof flag, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "graft_get_device_status");
+  if (flag) {
+    e = hipMemsetAsync(ctx->error_flag, 0, sizeof flag, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "graft_get_device_status: clear");
+    return fail(GRAFT_ERR_DEVICE_DATA, "kernels saw invalid data (flags 0x%x)", flag);
+  }
+  return GRAFT_OK;
+}
+
+int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t seed,
+                             const int32_t *root_token, const int32_t *n_nodes,
+                             const int32_t *tokens, const int32_t *parents,
+                             const int32_t *topk_ids, int32_t *target_root, int32_t *target_node,
+                             graft_stream_t stream) {
+  if (!ctx || !root_token || !n_nodes || !tokens || !parents || !topk_ids || !target_root ||
+      !target_node)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_synth_node_targets: NULL argument");
+  if (batch < 1 || batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_synth_node_targets: batch %d outside 1..%d", batch,
+                ctx->dims.max_batch);
+  hipError_t e = graft::launch_synth_targets(ctx, batch, seed, root_token, n_nodes, tokens,
+                                             parents, topk_ids, target_root, target_node,
+                                             reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graft_synth_node_targets");
+  return GRAFT_OK;
+}
+
+}  // extern "C"

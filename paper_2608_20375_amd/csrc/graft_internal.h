@@ -1,0 +1,186 @@
+// graft_internal.h -- internal declarations of the HIP library (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/graft.h"
+
+namespace graft {
+
+constexpr int kWave = 64;
+constexpr int kMaxL = 64;
+constexpr int kMaxK = 64;
+constexpr int kMaxNodes = 1024;
+constexpr int kMaxGrid = 64;
+constexpr int kMaxScoreDim = 64;
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+
+// Order-preserving map of an fp32 value to an unsigned key (NaN sorts below -inf
+// for the negative-NaN pattern and above +inf otherwise; logits are finite).
+__device__ __forceinline__ uint32_t ordered_f32(float x) {
+  uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float unordered_f32(uint32_t k) {
+  uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+  return __uint_as_float(u);
+}
+// Candidate key: larger = earlier in (logit desc, id asc).  0 = empty slot.
+__device__ __forceinline__ uint64_t cand_key(float x, uint32_t id) {
+  return (static_cast<uint64_t>(ordered_f32(x)) << 32) | static_cast<uint64_t>(~id);
+}
+__device__ __forceinline__ float cand_value(uint64_t k) {
+  return unordered_f32(static_cast<uint32_t>(k >> 32));
+}
+__device__ __forceinline__ int32_t cand_id(uint64_t k) {
+  return static_cast<int32_t>(~static_cast<uint32_t>(k));
+}
+// Order-preserving map of an fp64 value to an unsigned key.
+__device__ __forceinline__ uint64_t ordered_f64(double x) {
+  uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+  return (u & 0x8000000000000000ull) ? ~u : (u | 0x8000000000000000ull);
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  uint32_t lo = static_cast<uint32_t>(v), hi = static_cast<uint32_t>(v >> 32);
+  lo = __shfl_xor(lo, m);
+  hi = __shfl_xor(hi, m);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ double shfl_xor_f64(double v, int m) {
+  return __longlong_as_double(static_cast<long long>(
+      shfl_xor_u64(static_cast<uint64_t>(__double_as_longlong(v)), m)));
+}
+
+// Rank of this lane among the set lanes of `mask` below it.
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
+}
+
+// Bitonic sort of 64*E keys held by one wave, element index i = e*64 + lane;
+// afterwards the keys are in descending order of i.
+template <int E>
+__device__ __forceinline__ void wave_sort_desc(uint64_t (&k)[E]) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int size = 2; size <= 64 * E; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride >= 64) {
+        const int es = stride / 64;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          if ((e & es) == 0) {
+            const int p = e | es;
+            const int lo = e * 64 + lane;
+            const bool desc = (lo & size) == 0;
+            const uint64_t a = k[e], b = k[p];
+            const bool sw = desc ? (a < b) : (a > b);
+            k[e] = sw ? b : a;
+            k[p] = sw ? a : b;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const uint64_t o = shfl_xor_u64(k[e], stride);
+          const int i = e * 64 + lane;
+          const bool lower = (lane & stride) == 0;
+          const bool desc = (i & size) == 0;
+          const uint64_t mx = k[e] > o ? k[e] : o;
+          const uint64_t mn = k[e] > o ? o : k[e];
+          k[e] = (lower == desc) ? mx : mn;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Context
+// ---------------------------------------------------------------------------
+
+struct SabaParams {
+  int32_t grid[kMaxGrid];
+  int32_t n_grid;
+  float phi[4];
+  float tau_min, c0, c1, c2;
+};
+
+struct ScorerParams {
+  float scale, beta;
+  int32_t center;
+  int32_t score_dim;
+  int32_t has_depth_emb;
+};
+
+}  // namespace graft
+
+struct graft_ctx {
+  graft_dims dims;
+  int device;
+  // K1 split-row partials
+  int32_t part_slots;
+  double *part_stats;      // [part_slots][3]: mL (log2-scaled max), S, T2
+  uint64_t *part_keys;     // [part_slots][K]
+  uint32_t *row_counters;  // [max_batch * L], zero between launches
+  // per-round intermediates
+  int32_t *topk_ids;       // [max_batch, L, K]
+  float *topk_logq;        // [max_batch, L, K]
+  float *row_stats;        // [max_batch, L, 3]: lse, maxprob, entropy
+  float *sorted_score;     // [max_batch, L, K, K] children of each parent by rank
+  uint8_t *sorted_child;   // [max_batch, L, K, K]
+  // selection scratch
+  int32_t *sel_nodes;      // [max_batch, max_nodes] packed node records
+  double *sel_scores;      // [max_batch, max_nodes]
+  int64_t *heap;           // [max_batch, max_nodes + 1] frontier of the serial selector
+  // scorer
+  float *proj_parent;      // [V, m]
+  float *proj_child;       // [V, m]
+  float *depth_emb;        // [L, m] or nullptr
+  graft::ScorerParams scorer;
+  bool has_scorer;
+  graft::SabaParams saba;
+  bool has_saba;
+  // history ring
+  int32_t *hist_ring;      // [max_batch, window]
+  int32_t *hist_pos;       // [max_batch]
+  bool has_history;
+  // device-side data-error flag
+  uint32_t *error_flag;
+};
+
+namespace graft {
+
+// Launchers (stream-ordered, no synchronization).  They return hipError_t.
+hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
+                              const graft_tree_out *out, hipStream_t stream);
+hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStream_t stream);
+hipError_t launch_edge_scores(graft_ctx *ctx, int batch, const int32_t *root_token,
+                              float *edge_out, hipStream_t stream);
+hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+                         hipStream_t stream);
+hipError_t launch_accept(graft_ctx *ctx, int batch, const int32_t *n_nodes,
+                         const int32_t *tokens, const int32_t *parents,
+                         const graft_targets *t, int32_t *acc_len, int32_t *acc_nodes,
+                         int32_t *bonus, int update_history, hipStream_t stream);
+hipError_t launch_set_history(graft_ctx *ctx, int batch, const int32_t *init,
+                              hipStream_t stream);
+hipError_t launch_synth_targets(graft_ctx *ctx, int batch, uint64_t seed,
+                                const int32_t *root_token, const int32_t *n_nodes,
+                                const int32_t *tokens, const int32_t *parents,
+                                const int32_t *topk_ids, int32_t *target_root,
+                                int32_t *target_node, hipStream_t stream);
+
+// Number of splits per row used by the logits pass for a given row count.
+int logits_splits(const graft_dims &d, int rows);
+int logits_part_slots(const graft_dims &d);
+
+}  // namespace graft

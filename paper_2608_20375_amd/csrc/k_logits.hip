@@ -1,0 +1,480 @@
+// k_logits.hip -- the logits pass: log-softmax statistics and top-K candidates
+// of every drafter row q_{t,d} (the paper's Preliminaries, "DFlash one-pass
+// marginals"; candidates = the highest-probability tokens of each position, as
+// in the DDTree paragraph; conf_t of the SABA decoding state uses the top-1
+// probability).
+//
+// One pass over the bf16 logits, HBM-bound.  Each workgroup (4 waves) streams
+// one chunk of a row with 16-byte loads, 4 loads in flight per lane.  Per lane
+// it keeps an online softmax in log2 units: offset mL (fp32, = max * log2 e),
+// S = sum 2^y and T2 = sum 2^y * y with y = x * log2 e - mL, accumulated per
+// tile in fp32 and across tiles in fp64.  Top-K: every wave keeps a threshold
+// (the K-th best value it has buffered); a tile whose maximum falls below it
+// costs nothing more, otherwise its passing elements are appended to a per-wave
+// LDS buffer with ballot/mbcnt and the buffer is compacted by a wave bitonic
+// sort of (value desc, id asc) keys when full.  Rows split over several
+// workgroups are merged by the last workgroup of the row (atomic counter,
+// reset by that workgroup).
+#include "graft_internal.h"
+
+namespace graft {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kUnroll = 4;                        // 16-byte loads per lane per tile
+constexpr int kTileVec = kWave * kUnroll;         // 256 vectors = 2048 elements
+constexpr float kL2E = 1.44269504088896340736f;
+constexpr double kLn2 = 0.693147180559945309417232121458;
+constexpr double kLog2e = 1.44269504088896340735992468100;
+constexpr float kNegBig = -1e30f;                 // finite stand-in for -inf
+constexpr int kTargetBlocks = 2048;
+constexpr int kMinSplitVec = 512;                 // >= 4096 elements per split
+
+struct LaneStats {
+  float mx;      // largest logit seen
+  float mL;      // fp32 offset actually used: fl(mx * log2 e)
+  double S;      // sum 2^(x*log2e - mL)
+  double T2;     // sum 2^y * y
+};
+
+__device__ __forceinline__ void stats_init(LaneStats &s) {
+  s.mx = kNegBig;
+  s.mL = kNegBig * kL2E;
+  s.S = 0.0;
+  s.T2 = 0.0;
+}
+
+// Moves the offset to a larger maximum (rescales S and T2 exactly in fp64).
+__device__ __forceinline__ void stats_raise(LaneStats &s, float new_mx) {
+  if (new_mx > s.mx) {
+    const float nL = new_mx * kL2E;
+    const double d = static_cast<double>(s.mL) - static_cast<double>(nL);
+    const double a = exp2(d);
+    s.T2 = a * (s.T2 + d * s.S);
+    s.S = a * s.S;
+    s.mL = nL;
+    s.mx = new_mx;
+  }
+}
+
+template <int CAP>
+struct WaveBuf {
+  uint64_t *buf;   // LDS [CAP]
+  int count;       // wave-uniform
+  float thr;       // wave-uniform: a candidate needs value >= thr
+};
+
+// Sort the buffer, keep the best K, raise the threshold to the K-th value.
+template <int CAP>
+__device__ __forceinline__ void wave_compact(WaveBuf<CAP> &w, int K) {
+  constexpr int E = CAP / kWave;
+  const int lane = lane_id();
+  uint64_t k[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kWave + lane;
+    k[e] = (i < w.count) ? w.buf[i] : 0ull;
+  }
+  wave_sort_desc<E>(k);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kWave + lane;
+    if (i < K) w.buf[i] = k[e];
+  }
+  w.count = w.count < K ? w.count : K;
+  if (w.count >= K) {
+    const int src_e = (K - 1) / kWave, src_l = (K - 1) % kWave;
+    uint64_t kth = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (e == src_e) kth = k[e];
+    const uint32_t hi = __shfl(static_cast<uint32_t>(kth >> 32), src_l);
+    const float t = unordered_f32(hi);
+    w.thr = t > w.thr ? t : w.thr;
+  }
+}
+
+// Offers one value per lane (valid lanes only) to the wave's buffer.
+template <int CAP>
+__device__ __forceinline__ void wave_offer(WaveBuf<CAP> &w, int K, float v, uint32_t id,
+                                           bool valid) {
+  bool pass = valid && v >= w.thr;
+  uint64_t m = __ballot(pass);
+  if (m == 0) return;
+  int n = __popcll(m);
+  if (w.count + n > CAP) {
+    wave_compact<CAP>(w, K);
+    pass = valid && v >= w.thr;
+    m = __ballot(pass);
+    if (m == 0) return;
+    n = __popcll(m);
+  }
+  if (pass) w.buf[w.count + lanes_below(m)] = cand_key(v, id);
+  w.count += n;
+}
+
+// Offers a 64-bit key per lane (used when merging already-sorted lists).
+template <int CAP>
+__device__ __forceinline__ void wave_offer_key(WaveBuf<CAP> &w, int K, uint64_t key) {
+  const float v = cand_value(key);
+  bool pass = key != 0ull && v >= w.thr;
+  uint64_t m = __ballot(pass);
+  if (m == 0) return;
+  int n = __popcll(m);
+  if (w.count + n > CAP) {
+    wave_compact<CAP>(w, K);
+    pass = key != 0ull && v >= w.thr;
+    m = __ballot(pass);
+    if (m == 0) return;
+    n = __popcll(m);
+  }
+  if (pass) w.buf[w.count + lanes_below(m)] = key;
+  w.count += n;
+}
+
+__device__ __forceinline__ void unpack8(const uint4 q, float (&v)[8]) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+
+// One tile: lane handles vectors vbase + u*64 + lane, u < kUnroll.
+template <int CAP, bool MASKED>
+__device__ __forceinline__ void process_tile(const uint4 *__restrict__ vec, int64_t tile_vec,
+                                             int64_t n_vec, int64_t elem0, LaneStats &st,
+                                             WaveBuf<CAP> &w, int K) {
+  const int lane = lane_id();
+  float v[kUnroll][8];
+  bool ok[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int64_t vi = tile_vec + u * kWave + lane;
+    ok[u] = !MASKED || vi < n_vec;
+    uint4 q = make_uint4(0, 0, 0, 0);
+    if (ok[u]) q = vec[vi];
+    unpack8(q, v[u]);
+    if (MASKED && !ok[u]) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[u][e] = kNegBig;
+    }
+  }
+  float sub[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    float a = fmaxf(fmaxf(v[u][0], v[u][1]), fmaxf(v[u][2], v[u][3]));
+    float b = fmaxf(fmaxf(v[u][4], v[u][5]), fmaxf(v[u][6], v[u][7]));
+    sub[u] = fmaxf(a, b);
+  }
+  const float tmax = fmaxf(fmaxf(sub[0], sub[1]), fmaxf(sub[2], sub[3]));
+
+  // top-K candidates
+  if (__ballot(tmax >= w.thr) != 0ull) {
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (__ballot(ok[u] && sub[u] >= w.thr) != 0ull) {
+        const int64_t id0 = elem0 + (tile_vec + u * kWave + lane) * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          wave_offer<CAP>(w, K, v[u][e], static_cast<uint32_t>(id0 + e), ok[u]);
+      }
+    }
+  }
+
+  // softmax statistics
+  stats_raise(st, tmax);
+  const float mL = st.mL;
+  float s[kUnroll], t[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    s[u] = 0.f;
+    t[u] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float y = __builtin_fmaf(v[u][e], kL2E, -mL);
+      float ex = __builtin_amdgcn_exp2f(y);
+      if (MASKED) ex = ok[u] ? ex : 0.f;
+      s[u] += ex;
+      t[u] = __builtin_fmaf(ex, y, t[u]);
+    }
+  }
+  st.S += static_cast<double>((s[0] + s[1]) + (s[2] + s[3]));
+  st.T2 += static_cast<double>((t[0] + t[1]) + (t[2] + t[3]));
+}
+
+// Scalar elements of a row that fall outside its 16-byte aligned body.
+template <int CAP>
+__device__ __forceinline__ void process_scalar(const uint16_t *__restrict__ row, int64_t idx,
+                                               bool valid, LaneStats &st, WaveBuf<CAP> &w,
+                                               int K) {
+  float x = kNegBig;
+  if (valid) x = __uint_as_float(static_cast<uint32_t>(row[idx]) << 16);
+  wave_offer<CAP>(w, K, x, static_cast<uint32_t>(idx), valid);
+  stats_raise(st, x);
+  if (valid) {
+    const float y = __builtin_fmaf(x, kL2E, -st.mL);
+    const float ex = __builtin_amdgcn_exp2f(y);
+    st.S += static_cast<double>(ex);
+    st.T2 += static_cast<double>(ex * y);
+  }
+}
+
+// Wave reduction of the per-lane statistics into lane-uniform values.
+__device__ __forceinline__ void stats_wave_reduce(LaneStats &st) {
+  float mx = st.mx;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  stats_raise(st, mx);          // every lane now uses the same offset
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    st.S += shfl_xor_f64(st.S, o);
+    st.T2 += shfl_xor_f64(st.T2, o);
+  }
+}
+
+// Merges (mL, S, T2) triples given with different offsets.
+__device__ __forceinline__ void stats_merge(double &mL, double &S, double &T2, double mL2,
+                                            double S2, double T22) {
+  const double M = mL > mL2 ? mL : mL2;
+  const double d1 = mL - M, d2 = mL2 - M;
+  const double a1 = exp2(d1), a2 = exp2(d2);
+  T2 = a1 * (T2 + d1 * S) + a2 * (T22 + d2 * S2);
+  S = a1 * S + a2 * S2;
+  mL = M;
+}
+
+struct RowOut {
+  int32_t *ids;      // workspace [rows, K]
+  float *logq;       // workspace [rows, K]
+  float *stats;      // workspace [rows, 3]
+  int32_t *o_ids;    // optional caller outputs
+  float *o_logq, *o_lse, *o_maxprob, *o_ent;
+};
+
+// Final results of a row from merged statistics and the sorted top-K (wave 0).
+template <int CAP>
+__device__ __forceinline__ void write_row(const RowOut &o, int64_t row, int K, double mL,
+                                          double S, double T2, const uint64_t *top) {
+  const int lane = lane_id();
+  const double lse2 = mL + log2(S);
+  const double lse = lse2 * kLn2;
+  const double mx = static_cast<double>(cand_value(top[0]));
+  for (int r = lane; r < K; r += kWave) {
+    const uint64_t key = top[r];
+    const int32_t id = key ? cand_id(key) : -1;
+    const float lq = key ? static_cast<float>(static_cast<double>(cand_value(key)) - lse)
+                         : -INFINITY;
+    o.ids[row * K + r] = id;
+    o.logq[row * K + r] = lq;
+    if (o.o_ids) o.o_ids[row * K + r] = id;
+    if (o.o_logq) o.o_logq[row * K + r] = lq;
+  }
+  if (lane == 0) {
+    const float f_lse = static_cast<float>(lse);
+    const float f_mp = static_cast<float>(exp2(mx * kLog2e - lse2));
+    const float f_ent = static_cast<float>(log(S) - kLn2 * T2 / S);
+    o.stats[row * 3 + 0] = f_lse;
+    o.stats[row * 3 + 1] = f_mp;
+    o.stats[row * 3 + 2] = f_ent;
+    if (o.o_lse) o.o_lse[row] = f_lse;
+    if (o.o_maxprob) o.o_maxprob[row] = f_mp;
+    if (o.o_ent) o.o_ent[row] = f_ent;
+  }
+}
+
+template <int CAP>
+__global__ void __launch_bounds__(kThreads)
+logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, int K,
+                   double *__restrict__ part_stats, uint64_t *__restrict__ part_keys,
+                   uint32_t *__restrict__ counters, RowOut out) {
+  __shared__ uint64_t s_buf[kWaves][CAP];
+  __shared__ double s_stats[kWaves][3];
+
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int64_t row = blockIdx.x / splits;
+  const int split = blockIdx.x % splits;
+
+  const uint16_t *rowp = logits + row * V;
+  // 16-byte aligned body of the row: elements [a0, a0 + 8 * nv_row)
+  const int64_t abs0 = row * V;
+  int64_t a0 = (8 - (abs0 & 7)) & 7;
+  if (a0 > V) a0 = V;
+  const int64_t nv_row = (V - a0) / 8;
+  const int64_t per = (nv_row + splits - 1) / splits;
+  const int64_t v_begin = per * split < nv_row ? per * split : nv_row;
+  const int64_t v_end = v_begin + per < nv_row ? v_begin + per : nv_row;
+  const int64_t n_vec = v_end - v_begin;
+  const uint4 *vec = reinterpret_cast<const uint4 *>(rowp + a0) + v_begin;
+  const int64_t elem0 = a0 + v_begin * 8;   // element id of vec[0]
+
+  LaneStats st;
+  stats_init(st);
+  WaveBuf<CAP> w{s_buf[wave], 0, -INFINITY};
+
+  // Tiles interleaved over the waves of the block.
+  const int64_t n_full = n_vec / kTileVec;
+  int64_t t = wave;
+  if (t < n_full) {
+    // First tile: threshold = K-th largest lane maximum of the tile is a valid
+    // lower bound of the K-th largest element; take it before offering.
+    {
+      float tm = kNegBig;
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        float vv[8];
+        unpack8(vec[t * kTileVec + u * kWave + lane], vv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) tm = fmaxf(tm, vv[e]);
+      }
+      if (K <= kWave) {
+        uint64_t k1[1] = {cand_key(tm, lane)};
+        wave_sort_desc<1>(k1);
+        const uint32_t hi = __shfl(static_cast<uint32_t>(k1[0] >> 32), K - 1);
+        w.thr = unordered_f32(hi);
+      }
+    }
+    for (; t < n_full; t += kWaves)
+      process_tile<CAP, false>(vec, t * kTileVec, n_vec, elem0, st, w, K);
+  }
+  if (t == n_full && n_full * kTileVec < n_vec)
+    process_tile<CAP, true>(vec, t * kTileVec, n_vec, elem0, st, w, K);
+  // Misaligned head [0, a0) and tail [a0 + 8 nv_row, V): split 0, wave 0.
+  if (split == 0 && wave == 0) {
+    const int64_t tail0 = a0 + 8 * nv_row;
+    const int64_t n_head = a0, n_tail = V - tail0;
+    if (n_head + n_tail > 0) {
+      const bool valid = lane < n_head + n_tail;
+      const int64_t idx = lane < n_head ? lane : tail0 + (lane - n_head);
+      process_scalar<CAP>(rowp, valid ? idx : 0, valid, st, w, K);
+    }
+  }
+
+  wave_compact<CAP>(w, K);
+  stats_wave_reduce(st);
+  if (lane == 0) {
+    s_stats[wave][0] = static_cast<double>(st.mL);
+    s_stats[wave][1] = st.S;
+    s_stats[wave][2] = st.T2;
+  }
+  // clear the unused tail of each wave's top-K list
+  for (int i = w.count + lane; i < K; i += kWave) s_buf[wave][i] = 0ull;
+  __syncthreads();
+
+  if (wave != 0) return;
+
+  // Block merge in wave 0: statistics and the 4 waves' top-K lists.
+  double mL = s_stats[0][0], S = s_stats[0][1], T2 = s_stats[0][2];
+  for (int i = 1; i < kWaves; ++i) stats_merge(mL, S, T2, s_stats[i][0], s_stats[i][1], s_stats[i][2]);
+  constexpr int E = CAP / kWave;
+  {
+    uint64_t k[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = e * kWave + lane;   // i = wave * K + rank
+      k[e] = (i < kWaves * K) ? s_buf[i / K][i % K] : 0ull;
+    }
+    wave_sort_desc<E>(k);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = e * kWave + lane;
+      if (i < K) s_buf[0][i] = k[e];
+    }
+  }
+
+  if (splits == 1) {
+    write_row<CAP>(out, row, K, mL, S, T2, s_buf[0]);
+    return;
+  }
+
+  // Split row: publish the partial, the last block of the row merges.
+  const int64_t slot = row * splits + split;
+  for (int i = lane; i < K; i += kWave) part_keys[slot * K + i] = s_buf[0][i];
+  if (lane == 0) {
+    part_stats[slot * 3 + 0] = mL;
+    part_stats[slot * 3 + 1] = S;
+    part_stats[slot * 3 + 2] = T2;
+  }
+  __threadfence();
+  uint32_t last = 0;
+  if (lane == 0) last = atomicAdd(&counters[row], 1u) == static_cast<uint32_t>(splits - 1);
+  last = __shfl(last, 0);
+  if (!last) return;
+  __threadfence();
+
+  const volatile double *ps = part_stats + row * splits * 3;
+  mL = ps[0];
+  S = ps[1];
+  T2 = ps[2];
+  for (int i = 1; i < splits; ++i) stats_merge(mL, S, T2, ps[3 * i], ps[3 * i + 1], ps[3 * i + 2]);
+  WaveBuf<CAP> m{s_buf[0], 0, -INFINITY};
+  const volatile uint64_t *pk = part_keys + row * splits * K;
+  const int total = splits * K;
+  for (int base = 0; base < total; base += kWave) {
+    const int i = base + lane;
+    const uint64_t key = i < total ? pk[i] : 0ull;
+    wave_offer_key<CAP>(m, K, key);
+  }
+  wave_compact<CAP>(m, K);
+  for (int i = m.count + lane; i < K; i += kWave) s_buf[0][i] = 0ull;
+  if (lane == 0) counters[row] = 0u;
+  write_row<CAP>(out, row, K, mL, S, T2, s_buf[0]);
+}
+
+}  // namespace
+
+int logits_splits(const graft_dims &d, int rows) {
+  const int64_t nv_row = d.vocab / 8;
+  int64_t max_s = nv_row / kMinSplitVec;
+  if (max_s < 1) max_s = 1;
+  int64_t s = (kTargetBlocks + rows - 1) / rows;
+  if (s > max_s) s = max_s;
+  if (s < 1) s = 1;
+  return static_cast<int>(s);
+}
+
+int logits_part_slots(const graft_dims &d) {
+  int64_t best = 0;
+  const int max_rows = d.max_batch * d.num_pos;
+  for (int b = 1; b <= d.max_batch; ++b) {
+    const int rows = b * d.num_pos;
+    const int s = logits_splits(d, rows);
+    if (s > 1 && static_cast<int64_t>(rows) * s > best) best = static_cast<int64_t>(rows) * s;
+  }
+  (void)max_rows;
+  return static_cast<int>(best > 0 ? best : 1);
+}
+
+hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
+                              const graft_tree_out *out, hipStream_t stream) {
+  const graft_dims &d = ctx->dims;
+  const int rows = batch * d.num_pos;
+  const int splits = logits_splits(d, rows);
+  if (splits > 1 && static_cast<int64_t>(rows) * splits > ctx->part_slots)
+    return hipErrorInvalidValue;
+  RowOut o;
+  o.ids = ctx->topk_ids;
+  o.logq = ctx->topk_logq;
+  o.stats = ctx->row_stats;
+  o.o_ids = out ? out->topk_ids : nullptr;
+  o.o_logq = out ? out->topk_logq : nullptr;
+  o.o_lse = out ? out->row_lse : nullptr;
+  o.o_maxprob = out ? out->row_maxprob : nullptr;
+  o.o_ent = out ? out->row_entropy : nullptr;
+  const dim3 grid(static_cast<unsigned>(rows * splits));
+  if (d.top_k <= 32) {
+    hipLaunchKernelGGL(logits_pass_kernel<128>, grid, dim3(kThreads), 0, stream, logits,
+                       static_cast<int64_t>(d.vocab), splits, d.top_k, ctx->part_stats,
+                       ctx->part_keys, ctx->row_counters, o);
+  } else {
+    hipLaunchKernelGGL(logits_pass_kernel<256>, grid, dim3(kThreads), 0, stream, logits,
+                       static_cast<int64_t>(d.vocab), splits, d.top_k, ctx->part_stats,
+                       ctx->part_keys, ctx->row_counters, o);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace graft

@@ -116,19 +116,15 @@ def _boost_weights(n: int) -> np.ndarray:
 def gen_sequence_logits(w: Workload, rnd: int, b: int, attempt: int = 0):
     """Drafter logits of one sequence: (bf16 bits [L, V], boosted ids [L, n_boost])."""
     g = _rng(w, rnd, b, attempt, 0)
-    out = np.empty((w.L, w.V), dtype=np.uint16)
-    boost_ids = np.empty((w.L, w.n_boost), dtype=np.int64)
+    z = g.standard_normal((w.L, w.V), dtype=np.float32)
+    if w.temperature:
+        t = g.uniform(0.5, 1.5, size=w.L).astype(np.float32)
+        z /= t[:, None]
+    boost_ids = np.stack([g.choice(w.V, size=w.n_boost, replace=False) for _ in range(w.L)])
     wts = _boost_weights(w.n_boost)
-    for l in range(w.L):
-        z = g.standard_normal(w.V, dtype=np.float32)
-        if w.temperature:
-            t = np.float32(g.uniform(0.5, 1.5))
-            z = z / t
-        ids = g.choice(w.V, size=w.n_boost, replace=False)
-        z[ids] += wts
-        boost_ids[l] = ids
-        out[l] = bf16_from_f32(z)
-    return out, boost_ids
+    rows = np.arange(w.L)[:, None]
+    z[rows, boost_ids] += wts[None, :]
+    return bf16_from_f32(z), boost_ids.astype(np.int64)
 
 
 def _depth_targets(w: Workload, rnd: int, b: int, attempt: int, boost_ids: np.ndarray) -> np.ndarray:
@@ -141,27 +137,29 @@ def _depth_targets(w: Workload, rnd: int, b: int, attempt: int, boost_ids: np.nd
     """
     g = _rng(w, rnd, b, attempt, 1)
     wts = _boost_weights(w.n_boost)
+    z = g.standard_normal((w.L, w.V), dtype=np.float32)
+    swaps = g.random((w.L, w.n_boost - 1)) < 0.3
     tgt = np.empty(w.L + 1, dtype=np.int32)
     for l in range(w.L):
-        z = g.standard_normal(w.V, dtype=np.float32)
         perm = np.arange(w.n_boost)
-        swaps = g.random(w.n_boost - 1) < 0.3
         for i in range(w.n_boost - 1):
-            if swaps[i]:
+            if swaps[l, i]:
                 perm[i], perm[i + 1] = perm[i + 1], perm[i]
-        z[boost_ids[l][perm]] += wts
-        zb = f32_from_bf16(bf16_from_f32(z))
-        tgt[l] = int(np.argmax(zb))       # first maximum: ties go to the lower id
+        z[l, boost_ids[l][perm]] += wts
+    zb = f32_from_bf16(bf16_from_f32(z))
+    tgt[:w.L] = np.argmax(zb, axis=1)          # first maximum: ties go to the lower id
     tgt[w.L] = int(g.integers(0, w.V))
     return tgt
 
 
 def hist_ring_init(w: Workload, rnd: int = 0, attempts=None) -> np.ndarray:
-    """Initial acceptance-history window [batch, HIST_WINDOW], entries ~ U{0..16}."""
+    """Initial acceptance-history window [batch, HIST_WINDOW]: the previous
+    accepted length a ~ U{0..16} of each sequence, repeated over the window so
+    that hist (the window mean) equals it."""
     out = np.empty((w.batch, HIST_WINDOW), dtype=np.int32)
     for b in range(w.batch):
         a = 0 if attempts is None else int(attempts[b])
-        out[b] = _rng(w, rnd, b, a, 2).integers(0, 17, size=HIST_WINDOW)
+        out[b] = _rng(w, rnd, b, a, 2).integers(0, 17)
     return out
 
 
@@ -182,7 +180,8 @@ def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = Tru
     prefix = np.zeros(B, dtype=np.int32)
     tdepth = np.zeros((B, w.L + 1), dtype=np.int32)
     ring = hist_ring_init(w, rnd, attempts)
-    for b in seqs:
+
+    def one(b):
         a = int(attempts[b])
         logits[b], boost[b] = gen_sequence_logits(w, rnd, b, a)
         g = _rng(w, rnd, b, a, 3)
@@ -190,6 +189,15 @@ def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = Tru
         prefix[b] = g.integers(64, 4097)
         if with_targets and w.targets == "depth":
             tdepth[b] = _depth_targets(w, rnd, b, a, boost[b])
+
+    seqs = list(seqs)
+    if len(seqs) > 1 and w.L * w.V * len(seqs) > (1 << 22):
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(min(8, len(seqs))) as ex:
+            list(ex.map(one, seqs))
+    else:
+        for b in seqs:
+            one(b)
     hist = ring.astype(np.float64).mean(axis=1).astype(np.float32)
     out = dict(logits=logits, boost_ids=boost, root_token=root, prefix_len=prefix,
                base_pos=(prefix - 1).astype(np.int32), hist=hist, hist_ring=ring,

@@ -1,0 +1,319 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bars: candidate ids, trees, masks, position ids, budgets and acceptance are
+bit-exact; log-probabilities, row statistics and edge scores agree with the
+fp64 oracle within 1e-5 relative (absolute floor 1e-6 for values near zero).
+End-to-end parity holds on sequences whose inputs were re-drawn until every
+floating-point decision has a margin of L * 2**-17 (see tests/workload.py);
+staged parity (the oracle selecting on the GPU's own fp32 edge scores and
+budget) is bit-exact on every sequence.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synthetic as S
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import workload as WL  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+RTOL, ATOL = 1e-5, 1e-6
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def close(gpu, ref, rtol=RTOL, atol=ATOL):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return np.abs(gpu - ref) <= atol + rtol * np.abs(ref)
+
+
+def check_tree_equal(g, b, r, n_max, words):
+    n = r["n_nodes"]
+    assert g["n_nodes"][b] == n
+    assert np.array_equal(g["tokens"][b], r["tokens"])
+    assert np.array_equal(g["parents"][b], r["parents"])
+    assert np.array_equal(g["pos_ids"][b], r["pos_ids"])
+    gm = g["mask"][b].view(np.uint64).reshape(n_max, words)
+    assert np.array_equal(gm, r["mask"])
+
+
+def staged_check(w, g, sc, sp, inp, seqs):
+    P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
+    words = (w.n_max + 63) // 64
+    for b in seqs:
+        st = oracle.select_staged(P, g["topk_ids"][b], g["edge_scores"][b], int(g["budget"][b]),
+                                  int(inp["base_pos"][b]))
+        check_tree_equal(g, b, st, w.n_max, words)
+        n = st["n_nodes"]
+        assert np.array_equal(g["node_scores"][b][:n], st["node_scores"][:n])
+
+
+def saba_check(w, g, sc, sp, inp, seqs):
+    if sp is None:
+        assert np.array_equal(g["budget"], inp["fixed_budget"])
+        return
+    P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
+    for b in seqs:
+        conf = sum(float(v) for v in g["row_maxprob"][b]) / w.L
+        ent = sum(float(v) for v in g["row_entropy"][b]) / w.L
+        bud, tau, rel, _ = oracle.saba(P, conf, ent, float(inp["hist"][b]), int(inp["prefix_len"][b]))
+        if rel > 1e-12:
+            assert bud == g["budget"][b], (b, bud, g["budget"][b], rel)
+
+
+def end_to_end_check(w, g, inp, results):
+    words = (w.n_max + 63) // 64
+    for b, r in results.items():
+        assert np.array_equal(g["topk_ids"][b], r["topk_ids"]), b
+        assert close(g["topk_logq"][b], r["topk_logq"]).all(), b
+        assert close(g["row_lse"][b], r["row_lse"]).all(), b
+        assert close(g["row_maxprob"][b], r["row_maxprob"]).all(), b
+        assert close(g["row_entropy"][b], r["row_entropy"]).all(), b
+        for l in range(w.L):
+            rows = 1 if l == 0 else w.K
+            assert close(g["edge_scores"][b, l, :rows], r["edge"][l, :rows]).all(), (b, l)
+        assert g["budget"][b] == r["budget"], b
+        check_tree_equal(g, b, r, w.n_max, words)
+        n = r["n_nodes"]
+        assert close(g["node_scores"][b][:n], r["node_scores"][:n], rtol=1e-6).all()
+
+
+# ---------------------------------------------------------------------------
+# logits pass on shapes that exercise tiles, splits and ragged rows
+# ---------------------------------------------------------------------------
+
+SHAPES = [
+    # batch, L, V, K
+    (1, 3, 40, 32),        # a row shorter than one tile, K close to V
+    (2, 4, 777, 8),        # V % 8 != 0: misaligned rows, scalar head/tail
+    (1, 2, 5003, 16),      # several tiles + ragged tail, split rows
+    (3, 5, 20000, 4),
+    (2, 3, 70001, 64),     # K = 64 (the 256-entry buffer variant)
+    (4, 2, 9, 1),          # K = 1: DFlash's argmax draft
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_logits_pass_topk_and_stats(shape):
+    B, L, V, K = shape
+    _say("logits pass", shape)
+    w = S.workload(0, batch=B, L=L, V=V, K=K, n_max=64, fixed_budget=8)
+    inp = S.gen_round(w, with_targets=False)
+    # many exact ties among tail values: quantise part of the rows
+    g = np.random.default_rng(V)
+    x = S.f32_from_bf16(inp["logits"])
+    q = np.round(x * 4) / 4
+    x = np.where(g.random(x.shape) < 0.5, q, x)
+    inp["logits"] = S.bf16_from_f32(x)
+    sc = WL.scorer_inputs(w, "literal")
+    ctx = WL.gpu_context(w, sc, None, torch)
+    gr = WL.gpu_round(ctx, w, inp, torch)
+    for b in range(B):
+        for l in range(L):
+            row = inp["logits"][b, l]
+            ids, xv = oracle.topk(row, K)
+            lse, mp, h = oracle.row_stats(row)
+            assert np.array_equal(gr["topk_ids"][b, l], ids), (b, l)
+            assert close(gr["topk_logq"][b, l], xv - lse).all()
+            assert close(gr["row_lse"][b, l], lse)
+            assert close(gr["row_maxprob"][b, l], mp)
+            assert close(gr["row_entropy"][b, l], h)
+    ctx.close()
+
+
+# ---------------------------------------------------------------------------
+# whole round, every workload (full sizes; oracle on audited sequences)
+# ---------------------------------------------------------------------------
+
+AUDIT = {0: None, 1: None, 2: None, 3: [0, 17, 40, 63], 4: [0, 77, 127]}
+
+
+@pytest.mark.parametrize("wid", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("mode", ["literal", "paper"])
+def test_round_parity(wid, mode):
+    w = S.workload(wid)
+    _say("round parity workload", wid, mode)
+    inp, sc, sp, results = WL.audited_round(w, 0, mode, seqs=AUDIT[wid])
+    _say("  inputs ready; attempts", inp["attempts"][list(results)].tolist())
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    _say("  gpu done; budgets", g["budget"][:8].tolist(), "nodes", g["n_nodes"][:8].tolist())
+    end_to_end_check(w, g, inp, results)
+    seqs = range(w.batch)
+    staged_check(w, g, sc, sp, inp, seqs)
+    saba_check(w, g, sc, sp, inp, seqs)
+    # acceptance
+    if w.targets == "depth":
+        acc = ctx.accept(g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
+                         target_depth=torch.from_numpy(inp["target_depth"]).cuda())
+        acc = [a.cpu().numpy() for a in acc]
+        for b in seqs:
+            a, nodes, bonus = oracle.accept(g["n_nodes"][b], g["tokens"][b], g["parents"][b],
+                                            w.L, target_depth=inp["target_depth"][b])
+            assert acc[0][b] == a and acc[2][b] == bonus
+            assert np.array_equal(acc[1][b], nodes)
+    else:
+        tr, tn = ctx.synth_node_targets(w.seed, torch.from_numpy(inp["root_token"]).cuda(),
+                                        g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
+                                        g["_out"].topk_ids)
+        acc = ctx.accept(g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
+                         target_root=tr, target_node=tn)
+        acc = [a.cpu().numpy() for a in acc]
+        tr, tn = tr.cpu().numpy(), tn.cpu().numpy()
+        for b, r in results.items():
+            n = r["n_nodes"]
+            par, tok, dep = r["parents"][:n], r["tokens"][:n], r["depth"][:n]
+            ptok = np.where(par < 0, inp["root_token"][b], r["tokens"][np.maximum(par, 0)])
+            ref_nodes = S.node_targets(w.seed, b, dep, ptok, tok, r["topk_ids"], w.V, w.L, w.K)
+            ref_root = S.node_targets(w.seed, b, [0], [-1], [inp["root_token"][b]], r["topk_ids"],
+                                      w.V, w.L, w.K)[0]
+            assert tr[b] == ref_root
+            assert np.array_equal(tn[b][:n], ref_nodes)
+            a, nodes, bonus = oracle.accept(n, r["tokens"], r["parents"], w.L, int(ref_root),
+                                            target_node=np.concatenate(
+                                                [ref_nodes, -np.ones(w.n_max - n, np.int32)]))
+            assert acc[0][b] == a and acc[2][b] == bonus
+            assert np.array_equal(acc[1][b], nodes)
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
+def test_budgets_spread_under_saba():
+    """SABA picks several distinct budgets across the batch of workload 2."""
+    w = S.workload(2)
+    inp = S.gen_round(w, with_targets=False)
+    sc, sp = WL.scorer_inputs(w, "literal"), WL.saba_inputs(w)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    assert len(set(g["budget"].tolist())) >= 3
+    ctx.close()
+
+
+def test_determinism_bitwise():
+    w = S.workload(3, batch=8)
+    inp = S.gen_round(w, with_targets=False)
+    sc, sp = WL.scorer_inputs(w, "literal"), WL.saba_inputs(w)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    first = WL.gpu_round(ctx, w, inp, torch)
+    for _ in range(5):
+        again = WL.gpu_round(ctx, w, inp, torch)
+        for k in ("topk_ids", "topk_logq", "row_lse", "edge_scores", "budget", "tokens",
+                  "parents", "mask", "node_scores"):
+            assert np.array_equal(first[k], again[k]), k
+    ctx.close()
+
+
+def test_positive_edge_scores_staged():
+    """Non-monotone path scores (a positive interaction term larger than
+    -log q): the selection still matches the oracle bit for bit."""
+    w = S.workload(0, batch=2, V=3000, L=5, K=3, n_max=64, fixed_budget=40)
+    inp = S.gen_round(w, with_targets=False)
+    sc = WL.scorer_inputs(w, "paper")
+    sc["beta"] = 400.0                     # residual dominates log q
+    ctx = WL.gpu_context(w, sc, None, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    assert (g["edge_scores"] > 0).any()
+    staged_check(w, g, sc, None, inp, range(w.batch))
+    ctx.close()
+
+
+def test_history_ring_chain():
+    """Chained rounds: acceptance pushes acc_len into the device ring and the
+    next round's SABA reads the ring mean."""
+    w = S.workload(2, batch=4, V=4000)
+    sc, sp = WL.scorer_inputs(w, "literal"), WL.saba_inputs(w)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    ring = S.hist_ring_init(w)
+    ctx.set_history(torch.from_numpy(ring).cuda())
+    P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
+    pos = np.zeros(w.batch, int)
+    for rnd in range(4):
+        inp = S.gen_round(w, rnd)
+        g = WL.gpu_round(ctx, w, inp, torch, use_ring=True)
+        hist = ring.astype(np.float64).mean(axis=1)
+        for b in range(w.batch):
+            assert g["saba_state"][b, 2] == np.float32(hist[b])
+            conf = sum(float(v) for v in g["row_maxprob"][b]) / w.L
+            ent = sum(float(v) for v in g["row_entropy"][b]) / w.L
+            bud, _, rel, _ = oracle.saba(P, conf, ent, float(hist[b]), int(inp["prefix_len"][b]))
+            if rel > 1e-12:
+                assert bud == g["budget"][b]
+        acc = ctx.accept(g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
+                         target_depth=torch.from_numpy(inp["target_depth"]).cuda(),
+                         update_history=True)
+        a = acc[0].cpu().numpy()
+        for b in range(w.batch):
+            ring[b, pos[b]] = a[b]
+            pos[b] = (pos[b] + 1) % S.HIST_WINDOW
+    ctx.close()
+
+
+def test_abi_errors_on_device():
+    import paper_2608_20375_amd as G
+    w = S.workload(0, batch=2, V=1000)
+    sc = WL.scorer_inputs(w, "literal")
+    ctx = G.Context(2, w.L, w.V, w.K, w.n_max)
+    logits = torch.zeros(2, w.L, w.V, dtype=torch.int16, device="cuda")
+    root = torch.zeros(2, dtype=torch.int32, device="cuda")
+    # no scorer yet
+    with pytest.raises(G.GraftError) as e:
+        ctx.build_tree(logits, root, root, fixed_budget=root)
+    assert e.value.status == 1
+    T = lambda a: torch.from_numpy(a).cuda()
+    ctx.set_scorer(T(sc["emb"]), T(sc["g_parent"]), T(sc["g_child"]), None, sc["scale"], 1.0, 0)
+    # SABA without parameters
+    with pytest.raises(G.GraftError):
+        ctx.build_tree(logits, root, root, hist=torch.zeros(2, device="cuda"))
+    # bad SABA grids
+    for grid in ([32, 16], [0, 8], [8, 10 ** 6], list(range(1, 70))):
+        with pytest.raises(G.GraftError):
+            ctx.set_saba(grid, [1, 0, 0, 0])
+    # batch too large
+    big = torch.zeros(3, w.L, w.V, dtype=torch.int16, device="cuda")
+    r3 = torch.zeros(3, dtype=torch.int32, device="cuda")
+    with pytest.raises(G.GraftError):
+        ctx.build_tree(big, r3, r3, fixed_budget=r3)
+    # misaligned logits
+    flat = torch.zeros(2 * w.L * w.V + 8, dtype=torch.int16, device="cuda")
+    mis = flat[1:1 + 2 * w.L * w.V].view(2, w.L, w.V)
+    with pytest.raises(G.GraftError):
+        ctx.build_tree(mis, root, root, fixed_budget=root)
+    # out-of-range root token is reported by the device status
+    bad_root = torch.full((2,), w.V + 5, dtype=torch.int32, device="cuda")
+    ctx.build_tree(logits, bad_root, root, fixed_budget=torch.full((2,), 4, dtype=torch.int32,
+                                                                   device="cuda"))
+    assert ctx.device_status() == 5
+    assert ctx.device_status() == 0
+    # accept needs exactly one target mode
+    n = torch.zeros(2, dtype=torch.int32, device="cuda")
+    tk = torch.zeros(2, w.n_max, dtype=torch.int32, device="cuda")
+    with pytest.raises(G.GraftError):
+        ctx.accept(n, tk, tk)
+    ctx.close()
+
+
+def test_zero_budget_and_tiny_trees():
+    w = S.workload(0, batch=3, V=2000, n_max=32)
+    inp = S.gen_round(w)
+    inp["fixed_budget"] = np.array([0, 1, 32], np.int32)
+    sc = WL.scorer_inputs(w, "literal")
+    ctx = WL.gpu_context(w, sc, None, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    assert g["n_nodes"].tolist() == [0, 1, 32]
+    assert (g["tokens"][0] == -1).all() and (g["mask"][0] == 0).all()
+    staged_check(w, g, sc, None, inp, range(3))
+    acc = ctx.accept(g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
+                     target_depth=torch.from_numpy(inp["target_depth"]).cuda())
+    a, nodes, bonus = [x.cpu().numpy() for x in acc]
+    assert a[0] == 0 and bonus[0] == inp["target_depth"][0, 0]
+    ctx.close()

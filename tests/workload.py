@@ -1,0 +1,92 @@
+"""Test-side helpers: audited synthetic rounds and oracle/GPU runners.
+
+Audit: a sequence's inputs are re-drawn (attempt + 1) until every
+floating-point decision the oracle takes for it has a margin that an fp32
+implementation cannot cross (oracle.sequence_ok).  Only the oracle is consulted,
+never the HIP path.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+import synthetic as S
+
+MAX_ATTEMPTS = 12
+
+
+def scorer_inputs(w, mode):
+    sc = S.gen_scorer(w, mode)
+    # the ABI carries scale and beta as fp32; hand the oracle the same values
+    sc["scale"] = float(np.float32(sc["scale"]))
+    sc["beta"] = float(np.float32(sc["beta"]))
+    return sc
+
+
+def saba_inputs(w):
+    if w.budget_mode != "saba":
+        return None
+    sp = S.saba_params(w)
+    for k in ("tau_min", "c0", "c1", "c2"):
+        sp[k] = float(np.float32(sp[k]))
+    sp["phi"] = np.asarray(sp["phi"], np.float32)
+    return sp
+
+
+def audited_round(w, rnd=0, mode="literal", seqs=None, with_targets=True):
+    """Inputs for the whole batch; sequences in `seqs` (default: all) are
+    audited with the oracle and re-drawn until their decisions are robust.
+    Returns (inputs, scorer, saba, {b: oracle result})."""
+    sc = scorer_inputs(w, mode)
+    sp = saba_inputs(w)
+    seqs = list(range(w.batch)) if seqs is None else list(seqs)
+    attempts = np.zeros(w.batch, np.int64)
+    inp = S.gen_round(w, rnd, attempts, with_targets=with_targets)
+    P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
+    results = {}
+    for b in seqs:
+        for a in range(MAX_ATTEMPTS):
+            if a:
+                attempts[b] = a
+                one = S.gen_round(w, rnd, attempts, with_targets=with_targets, seqs=[b])
+                for k, v in one.items():
+                    if isinstance(v, np.ndarray) and v.shape and v.shape[0] == w.batch:
+                        inp[k][b] = v[b]
+            r = oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b],
+                                      inp["base_pos"][b], inp["prefix_len"][b],
+                                      inp["fixed_budget"][b] if "fixed_budget" in inp else 0,
+                                      float(inp["hist"][b]))
+            if oracle.sequence_ok(r, w.L):
+                break
+        else:
+            raise RuntimeError("no robust draw for sequence %d" % b)
+        results[b] = r
+    inp["attempts"] = attempts
+    return inp, sc, sp, results
+
+
+def gpu_context(w, sc, sp, torch, dev="cuda"):
+    import paper_2608_20375_amd as G
+    ctx = G.Context(w.batch, w.L, w.V, w.K, w.n_max, S.HIST_WINDOW)
+    T = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    ctx.set_scorer(T(sc["emb"]), T(sc["g_parent"]), T(sc["g_child"]), T(sc["depth_emb"]),
+                   sc["scale"], sc["beta"], sc["center"])
+    if sp is not None:
+        ctx.set_saba(list(sp["grid"]), list(sp["phi"]), sp["tau_min"], sp["c0"], sp["c1"],
+                     sp["c2"])
+    return ctx
+
+
+def gpu_round(ctx, w, inp, torch, dev="cuda", use_ring=False, edges=True):
+    """Upload a round, build trees on the GPU, return numpy copies."""
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    logits = T(inp["logits"].view(np.int16))
+    out = ctx.build_tree(logits, T(inp["root_token"]), T(inp["base_pos"]),
+                         prefix_len=T(inp["prefix_len"]),
+                         hist=None if use_ring else T(inp["hist"]),
+                         fixed_budget=T(inp["fixed_budget"]) if "fixed_budget" in inp else None,
+                         edges=edges)
+    torch.cuda.synchronize()
+    res = {k: v.cpu().numpy() for k, v in out.as_dict().items()}
+    res["_out"] = out
+    return res
