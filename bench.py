@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Benchmark of GRAFT's per-round draft-tree construction on one MI355X.
+
+A step is one full round for the whole batch: graft_build_tree (logits pass,
+TDES edge scoring, SABA budget, best-first selection, emission and ancestor
+mask) followed by graft_accept (greedy acceptance walk), on synthetic drafter
+logits already resident in HBM.  The default workload is the batch-64 one
+(B=64, L=16, V=128256, K=16, SABA budgets 32..512): the metric's
+configuration.  Logit buffers are rotated so that the 256 MB Infinity Cache
+cannot serve a round's reads from the previous round.
+
+Prints one JSON line: rounds/s, us/round, the logits pass against the HBM
+roofline (its duration from HIP events recorded around it in the timed
+region), and the CPU oracle timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "draft-tree rounds/sec and µs/round at B=64; logits-pass HBM GB/s vs peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_digest() -> str:
+    p = os.path.join(ROOT, "paper_2608_20375_amd", "csrc", "k_logits.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def stored_traffic(workload: int):
+    """HBM bytes per logits-pass launch from the committed rocprofv3 PMC
+    summary, valid only for the kernel source it was measured on."""
+    p = os.path.join(ROOT, "profiles", "logits_pass_w%d_traffic.json" % workload)
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("k_logits_sha256_16") != source_digest():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, inp, sc, sp, seconds: float):
+    import oracle
+    P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
+    fb = inp.get("fixed_budget")
+    done = 0
+    t0 = time.perf_counter()
+    while done < w.batch:
+        b = done
+        oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b], inp["base_pos"][b],
+                              inp["prefix_len"][b], 0 if fb is None else fb[b],
+                              float(inp["hist"][b]))
+        if w.targets == "depth":
+            pass  # acceptance cost is negligible next to the logits pass
+        done += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    el = time.perf_counter() - t0
+    rounds_per_s = (done / w.batch) / el
+    return {"value": rounds_per_s, "unit": "rounds/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d sequences of one round (%d rows x %d bf16 logits each), "
+                      "single thread, fp64, scaled to whole rounds" % (done, w.batch, w.L, w.V),
+            "seconds": el}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--rotate", type=int, default=0, help="logit buffers (0: >= 1 GiB total)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain device copy of known size (PMC calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the draft-tree path shards by sequence with no "
+              "communication, so a multi-GPU figure adds nothing here (got --gpus %d, "
+              "WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synthetic as S
+    import paper_2608_20375_amd as G
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = S.workload(args.workload)
+    t0 = time.time()
+    inp = S.gen_round(w, 0)
+    sc = S.gen_scorer(w, "literal")
+    sp = S.saba_params(w) if w.budget_mode == "saba" else None
+    log("inputs generated in %.1fs" % (time.time() - t0))
+
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    ctx = G.Context(w.batch, w.L, w.V, w.K, w.n_max, S.HIST_WINDOW)
+    ctx.set_scorer(T(sc["emb"]), T(sc["g_parent"]), T(sc["g_child"]),
+                   None if sc["depth_emb"] is None else T(sc["depth_emb"]),
+                   sc["scale"], sc["beta"], sc["center"])
+    if sp is not None:
+        ctx.set_saba(list(sp["grid"]), list(sp["phi"]), sp["tau_min"], sp["c0"], sp["c1"], sp["c2"])
+
+    logit_bytes = w.batch * w.L * w.V * 2
+    R = args.rotate or max(2, math.ceil((1 << 30) / logit_bytes))
+    base_logits = T(inp["logits"].view(np.int16))
+    bufs = [base_logits] + [base_logits.clone() for _ in range(R - 1)]
+    root, base_pos = T(inp["root_token"]), T(inp["base_pos"])
+    prefix = T(inp["prefix_len"])
+    fixed = T(inp["fixed_budget"]) if "fixed_budget" in inp else None
+    node_mode = w.targets == "node"
+    hist = None if node_mode else T(inp["hist"])
+    if node_mode:
+        ctx.set_history(T(inp["hist_ring"]))
+    tdepth = T(inp["target_depth"]) if not node_mode else None
+    tb = G.TreeBuffers(ctx, w.batch)
+    acc_len = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    acc_nodes = torch.empty(w.batch, w.L, dtype=torch.int32, device=dev)
+    bonus = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    troot = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    tnode = torch.empty(w.batch, w.n_max, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+
+    def one_round(i):
+        ctx.build_tree(bufs[i % R], root, base_pos, prefix_len=prefix, hist=hist,
+                       fixed_budget=fixed, out=tb)
+        if node_mode:
+            ctx.synth_node_targets(w.seed + i, root, tb.n_nodes, tb.tokens, tb.parents,
+                                   tb.topk_ids, troot, tnode)
+            ctx.accept(tb.n_nodes, tb.tokens, tb.parents, target_root=troot, target_node=tnode,
+                       update_history=True, acc_len=acc_len, acc_nodes=acc_nodes, bonus=bonus)
+        else:
+            ctx.accept(tb.n_nodes, tb.tokens, tb.parents, target_depth=tdepth, acc_len=acc_len,
+                       acc_nodes=acc_nodes, bonus=bonus)
+
+    for i in range(args.warmup):
+        one_round(i)
+    torch.cuda.synchronize()
+    log("warmup done (%d rounds)" % args.warmup)
+
+    # timed region, with stage events recorded around every kernel
+    ctx.profile_begin(args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_host = time.perf_counter()
+    e0.record()
+    for i in range(args.steps):
+        one_round(args.warmup + i)
+    e1.record()
+    torch.cuda.synchronize()
+    host_s = time.perf_counter() - t_host
+    ms_total = e0.elapsed_time(e1)
+    stage_ms, stage_n = ctx.profile_end()
+    ms_per_step = ms_total / args.steps
+    stage_avg = [m / n if n else 0.0 for m, n in zip(stage_ms, stage_n)]
+    log("timed %d rounds: %.3f ms/round (host %.3f ms/round); stages ms %s" %
+        (args.steps, ms_per_step, 1e3 * host_s / args.steps, ["%.4f" % s for s in stage_avg]))
+
+    # the same region without stage events, as a check of their overhead
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(args.steps):
+        one_round(i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_plain = e0.elapsed_time(e1) / args.steps
+
+    k1_s = stage_avg[0] * 1e-3
+    achieved = logit_bytes / k1_s / 1e9 if k1_s > 0 else 0.0
+    traffic = stored_traffic(args.workload)
+
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 copies of %d bytes" % n)
+
+    nodes = tb.n_nodes.float().mean().item()
+    budgets = tb.budget.float().mean().item()
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, inp, sc, sp, args.cpu_seconds)
+        log("cpu baseline: %.4f rounds/s over %.1fs" % (cpu["value"], cpu["seconds"]))
+        cpu.pop("seconds")
+
+    result = {
+        "metric": METRIC,
+        "value": 1e3 / ms_per_step,
+        "unit": "rounds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "us_per_round": 1e3 * ms_per_step,
+        "us_per_round_without_stage_events": 1e3 * ms_plain,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic",
+        "config": {
+            "workload": "B=%d sequences, L=%d, V=%d bf16 logits, K=%d, %s, N_max=%d, scorer "
+                        "d=%d rank %d, %s targets, %d rotating logit buffers" % (
+                            w.batch, w.L, w.V, w.K,
+                            "SABA budgets %d..%d" % (min(w.grid), max(w.grid))
+                            if w.budget_mode == "saba" else "fixed budget %d" % w.fixed_budget,
+                            w.n_max, w.emb_dim, w.rank, "per-node" if node_mode else "per-depth", R),
+            "global_batch": w.batch,
+            "mean_budget": budgets,
+            "mean_nodes": nodes,
+            "stage_us": {"logits_pass": 1e3 * stage_avg[0], "edge_scores": 1e3 * stage_avg[1],
+                         "select_emit_mask": 1e3 * stage_avg[2], "accept": 1e3 * stage_avg[3]},
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "logits_pass_kernel",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": logit_bytes,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -21,7 +21,7 @@ _lib = None
 EXPORTED_SYMBOLS = (
     "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
     "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
-    "graft_status_string", "graft_last_error",
+    "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
 )
 
 
@@ -92,13 +92,15 @@ def lib():
         L.graft_accept.argtypes = [vp, i32, vp, vp, vp, C.POINTER(Targets), vp, vp, vp, i32, vp]
         L.graft_get_device_status.argtypes = [vp, vp]
         L.graft_synth_node_targets.argtypes = [vp, i32, C.c_uint64, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.graft_profile_begin.argtypes = [vp, i32]
+        L.graft_profile_end.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
         L.graft_status_string.argtypes = [C.c_int]
         L.graft_status_string.restype = C.c_char_p
         L.graft_last_error.argtypes = []
         L.graft_last_error.restype = C.c_char_p
         for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
                   "graft_build_tree", "graft_accept", "graft_get_device_status",
-                  "graft_synth_node_targets"):
+                  "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -253,6 +255,16 @@ class Context:
             _ptr(topk_ids, torch.int32, "topk_ids"), _ptr(target_root, torch.int32, "target_root"),
             _ptr(target_node, torch.int32, "target_node"), _stream()), "graft_synth_node_targets")
         return target_root, target_node
+
+    def profile_begin(self, max_calls: int):
+        _check(lib().graft_profile_begin(self._h, int(max_calls)), "graft_profile_begin")
+
+    def profile_end(self):
+        """(summed ms, timed launches) per stage: logits, edges, select, accept."""
+        ms = (C.c_double * 4)()
+        n = (C.c_int32 * 4)()
+        _check(lib().graft_profile_end(self._h, ms, n), "graft_profile_end")
+        return list(ms), list(n)
 
     def device_status(self) -> int:
         return lib().graft_get_device_status(self._h, _stream())

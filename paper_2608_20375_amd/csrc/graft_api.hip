@@ -32,8 +32,20 @@ hipError_t dalloc(T **p, size_t n) {
   return hipMalloc(reinterpret_cast<void **>(p), n * sizeof(T));
 }
 
+void prof_release(graft_ctx *c) {
+  if (c->prof_build) {
+    for (int i = 0; i < 4 * c->prof_cap; ++i) (void)hipEventDestroy(c->prof_build[i]);
+    for (int i = 0; i < 2 * c->prof_cap; ++i) (void)hipEventDestroy(c->prof_acc[i]);
+    delete[] c->prof_build;
+    delete[] c->prof_acc;
+  }
+  c->prof_build = c->prof_acc = nullptr;
+  c->prof_cap = c->prof_nbuild = c->prof_nacc = 0;
+}
+
 void free_ctx(graft_ctx *c) {
   if (!c) return;
+  prof_release(c);
   (void)hipFree(c->part_stats);
   (void)hipFree(c->part_keys);
   (void)hipFree(c->row_counters);
@@ -247,12 +259,18 @@ int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_
     return fail(GRAFT_ERR_INVALID_ARG,
                 "graft_build_tree: no hist input and no history ring (graft_set_history)");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipEvent_t *ev = nullptr;
+  if (ctx->prof_build && ctx->prof_nbuild < ctx->prof_cap) ev = ctx->prof_build + 4 * ctx->prof_nbuild++;
+  if (ev) (void)hipEventRecord(ev[0], s);
   hipError_t e = graft::launch_logits_pass(ctx, in->batch, in->logits, out, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: logits pass");
+  if (ev) (void)hipEventRecord(ev[1], s);
   e = graft::launch_edge_scores(ctx, in->batch, in->root_token, out->edge_scores, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: edge scores");
+  if (ev) (void)hipEventRecord(ev[2], s);
   e = graft::launch_select(ctx, in, out, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: selection");
+  if (ev) (void)hipEventRecord(ev[3], s);
   return GRAFT_OK;
 }
 
@@ -274,10 +292,14 @@ int graft_accept(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes, const in
     return fail(GRAFT_ERR_INVALID_ARG, "graft_accept: per-node targets need target_root");
   if (update_history && !ctx->has_history)
     return fail(GRAFT_ERR_INVALID_ARG, "graft_accept: no history ring (graft_set_history)");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipEvent_t *ev = nullptr;
+  if (ctx->prof_acc && ctx->prof_nacc < ctx->prof_cap) ev = ctx->prof_acc + 2 * ctx->prof_nacc++;
+  if (ev) (void)hipEventRecord(ev[0], s);
   hipError_t e = graft::launch_accept(ctx, batch, n_nodes, tokens, parents, targets, acc_len,
-                                      acc_nodes, bonus, update_history,
-                                      reinterpret_cast<hipStream_t>(stream));
+                                      acc_nodes, bonus, update_history, s);
   if (e != hipSuccess) return hip_fail(e, "graft_accept");
+  if (ev) (void)hipEventRecord(ev[1], s);
   return GRAFT_OK;
 }
 
@@ -294,6 +316,65 @@ int graft_get_device_status(graft_ctx *ctx, graft_stream_t stream) {
     if (e != hipSuccess) return hip_fail(e, "graft_get_device_status: clear");
     return fail(GRAFT_ERR_DEVICE_DATA, "kernels saw invalid data (flags 0x%x)", flag);
   }
+  return GRAFT_OK;
+}
+
+int graft_profile_begin(graft_ctx *ctx, int32_t max_calls) {
+  if (!ctx || max_calls < 1 || max_calls > (1 << 20))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_profile_begin: bad arguments");
+  prof_release(ctx);
+  ctx->prof_build = new (std::nothrow) hipEvent_t[4 * static_cast<size_t>(max_calls)];
+  ctx->prof_acc = new (std::nothrow) hipEvent_t[2 * static_cast<size_t>(max_calls)];
+  if (!ctx->prof_build || !ctx->prof_acc) {
+    delete[] ctx->prof_build;
+    delete[] ctx->prof_acc;
+    ctx->prof_build = ctx->prof_acc = nullptr;
+    return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_profile_begin: host allocation failed");
+  }
+  ctx->prof_cap = 0;
+  for (int i = 0; i < max_calls; ++i) {
+    hipError_t e = hipSuccess;
+    for (int j = 0; j < 4 && e == hipSuccess; ++j) e = hipEventCreate(&ctx->prof_build[4 * i + j]);
+    for (int j = 0; j < 2 && e == hipSuccess; ++j) e = hipEventCreate(&ctx->prof_acc[2 * i + j]);
+    if (e != hipSuccess) {
+      prof_release(ctx);
+      return hip_fail(e, "graft_profile_begin: hipEventCreate");
+    }
+    ctx->prof_cap = i + 1;
+  }
+  ctx->prof_nbuild = ctx->prof_nacc = 0;
+  return GRAFT_OK;
+}
+
+int graft_profile_end(graft_ctx *ctx, double *stage_ms, int32_t *stage_calls) {
+  if (!ctx || !stage_ms || !stage_calls)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_profile_end: NULL argument");
+  for (int j = 0; j < 4; ++j) {
+    stage_ms[j] = 0.0;
+    stage_calls[j] = 0;
+  }
+  if (!ctx->prof_build) return fail(GRAFT_ERR_INVALID_ARG, "graft_profile_end: not armed");
+  hipError_t e = hipSuccess;
+  for (int i = 0; i < ctx->prof_nbuild && e == hipSuccess; ++i) {
+    hipEvent_t *ev = ctx->prof_build + 4 * i;
+    e = hipEventSynchronize(ev[3]);
+    for (int j = 0; j < 3 && e == hipSuccess; ++j) {
+      float ms = 0.f;
+      e = hipEventElapsedTime(&ms, ev[j], ev[j + 1]);
+      stage_ms[j] += ms;
+      stage_calls[j] += 1;
+    }
+  }
+  for (int i = 0; i < ctx->prof_nacc && e == hipSuccess; ++i) {
+    hipEvent_t *ev = ctx->prof_acc + 2 * i;
+    float ms = 0.f;
+    e = hipEventSynchronize(ev[1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev[0], ev[1]);
+    stage_ms[3] += ms;
+    stage_calls[3] += 1;
+  }
+  prof_release(ctx);
+  if (e != hipSuccess) return hip_fail(e, "graft_profile_end");
   return GRAFT_OK;
 }
 

@@ -155,6 +155,10 @@ struct graft_ctx {
   bool has_history;
   // device-side data-error flag
   uint32_t *error_flag;
+  // stage timing (graft_profile_begin / graft_profile_end)
+  hipEvent_t *prof_build;  // [prof_cap][4]
+  hipEvent_t *prof_acc;    // [prof_cap][2]
+  int32_t prof_cap, prof_nbuild, prof_nacc;
 };
 
 namespace graft {

@@ -12,9 +12,9 @@
 // (the K-th best value it has buffered); a tile whose maximum falls below it
 // costs nothing more, otherwise its passing elements are appended to a per-wave
 // LDS buffer with ballot/mbcnt and the buffer is compacted by a wave bitonic
-// sort of (value desc, id asc) keys when full.  Rows split over several
-// workgroups are merged by the last workgroup of the row (atomic counter,
-// reset by that workgroup).
+// sort of (value desc, id asc) keys when full.  When there are too few rows to
+// fill the chip, rows are split over several workgroups whose partial results
+// a second small kernel merges.
 #include "graft_internal.h"
 
 namespace graft {
@@ -28,8 +28,10 @@ constexpr float kL2E = 1.44269504088896340736f;
 constexpr double kLn2 = 0.693147180559945309417232121458;
 constexpr double kLog2e = 1.44269504088896340735992468100;
 constexpr float kNegBig = -1e30f;                 // finite stand-in for -inf
-constexpr int kTargetBlocks = 2048;
+constexpr int kTargetBlocks = 1024;                // one residency round at 4 waves/SIMD
 constexpr int kMinSplitVec = 512;                 // >= 4096 elements per split
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 struct LaneStats {
   float mx;      // largest logit seen
@@ -45,13 +47,15 @@ __device__ __forceinline__ void stats_init(LaneStats &s) {
   s.T2 = 0.0;
 }
 
-// Moves the offset to a larger maximum (rescales S and T2 exactly in fp64).
+// Moves the offset to a larger maximum and rescales S and T2.  The factor
+// 2^(mL_old - mL_new) is one v_exp_f32 of an fp32 difference (exact for offsets
+// within a factor two of each other, and 0 for the initial finite stand-in).
 __device__ __forceinline__ void stats_raise(LaneStats &s, float new_mx) {
   if (new_mx > s.mx) {
     const float nL = new_mx * kL2E;
-    const double d = static_cast<double>(s.mL) - static_cast<double>(nL);
-    const double a = exp2(d);
-    s.T2 = a * (s.T2 + d * s.S);
+    const float d = s.mL - nL;
+    const double a = static_cast<double>(__builtin_amdgcn_exp2f(d));
+    s.T2 = a * (s.T2 + static_cast<double>(d) * s.S);
     s.S = a * s.S;
     s.mL = nL;
     s.mx = new_mx;
@@ -65,7 +69,8 @@ struct WaveBuf {
   float thr;       // wave-uniform: a candidate needs value >= thr
 };
 
-// Sort the buffer, keep the best K, raise the threshold to the K-th value.
+// Sorts a wave's buffer, keeps the best K keys, raises the threshold to the
+// K-th value.
 template <int CAP>
 __device__ __forceinline__ void wave_compact(WaveBuf<CAP> &w, int K) {
   constexpr int E = CAP / kWave;
@@ -114,6 +119,28 @@ __device__ __forceinline__ void wave_offer(WaveBuf<CAP> &w, int K, float v, uint
   w.count += n;
 }
 
+// Offers the tile elements flagged in `bits` (bit 8u+e: element e of the
+// lane's u-th vector), one per lane per step, lowest bit first.  The values are
+// read back from an LDS copy of the lane's words (`stage`, [kUnroll][64] uint4)
+// by computed address, which avoids dynamically indexed register arrays and
+// leaves the prefetched global loads of the next tile in flight.
+template <int CAP>
+__device__ __forceinline__ void offer_bits(WaveBuf<CAP> &w, int K, uint32_t bits,
+                                           const uint4 *stage, int64_t base_id) {
+  const int lane = lane_id();
+  const uint32_t *words = reinterpret_cast<const uint32_t *>(stage);
+  while (__ballot(bits != 0) != 0ull) {
+    const bool has = bits != 0;
+    const int j = has ? __builtin_ctz(bits) : 0;
+    const int u = j >> 3, e = j & 7;
+    const int64_t id = base_id + (u * kWave + lane) * 8 + e;
+    const uint32_t word = words[(u * kWave + lane) * 4 + (e >> 1)];
+    const float x = __uint_as_float((e & 1) ? (word & 0xFFFF0000u) : (word << 16));
+    wave_offer<CAP>(w, K, x, static_cast<uint32_t>(id), has);
+    bits &= bits - 1u;
+  }
+}
+
 // Offers a 64-bit key per lane (used when merging already-sorted lists).
 template <int CAP>
 __device__ __forceinline__ void wave_offer_key(WaveBuf<CAP> &w, int K, uint64_t key) {
@@ -142,11 +169,28 @@ __device__ __forceinline__ void unpack8(const uint4 q, float (&v)[8]) {
   }
 }
 
-// One tile: lane handles vectors vbase + u*64 + lane, u < kUnroll.
+// Loads one tile: lane handles vectors tile_vec + u*64 + lane, u < kUnroll.
+template <bool MASKED>
+__device__ __forceinline__ void load_tile(const uint4 *__restrict__ vec, int64_t tile_vec,
+                                          int64_t n_vec, uint4 (&q)[kUnroll]) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int64_t vi = tile_vec + u * kWave + lane;
+    q[u] = make_uint4(0, 0, 0, 0);
+    if (!MASKED || vi < n_vec) {
+      const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(vec) + vi);
+      q[u] = make_uint4(x.x, x.y, x.z, x.w);
+    }
+  }
+}
+
+// One tile of loaded data: top-K candidates and softmax statistics.
 template <int CAP, bool MASKED>
-__device__ __forceinline__ void process_tile(const uint4 *__restrict__ vec, int64_t tile_vec,
-                                             int64_t n_vec, int64_t elem0, LaneStats &st,
-                                             WaveBuf<CAP> &w, int K) {
+__device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t tile_vec,
+                                             int64_t n_vec, int64_t elem0, uint4 *stage,
+                                             LaneStats &st, WaveBuf<CAP> &w, int K,
+                                             float shared_thr) {
   const int lane = lane_id();
   float v[kUnroll][8];
   bool ok[kUnroll];
@@ -154,9 +198,7 @@ __device__ __forceinline__ void process_tile(const uint4 *__restrict__ vec, int6
   for (int u = 0; u < kUnroll; ++u) {
     const int64_t vi = tile_vec + u * kWave + lane;
     ok[u] = !MASKED || vi < n_vec;
-    uint4 q = make_uint4(0, 0, 0, 0);
-    if (ok[u]) q = vec[vi];
-    unpack8(q, v[u]);
+    unpack8(q[u], v[u]);
     if (MASKED && !ok[u]) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[u][e] = kNegBig;
@@ -171,17 +213,18 @@ __device__ __forceinline__ void process_tile(const uint4 *__restrict__ vec, int6
   }
   const float tmax = fmaxf(fmaxf(sub[0], sub[1]), fmaxf(sub[2], sub[3]));
 
-  // top-K candidates
+  // top-K candidates; any wave's threshold bounds the block's K-th value
+  if (shared_thr > w.thr) w.thr = shared_thr;
   if (__ballot(tmax >= w.thr) != 0ull) {
+    uint32_t bits = 0;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      if (__ballot(ok[u] && sub[u] >= w.thr) != 0ull) {
-        const int64_t id0 = elem0 + (tile_vec + u * kWave + lane) * 8;
+    for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          wave_offer<CAP>(w, K, v[u][e], static_cast<uint32_t>(id0 + e), ok[u]);
-      }
-    }
+      for (int e = 0; e < 8; ++e)
+        bits |= (ok[u] && v[u][e] >= w.thr) ? (1u << (u * 8 + e)) : 0u;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) stage[u * kWave + lane] = q[u];
+    offer_bits<CAP>(w, K, bits, stage, elem0 + tile_vec * 8);
   }
 
   // softmax statistics
@@ -203,6 +246,23 @@ __device__ __forceinline__ void process_tile(const uint4 *__restrict__ vec, int6
   }
   st.S += static_cast<double>((s[0] + s[1]) + (s[2] + s[3]));
   st.T2 += static_cast<double>((t[0] + t[1]) + (t[2] + t[3]));
+}
+
+// One full tile with the block-shared threshold (other waves update their
+// entries without a barrier; relaxed atomic reads keep the LDS addressing).
+template <int CAP>
+__device__ __forceinline__ void step_tile(const uint4 (&q)[kUnroll], int64_t t, int64_t n_vec,
+                                          int64_t elem0, uint4 *stage, LaneStats &st,
+                                          WaveBuf<CAP> &w, int K, float *s_thr, int wave) {
+  float other = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i)
+    other = fmaxf(other, __hip_atomic_load(&s_thr[i], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP));
+  const float before = w.thr;
+  process_tile<CAP, false>(q, t * kTileVec, n_vec, elem0, stage, st, w, K, other);
+  if (lane_id() == 0 && w.thr > before)
+    __hip_atomic_store(&s_thr[wave], w.thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Scalar elements of a row that fall outside its 16-byte aligned body.
@@ -286,12 +346,13 @@ __device__ __forceinline__ void write_row(const RowOut &o, int64_t row, int K, d
 }
 
 template <int CAP>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kThreads, 4)
 logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, int K,
                    double *__restrict__ part_stats, uint64_t *__restrict__ part_keys,
-                   uint32_t *__restrict__ counters, RowOut out) {
+                   RowOut out) {
   __shared__ uint64_t s_buf[kWaves][CAP];
   __shared__ double s_stats[kWaves][3];
+  __shared__ uint4 s_stage[kWaves][kUnroll * kWave];
 
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
@@ -315,33 +376,52 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
   stats_init(st);
   WaveBuf<CAP> w{s_buf[wave], 0, -INFINITY};
 
-  // Tiles interleaved over the waves of the block.
+  // Tiles interleaved over the waves of the block; the next tile's loads are
+  // issued before the current tile is processed.
+  __shared__ float s_thr[kWaves];
+  if (lane == 0) s_thr[wave] = -INFINITY;
+  __syncthreads();
   const int64_t n_full = n_vec / kTileVec;
   int64_t t = wave;
   if (t < n_full) {
-    // First tile: threshold = K-th largest lane maximum of the tile is a valid
-    // lower bound of the K-th largest element; take it before offering.
+    uint4 cur[kUnroll], nxt[kUnroll];
+    load_tile<false>(vec, t * kTileVec, n_vec, cur);
+    // First tile: the K-th largest lane maximum is a lower bound of the K-th
+    // largest element, so it can serve as the threshold from the start.
     {
       float tm = kNegBig;
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         float vv[8];
-        unpack8(vec[t * kTileVec + u * kWave + lane], vv);
+        unpack8(cur[u], vv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) tm = fmaxf(tm, vv[e]);
       }
-      if (K <= kWave) {
-        uint64_t k1[1] = {cand_key(tm, lane)};
-        wave_sort_desc<1>(k1);
-        const uint32_t hi = __shfl(static_cast<uint32_t>(k1[0] >> 32), K - 1);
-        w.thr = unordered_f32(hi);
-      }
+      uint64_t k1[1] = {cand_key(tm, lane)};
+      wave_sort_desc<1>(k1);
+      const uint32_t hi = __shfl(static_cast<uint32_t>(k1[0] >> 32), K - 1);
+      w.thr = unordered_f32(hi);
     }
-    for (; t < n_full; t += kWaves)
-      process_tile<CAP, false>(vec, t * kTileVec, n_vec, elem0, st, w, K);
+    // ping-pong between two register buffers: the loads of tile t + kWaves are
+    // in flight while tile t is processed
+    for (;;) {
+      int64_t tn = t + kWaves;
+      if (tn < n_full) load_tile<false>(vec, tn * kTileVec, n_vec, nxt);
+      step_tile<CAP>(cur, t, n_vec, elem0, s_stage[wave], st, w, K, s_thr, wave);
+      t = tn;
+      if (t >= n_full) break;
+      tn = t + kWaves;
+      if (tn < n_full) load_tile<false>(vec, tn * kTileVec, n_vec, cur);
+      step_tile<CAP>(nxt, t, n_vec, elem0, s_stage[wave], st, w, K, s_thr, wave);
+      t = tn;
+      if (t >= n_full) break;
+    }
   }
-  if (t == n_full && n_full * kTileVec < n_vec)
-    process_tile<CAP, true>(vec, t * kTileVec, n_vec, elem0, st, w, K);
+  if (t == n_full && n_full * kTileVec < n_vec) {
+    uint4 cur[kUnroll];
+    load_tile<true>(vec, t * kTileVec, n_vec, cur);
+    process_tile<CAP, true>(cur, t * kTileVec, n_vec, elem0, s_stage[wave], st, w, K, -INFINITY);
+  }
   // Misaligned head [0, a0) and tail [a0 + 8 nv_row, V): split 0, wave 0.
   if (split == 0 && wave == 0) {
     const int64_t tail0 = a0 + 8 * nv_row;
@@ -390,7 +470,8 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     return;
   }
 
-  // Split row: publish the partial, the last block of the row merges.
+  // Split row: publish the partial; merge_kernel combines them after this
+  // kernel has finished (the kernel boundary makes the writes visible).
   const int64_t slot = row * splits + split;
   for (int i = lane; i < K; i += kWave) part_keys[slot * K + i] = s_buf[0][i];
   if (lane == 0) {
@@ -398,20 +479,21 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     part_stats[slot * 3 + 1] = S;
     part_stats[slot * 3 + 2] = T2;
   }
-  __threadfence();
-  uint32_t last = 0;
-  if (lane == 0) last = atomicAdd(&counters[row], 1u) == static_cast<uint32_t>(splits - 1);
-  last = __shfl(last, 0);
-  if (!last) return;
-  __threadfence();
+}
 
-  const volatile double *ps = part_stats + row * splits * 3;
-  mL = ps[0];
-  S = ps[1];
-  T2 = ps[2];
+// One wave per split row: merges the partial statistics and top-K lists.
+template <int CAP>
+__global__ void __launch_bounds__(kWave)
+merge_kernel(int splits, int K, const double *__restrict__ part_stats,
+             const uint64_t *__restrict__ part_keys, RowOut out) {
+  __shared__ uint64_t s_buf[CAP];
+  const int64_t row = blockIdx.x;
+  const int lane = lane_id();
+  const double *ps = part_stats + row * splits * 3;
+  double mL = ps[0], S = ps[1], T2 = ps[2];
   for (int i = 1; i < splits; ++i) stats_merge(mL, S, T2, ps[3 * i], ps[3 * i + 1], ps[3 * i + 2]);
-  WaveBuf<CAP> m{s_buf[0], 0, -INFINITY};
-  const volatile uint64_t *pk = part_keys + row * splits * K;
+  WaveBuf<CAP> m{s_buf, 0, -INFINITY};
+  const uint64_t *pk = part_keys + row * splits * K;
   const int total = splits * K;
   for (int base = 0; base < total; base += kWave) {
     const int i = base + lane;
@@ -419,9 +501,8 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     wave_offer_key<CAP>(m, K, key);
   }
   wave_compact<CAP>(m, K);
-  for (int i = m.count + lane; i < K; i += kWave) s_buf[0][i] = 0ull;
-  if (lane == 0) counters[row] = 0u;
-  write_row<CAP>(out, row, K, mL, S, T2, s_buf[0]);
+  for (int i = m.count + lane; i < K; i += kWave) s_buf[i] = 0ull;
+  write_row<CAP>(out, row, K, mL, S, T2, s_buf);
 }
 
 }  // namespace
@@ -465,14 +546,19 @@ hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
   o.o_maxprob = out ? out->row_maxprob : nullptr;
   o.o_ent = out ? out->row_entropy : nullptr;
   const dim3 grid(static_cast<unsigned>(rows * splits));
+  const int64_t V = d.vocab;
   if (d.top_k <= 32) {
-    hipLaunchKernelGGL(logits_pass_kernel<128>, grid, dim3(kThreads), 0, stream, logits,
-                       static_cast<int64_t>(d.vocab), splits, d.top_k, ctx->part_stats,
-                       ctx->part_keys, ctx->row_counters, o);
+    hipLaunchKernelGGL(logits_pass_kernel<128>, grid, dim3(kThreads), 0, stream, logits, V,
+                       splits, d.top_k, ctx->part_stats, ctx->part_keys, o);
+    if (splits > 1)
+      hipLaunchKernelGGL(merge_kernel<128>, dim3(rows), dim3(kWave), 0, stream, splits, d.top_k,
+                         ctx->part_stats, ctx->part_keys, o);
   } else {
-    hipLaunchKernelGGL(logits_pass_kernel<256>, grid, dim3(kThreads), 0, stream, logits,
-                       static_cast<int64_t>(d.vocab), splits, d.top_k, ctx->part_stats,
-                       ctx->part_keys, ctx->row_counters, o);
+    hipLaunchKernelGGL(logits_pass_kernel<256>, grid, dim3(kThreads), 0, stream, logits, V,
+                       splits, d.top_k, ctx->part_stats, ctx->part_keys, o);
+    if (splits > 1)
+      hipLaunchKernelGGL(merge_kernel<256>, dim3(rows), dim3(kWave), 0, stream, splits, d.top_k,
+                         ctx->part_stats, ctx->part_keys, o);
   }
   return hipGetLastError();
 }
