@@ -43,14 +43,22 @@ def source_digest() -> str:
 
 def stored_traffic(workload: int):
     """HBM bytes per logits-pass launch from the committed rocprofv3 PMC
-    summary, valid only for the kernel source it was measured on."""
-    p = os.path.join(ROOT, "profiles", "logits_pass_w%d_traffic.json" % workload)
+    summary (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy), valid only
+    for the kernel source it was measured on."""
+    p = os.path.join(ROOT, "profiles", "logits_pass_w%d_traffic.txt" % workload)
     if not os.path.exists(p):
         return None
-    d = json.load(open(p))
-    if d.get("k_logits_sha256_16") != source_digest():
+    kv = {}
+    for line in open(p):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("k_logits_sha256_16") != source_digest():
         return None
-    return d.get("hbm_bytes_per_launch")
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(w, inp, sc, sp, seconds: float):
