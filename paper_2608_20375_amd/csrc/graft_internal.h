@@ -64,6 +64,31 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
 }
 
+// Value of lane (lane ^ m) for m in {1, 2, 4, 8, 16, 32}.  Masks below 16 use
+// DPP lane moves inside a row of 16 (quad_perm for 1 and 2, row_shl/row_shr by
+// 4 with a select, row_ror by 8), 16 uses ds_swizzle's xor mode, 32 a permute.
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v, int m) {
+  const int x = static_cast<int>(v);
+  switch (m) {
+    case 1: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, true));
+    case 2: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, true));
+    case 4: {
+      const int up = __builtin_amdgcn_mov_dpp(x, 0x104, 0xF, 0xF, true);   // lane + 4
+      const int dn = __builtin_amdgcn_mov_dpp(x, 0x114, 0xF, 0xF, true);   // lane - 4
+      return static_cast<uint32_t>((__lane_id() & 4) ? dn : up);
+    }
+    case 8: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, true));
+    case 16: return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(x, 0x401F));
+    default: return static_cast<uint32_t>(__shfl_xor(x, m));
+  }
+}
+
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t v, int m) {
+  const uint32_t lo = xor_lane(static_cast<uint32_t>(v), m);
+  const uint32_t hi = xor_lane(static_cast<uint32_t>(v >> 32), m);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
 // Bitonic sort of 64*E keys held by one wave, element index i = e*64 + lane;
 // afterwards the keys are in descending order of i.
 template <int E>
@@ -90,7 +115,7 @@ __device__ __forceinline__ void wave_sort_desc(uint64_t (&k)[E]) {
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const uint64_t o = shfl_xor_u64(k[e], stride);
+          const uint64_t o = xor_lane_u64(k[e], stride);
           const int i = e * 64 + lane;
           const bool lower = (lane & stride) == 0;
           const bool desc = (i & size) == 0;

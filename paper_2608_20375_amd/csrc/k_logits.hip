@@ -69,26 +69,32 @@ struct WaveBuf {
   float thr;       // wave-uniform: a candidate needs value >= thr
 };
 
-// Sorts a wave's buffer, keeps the best K keys, raises the threshold to the
-// K-th value.
-template <int CAP>
-__device__ __forceinline__ void wave_compact(WaveBuf<CAP> &w, int K) {
-  constexpr int E = CAP / kWave;
+struct Compacted {
+  int count;
+  float thr;
+};
+
+// Sorts the first 64*E entries of a wave's buffer (count of them valid), keeps
+// the best K keys and raises the threshold to the K-th value.  Out of line: it
+// runs a few times per wave at most, and a single copy keeps the offer sites
+// small.
+template <int E>
+__device__ __noinline__ Compacted compact_ool(uint64_t *buf, int count, float thr, int K) {
   const int lane = lane_id();
   uint64_t k[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = e * kWave + lane;
-    k[e] = (i < w.count) ? w.buf[i] : 0ull;
+    k[e] = (i < count) ? buf[i] : 0ull;
   }
   wave_sort_desc<E>(k);
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = e * kWave + lane;
-    if (i < K) w.buf[i] = k[e];
+    if (i < K) buf[i] = k[e];
   }
-  w.count = w.count < K ? w.count : K;
-  if (w.count >= K) {
+  count = count < K ? count : K;
+  if (count >= K) {
     const int src_e = (K - 1) / kWave, src_l = (K - 1) % kWave;
     uint64_t kth = 0;
 #pragma unroll
@@ -96,8 +102,22 @@ __device__ __forceinline__ void wave_compact(WaveBuf<CAP> &w, int K) {
       if (e == src_e) kth = k[e];
     const uint32_t hi = __shfl(static_cast<uint32_t>(kth >> 32), src_l);
     const float t = unordered_f32(hi);
-    w.thr = t > w.thr ? t : w.thr;
+    thr = t > thr ? t : thr;
   }
+  return {count, thr};
+}
+
+// Compaction sized to the number of buffered keys (K <= count rounded up).
+template <int CAP>
+__device__ __forceinline__ void wave_compact(WaveBuf<CAP> &w, int K) {
+  const int need = w.count > K ? w.count : K;
+  Compacted c;
+  if (need <= kWave) c = compact_ool<1>(w.buf, w.count, w.thr, K);
+  else if (need <= 2 * kWave || CAP == 2 * kWave) c = compact_ool<2>(w.buf, w.count, w.thr, K);
+  else c = compact_ool<CAP / kWave>(w.buf, w.count, w.thr, K);
+  // wave-uniform results: keep them in scalar registers
+  w.count = __builtin_amdgcn_readfirstlane(c.count);
+  w.thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(c.thr)));
 }
 
 // Offers one value per lane (valid lanes only) to the wave's buffer.
@@ -116,29 +136,7 @@ __device__ __forceinline__ void wave_offer(WaveBuf<CAP> &w, int K, float v, uint
     n = __popcll(m);
   }
   if (pass) w.buf[w.count + lanes_below(m)] = cand_key(v, id);
-  w.count += n;
-}
-
-// Offers the tile elements flagged in `bits` (bit 8u+e: element e of the
-// lane's u-th vector), one per lane per step, lowest bit first.  The values are
-// read back from an LDS copy of the lane's words (`stage`, [kUnroll][64] uint4)
-// by computed address, which avoids dynamically indexed register arrays and
-// leaves the prefetched global loads of the next tile in flight.
-template <int CAP>
-__device__ __forceinline__ void offer_bits(WaveBuf<CAP> &w, int K, uint32_t bits,
-                                           const uint4 *stage, int64_t base_id) {
-  const int lane = lane_id();
-  const uint32_t *words = reinterpret_cast<const uint32_t *>(stage);
-  while (__ballot(bits != 0) != 0ull) {
-    const bool has = bits != 0;
-    const int j = has ? __builtin_ctz(bits) : 0;
-    const int u = j >> 3, e = j & 7;
-    const int64_t id = base_id + (u * kWave + lane) * 8 + e;
-    const uint32_t word = words[(u * kWave + lane) * 4 + (e >> 1)];
-    const float x = __uint_as_float((e & 1) ? (word & 0xFFFF0000u) : (word << 16));
-    wave_offer<CAP>(w, K, x, static_cast<uint32_t>(id), has);
-    bits &= bits - 1u;
-  }
+  w.count = __builtin_amdgcn_readfirstlane(w.count + n);
 }
 
 // Offers a 64-bit key per lane (used when merging already-sorted lists).
@@ -157,7 +155,7 @@ __device__ __forceinline__ void wave_offer_key(WaveBuf<CAP> &w, int K, uint64_t 
     n = __popcll(m);
   }
   if (pass) w.buf[w.count + lanes_below(m)] = key;
-  w.count += n;
+  w.count = __builtin_amdgcn_readfirstlane(w.count + n);
 }
 
 __device__ __forceinline__ void unpack8(const uint4 q, float (&v)[8]) {
@@ -188,9 +186,8 @@ __device__ __forceinline__ void load_tile(const uint4 *__restrict__ vec, int64_t
 // One tile of loaded data: top-K candidates and softmax statistics.
 template <int CAP, bool MASKED>
 __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t tile_vec,
-                                             int64_t n_vec, int64_t elem0, uint4 *stage,
-                                             LaneStats &st, WaveBuf<CAP> &w, int K,
-                                             float shared_thr) {
+                                             int64_t n_vec, int64_t elem0, LaneStats &st,
+                                             WaveBuf<CAP> &w, int K, float shared_thr) {
   const int lane = lane_id();
   float v[kUnroll][8];
   bool ok[kUnroll];
@@ -216,15 +213,15 @@ __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t 
   // top-K candidates; any wave's threshold bounds the block's K-th value
   if (shared_thr > w.thr) w.thr = shared_thr;
   if (__ballot(tmax >= w.thr) != 0ull) {
-    uint32_t bits = 0;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
+    for (int u = 0; u < kUnroll; ++u) {
+      if (__ballot(ok[u] && sub[u] >= w.thr) != 0ull) {
+        const int64_t id0 = elem0 + (tile_vec + u * kWave + lane) * 8;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        bits |= (ok[u] && v[u][e] >= w.thr) ? (1u << (u * 8 + e)) : 0u;
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) stage[u * kWave + lane] = q[u];
-    offer_bits<CAP>(w, K, bits, stage, elem0 + tile_vec * 8);
+        for (int e = 0; e < 8; ++e)
+          wave_offer<CAP>(w, K, v[u][e], static_cast<uint32_t>(id0 + e), ok[u]);
+      }
+    }
   }
 
   // softmax statistics
@@ -252,15 +249,16 @@ __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t 
 // entries without a barrier; relaxed atomic reads keep the LDS addressing).
 template <int CAP>
 __device__ __forceinline__ void step_tile(const uint4 (&q)[kUnroll], int64_t t, int64_t n_vec,
-                                          int64_t elem0, uint4 *stage, LaneStats &st,
-                                          WaveBuf<CAP> &w, int K, float *s_thr, int wave) {
+                                          int64_t elem0, LaneStats &st, WaveBuf<CAP> &w, int K,
+                                          float *s_thr, int wave) {
   float other = -INFINITY;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i)
     other = fmaxf(other, __hip_atomic_load(&s_thr[i], __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_WORKGROUP));
+  other = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(other)));
   const float before = w.thr;
-  process_tile<CAP, false>(q, t * kTileVec, n_vec, elem0, stage, st, w, K, other);
+  process_tile<CAP, false>(q, t * kTileVec, n_vec, elem0, st, w, K, other);
   if (lane_id() == 0 && w.thr > before)
     __hip_atomic_store(&s_thr[wave], w.thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
@@ -300,7 +298,8 @@ __device__ __forceinline__ void stats_merge(double &mL, double &S, double &T2, d
                                             double S2, double T22) {
   const double M = mL > mL2 ? mL : mL2;
   const double d1 = mL - M, d2 = mL2 - M;
-  const double a1 = exp2(d1), a2 = exp2(d2);
+  const double a1 = static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(d1)));
+  const double a2 = static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(d2)));
   T2 = a1 * (T2 + d1 * S) + a2 * (T22 + d2 * S2);
   S = a1 * S + a2 * S2;
   mL = M;
@@ -352,7 +351,7 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
                    RowOut out) {
   __shared__ uint64_t s_buf[kWaves][CAP];
   __shared__ double s_stats[kWaves][3];
-  __shared__ uint4 s_stage[kWaves][kUnroll * kWave];
+  __shared__ uint64_t s_init[kWaves * kMaxK];
 
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
@@ -383,44 +382,76 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
   __syncthreads();
   const int64_t n_full = n_vec / kTileVec;
   int64_t t = wave;
-  if (t < n_full) {
-    uint4 cur[kUnroll], nxt[kUnroll];
+  uint4 cur[kUnroll], nxt[kUnroll];
+  const bool one = t < n_full, two = t + kWaves < n_full;
+  if (one) {
     load_tile<false>(vec, t * kTileVec, n_vec, cur);
-    // First tile: the K-th largest lane maximum is a lower bound of the K-th
-    // largest element, so it can serve as the threshold from the start.
-    {
-      float tm = kNegBig;
+    load_tile<false>(vec, (two ? t + kWaves : t) * kTileVec, n_vec, nxt);
+  }
+  // Initial threshold, block wide: the K-th largest of the 256 lane maxima
+  // over the waves' first two tiles.  K elements reach it, so it is a lower
+  // bound of the row's K-th largest value.
+  {
+    float tm = kNegBig;
+    if (one) {
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         float vv[8];
         unpack8(cur[u], vv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) tm = fmaxf(tm, vv[e]);
+        if (two) {
+          unpack8(nxt[u], vv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) tm = fmaxf(tm, vv[e]);
+        }
       }
-      uint64_t k1[1] = {cand_key(tm, lane)};
-      wave_sort_desc<1>(k1);
-      const uint32_t hi = __shfl(static_cast<uint32_t>(k1[0] >> 32), K - 1);
-      w.thr = unordered_f32(hi);
     }
+    uint64_t k1[1] = {cand_key(tm, lane)};
+    wave_sort_desc<1>(k1);
+    if (lane < K) s_init[wave * K + lane] = k1[0];
+    __syncthreads();
+    constexpr int E2 = CAP / kWave;   // 4 waves x K <= CAP lane maxima
+    uint64_t k2[E2];
+#pragma unroll
+    for (int e = 0; e < E2; ++e) {
+      const int i = e * kWave + lane;
+      k2[e] = i < kWaves * K ? s_init[i] : 0ull;
+    }
+    wave_sort_desc<E2>(k2);
+    const int src_e = (K - 1) / kWave, src_l = (K - 1) % kWave;
+    uint64_t kth = 0;
+#pragma unroll
+    for (int e = 0; e < E2; ++e)
+      if (e == src_e) kth = k2[e];
+    const uint32_t hi = __shfl(static_cast<uint32_t>(kth >> 32), src_l);
+    w.thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(unordered_f32(hi))));
+    if (w.thr < -1e29f) w.thr = -INFINITY;   // fewer than K real elements seen
+  }
+  if (one) {
     // ping-pong between two register buffers: the loads of tile t + kWaves are
     // in flight while tile t is processed
+    // The prefetch of tile t + kWaves is issued on every step (past the last
+    // tile it re-reads a valid one, a cache hit), so the wait before the
+    // current tile covers only its own loads and never the prefetch.
+    step_tile<CAP>(cur, t, n_vec, elem0, st, w, K, s_thr, wave);
     for (;;) {
-      int64_t tn = t + kWaves;
-      if (tn < n_full) load_tile<false>(vec, tn * kTileVec, n_vec, nxt);
-      step_tile<CAP>(cur, t, n_vec, elem0, s_stage[wave], st, w, K, s_thr, wave);
-      t = tn;
+      t += kWaves;
       if (t >= n_full) break;
-      tn = t + kWaves;
-      if (tn < n_full) load_tile<false>(vec, tn * kTileVec, n_vec, cur);
-      step_tile<CAP>(nxt, t, n_vec, elem0, s_stage[wave], st, w, K, s_thr, wave);
-      t = tn;
+      int64_t tl = t + kWaves < n_full ? t + kWaves : n_full - 1;
+      load_tile<false>(vec, tl * kTileVec, n_vec, cur);
+      step_tile<CAP>(nxt, t, n_vec, elem0, st, w, K, s_thr, wave);
+      t += kWaves;
       if (t >= n_full) break;
+      tl = t + kWaves < n_full ? t + kWaves : n_full - 1;
+      load_tile<false>(vec, tl * kTileVec, n_vec, nxt);
+      step_tile<CAP>(cur, t, n_vec, elem0, st, w, K, s_thr, wave);
     }
   }
   if (t == n_full && n_full * kTileVec < n_vec) {
     uint4 cur[kUnroll];
     load_tile<true>(vec, t * kTileVec, n_vec, cur);
-    process_tile<CAP, true>(cur, t * kTileVec, n_vec, elem0, s_stage[wave], st, w, K, -INFINITY);
+    process_tile<CAP, true>(cur, t * kTileVec, n_vec, elem0, st, w, K, -INFINITY);
   }
   // Misaligned head [0, a0) and tail [a0 + 8 nv_row, V): split 0, wave 0.
   if (split == 0 && wave == 0) {
