@@ -48,15 +48,13 @@ void free_ctx(graft_ctx *c) {
   prof_release(c);
   (void)hipFree(c->part_stats);
   (void)hipFree(c->part_keys);
-  (void)hipFree(c->row_counters);
   (void)hipFree(c->topk_ids);
   (void)hipFree(c->topk_logq);
   (void)hipFree(c->row_stats);
   (void)hipFree(c->sorted_score);
   (void)hipFree(c->sorted_child);
-  (void)hipFree(c->sel_nodes);
-  (void)hipFree(c->sel_scores);
-  (void)hipFree(c->heap);
+  (void)hipFree(c->id_rank);
+  (void)hipFree(c->positive);
   (void)hipFree(c->proj_parent);
   (void)hipFree(c->proj_child);
   (void)hipFree(c->depth_emb);
@@ -110,27 +108,24 @@ int graft_create(const graft_dims *dims, graft_ctx **out) {
   if (!c) return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_create: host allocation failed");
   c->dims = d;
   (void)hipGetDevice(&c->device);
-  const size_t B = d.max_batch, L = d.num_pos, K = d.top_k, N = d.max_nodes;
+  const size_t B = d.max_batch, L = d.num_pos, K = d.top_k;
   c->part_slots = graft::logits_part_slots(d);
   hipError_t e = hipSuccess;
 #define GRAFT_ALLOC(ptr, n)              \
   if (e == hipSuccess) e = dalloc(&(ptr), (n));
   GRAFT_ALLOC(c->part_stats, static_cast<size_t>(c->part_slots) * 3);
   GRAFT_ALLOC(c->part_keys, static_cast<size_t>(c->part_slots) * K);
-  GRAFT_ALLOC(c->row_counters, B * L);
   GRAFT_ALLOC(c->topk_ids, B * L * K);
   GRAFT_ALLOC(c->topk_logq, B * L * K);
   GRAFT_ALLOC(c->row_stats, B * L * 3);
   GRAFT_ALLOC(c->sorted_score, B * L * K * K);
   GRAFT_ALLOC(c->sorted_child, B * L * K * K);
-  GRAFT_ALLOC(c->sel_nodes, B * N);
-  GRAFT_ALLOC(c->sel_scores, B * N);
-  GRAFT_ALLOC(c->heap, B * (N + 1));
+  GRAFT_ALLOC(c->id_rank, B * L * K);
+  GRAFT_ALLOC(c->positive, B * L);
   GRAFT_ALLOC(c->hist_ring, B * d.hist_window);
   GRAFT_ALLOC(c->hist_pos, B);
   GRAFT_ALLOC(c->error_flag, 1);
 #undef GRAFT_ALLOC
-  if (e == hipSuccess) e = hipMemset(c->row_counters, 0, B * L * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(c->error_flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(c->hist_ring, 0, B * d.hist_window * sizeof(int32_t));
   if (e == hipSuccess) e = hipMemset(c->hist_pos, 0, B * sizeof(int32_t));

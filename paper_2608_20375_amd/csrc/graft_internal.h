@@ -44,6 +44,10 @@ __device__ __forceinline__ uint64_t ordered_f64(double x) {
   uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
   return (u & 0x8000000000000000ull) ? ~u : (u | 0x8000000000000000ull);
 }
+__device__ __forceinline__ double unordered_f64(uint64_t k) {
+  const uint64_t u = (k & 0x8000000000000000ull) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+  return __longlong_as_double(static_cast<long long>(u));
+}
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
@@ -87,6 +91,34 @@ __device__ __forceinline__ uint64_t xor_lane_u64(uint64_t v, int m) {
   const uint32_t lo = xor_lane(static_cast<uint32_t>(v), m);
   const uint32_t hi = xor_lane(static_cast<uint32_t>(v >> 32), m);
   return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: Hillis-Steele steps inside
+// rows of 16 lanes (row_shr 1, 2, 4, 8; lanes whose source falls outside the
+// row add 0), then row_bcast:15 adds row 0's total to row 1 and row 2's to row
+// 3, and row_bcast:31 adds lane 31's value to rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);
+  return v;
+}
+// The same over each half-wave (lanes 0-31 and 32-63) separately.
+__device__ __forceinline__ int half_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
+  return v;
+}
+
+__device__ __forceinline__ double xor_lane_f64(double v, int m) {
+  return __longlong_as_double(static_cast<long long>(
+      xor_lane_u64(static_cast<uint64_t>(__double_as_longlong(v)), m)));
 }
 
 // Bitonic sort of 64*E keys held by one wave, element index i = e*64 + lane;
@@ -155,17 +187,14 @@ struct graft_ctx {
   int32_t part_slots;
   double *part_stats;      // [part_slots][3]: mL (log2-scaled max), S, T2
   uint64_t *part_keys;     // [part_slots][K]
-  uint32_t *row_counters;  // [max_batch * L], zero between launches
   // per-round intermediates
   int32_t *topk_ids;       // [max_batch, L, K]
   float *topk_logq;        // [max_batch, L, K]
   float *row_stats;        // [max_batch, L, 3]: lse, maxprob, entropy
   float *sorted_score;     // [max_batch, L, K, K] children of each parent by rank
   uint8_t *sorted_child;   // [max_batch, L, K, K]
-  // selection scratch
-  int32_t *sel_nodes;      // [max_batch, max_nodes] packed node records
-  double *sel_scores;      // [max_batch, max_nodes]
-  int64_t *heap;           // [max_batch, max_nodes + 1] frontier of the serial selector
+  uint8_t *id_rank;        // [max_batch, L, K] rank of each candidate's token id in its depth
+  uint8_t *positive;       // [max_batch, L] 1 if some edge score of that depth is > 0
   // scorer
   float *proj_parent;      // [V, m]
   float *proj_child;       // [V, m]

@@ -21,10 +21,13 @@
 //           members are ranked with the full order); let theta be the N-th;
 //           expand every kept prefix not yet expanded, adding only children
 //           whose score reaches theta (a prefix of each parent's ranked row);
-//           stop when every kept prefix is expanded.
+//           stop when an expansion adds nothing.
 //   A prefix outside the kept set can only gain better competitors, and a
 //   skipped child is worse than theta, which only rises, so the result is the
-//   exact top N.  Iterations <= depth of the tree + 1.
+//   exact top N.  Iterations <= depth of the tree + 1.  The pool is
+//   append-only: dropped prefixes are marked dead and stay in place (so the
+//   children of a prefix always form one contiguous run), and it is compacted
+//   only when an expansion would not fit.
 //   Otherwise (some positive edge score) one thread runs the heap directly.
 //
 // Emission: canonical numbering (depth ascending, token path ascending), token
@@ -38,7 +41,9 @@ namespace {
 constexpr int kSelThreads = 512;
 constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kPoolCap = 4096;
+constexpr int kPerThread = kPoolCap / kSelThreads;
 constexpr int kBins = 2048;
+constexpr int kStageRows = 4096;   // L * K * K edges staged in LDS up to this size
 
 struct SelectArgs {
   int L, K, n_max, words, window;
@@ -46,6 +51,8 @@ struct SelectArgs {
   const float *sorted_score;    // [B, L, K, K]
   const uint8_t *sorted_child;  // [B, L, K, K]
   const int32_t *topk_ids;      // [B, L, K]
+  const uint8_t *id_rank;       // [B, L, K] rank of each candidate's token id in its depth
+  const uint8_t *positive;      // [B, L] some edge score of that depth is > 0
   const int32_t *root_token, *base_pos, *prefix_len, *fixed_budget;
   const float *hist;
   const int32_t *hist_ring;     // [B, window] (used when hist == nullptr)
@@ -53,40 +60,56 @@ struct SelectArgs {
   uint64_t *mask;
   double *node_scores;
   float *saba_state;
+  uint32_t *error_flag;
 };
 
-// Pool entry info: parent + 1 (13 bits) | depth - 1 (6) | slot (6) | expanded (1)
-__device__ __forceinline__ int32_t pinfo(int parent, int depth, int slot, int expanded) {
-  return (parent + 1) | ((depth - 1) << 13) | (slot << 19) | (expanded << 25);
+// Pool entry info: parent + 1 (13 bits) | depth - 1 (6) | slot of the token
+// among its depth's candidates (6) | rank of the token id in that depth (6) |
+// dead (1)
+constexpr uint32_t kDead = 1u << 31;
+__device__ __forceinline__ uint32_t pinfo(int parent, int depth, int slot, int idr) {
+  return static_cast<uint32_t>(parent + 1) | (static_cast<uint32_t>(depth - 1) << 13) |
+         (static_cast<uint32_t>(slot) << 19) | (static_cast<uint32_t>(idr) << 25);
 }
-__device__ __forceinline__ int pi_parent(int32_t v) { return (v & 0x1FFF) - 1; }
-__device__ __forceinline__ int pi_depth(int32_t v) { return ((v >> 13) & 63) + 1; }
-__device__ __forceinline__ int pi_slot(int32_t v) { return (v >> 19) & 63; }
-__device__ __forceinline__ int pi_expanded(int32_t v) { return (v >> 25) & 1; }
+__device__ __forceinline__ int pi_parent(uint32_t v) { return static_cast<int>(v & 0x1FFF) - 1; }
+__device__ __forceinline__ int pi_depth(uint32_t v) { return static_cast<int>((v >> 13) & 63) + 1; }
+__device__ __forceinline__ int pi_slot(uint32_t v) { return static_cast<int>((v >> 19) & 63); }
+__device__ __forceinline__ int pi_idr(uint32_t v) { return static_cast<int>((v >> 25) & 63); }
+__device__ __forceinline__ bool alive(uint32_t v) { return (v & kDead) == 0; }
 
 struct SelMem {
   double p_score[kPoolCap];
-  int32_t p_info[kPoolCap];
+  uint32_t p_info[kPoolCap];
   int32_t map[kPoolCap];
   int32_t aux[kPoolCap + 1];
-  int32_t hist[kBins + 1];
-  int32_t pcnt[kBins + 1];
+  union {
+    struct {
+      int32_t hist[kBins + 1];
+      int32_t pcnt[kBins + 1];
+    } b;
+    struct {                        // serial selector only
+      double score[kMaxNodes + 1];
+      uint32_t info[kMaxNodes + 1];
+    } heap;
+  } u;
   int32_t cand[kMaxL * kMaxK];
   uint8_t idr[kMaxL * kMaxK];
-  // serial heap (fallback)
-  double h_score[kMaxNodes + 1];
-  int32_t h_info[kMaxNodes + 1];
+  // ranked rows of the sequence, staged when they fit
+  alignas(16) float rows[kStageRows];
+  alignas(16) uint8_t rowc[kStageRows];
   // reductions and scalars
+  int32_t dcnt[kMaxL];   // nodes per depth
+  int32_t doff[kMaxL];   // first canonical index of each depth
   int32_t wsum[kSelWaves];
-  double dred[2 * kSelWaves];
-  double saba_u[kMaxGrid];
   double theta;
+  unsigned long long thkey;   // ordered key of theta when a whole bin is kept
+  unsigned long long lomin;   // ordered key of the smallest score appended
   int32_t sc[16];
 };
 
-enum { kNPool = 0, kBudget, kMono, kBstar, kA, kG, kNX, kXfit, kTotal, kMaxDepth, kNSel, kDepthN };
+enum { kNPool = 0, kBudget, kMono, kBstar, kA, kBcnt, kG, kXfit, kMaxDepth, kNSel, kDepthN };
 
-__device__ __forceinline__ int32_t ptoken(const SelMem &s, int K, int32_t info) {
+__device__ __forceinline__ int32_t ptoken(const SelMem &s, int K, uint32_t info) {
   return s.cand[(pi_depth(info) - 1) * K + pi_slot(info)];
 }
 
@@ -94,7 +117,7 @@ __device__ __forceinline__ int32_t ptoken(const SelMem &s, int K, int32_t info) 
 __device__ bool pool_before(const SelMem &s, int K, int a, int b) {
   const double sa = s.p_score[a], sb = s.p_score[b];
   if (sa != sb) return sa > sb;
-  const int32_t ia = s.p_info[a], ib = s.p_info[b];
+  const uint32_t ia = s.p_info[a], ib = s.p_info[b];
   const int da = pi_depth(ia), db = pi_depth(ib);
   if (da != db) return da < db;
   int ta = ptoken(s, K, ia), tb = ptoken(s, K, ib);
@@ -115,12 +138,7 @@ __device__ int block_scan(SelMem &s, int32_t *data, int n) {
   const int lo = tid * per, hi = lo + per < n ? lo + per : n;
   int sum = 0;
   for (int i = lo; i < hi; ++i) sum += data[i];
-  int inc = sum;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int v = __shfl_up(inc, o);
-    if (lane >= o) inc += v;
-  }
+  const int inc = wave_incl_scan(sum);
   if (lane == kWave - 1) s.wsum[wave] = inc;
   __syncthreads();
   int wbase = 0, total = 0;
@@ -139,182 +157,518 @@ __device__ int block_scan(SelMem &s, int32_t *data, int n) {
   return total;
 }
 
-// Block-wide min and max of p_score[0, n).
-__device__ void block_minmax(SelMem &s, int n, double &mn, double &mx) {
-  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  double a = INFINITY, b = -INFINITY;
-  for (int i = tid; i < n; i += kSelThreads) {
-    const double v = s.p_score[i];
-    a = v < a ? v : a;
-    b = v > b ? v : b;
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const double oa = shfl_xor_f64(a, o), ob = shfl_xor_f64(b, o);
-    a = oa < a ? oa : a;
-    b = ob > b ? ob : b;
-  }
-  if (lane == 0) {
-    s.dred[wave] = a;
-    s.dred[kSelWaves + wave] = b;
-  }
-  __syncthreads();
-  mn = s.dred[0];
-  mx = s.dred[kSelWaves];
-  for (int w = 1; w < kSelWaves; ++w) {
-    mn = s.dred[w] < mn ? s.dred[w] : mn;
-    mx = s.dred[kSelWaves + w] > mx ? s.dred[kSelWaves + w] : mx;
-  }
-  __syncthreads();
-}
-
-__device__ __forceinline__ int score_bin(double v, double smax, double scale) {
-  const double f = (smax - v) * scale;
+__device__ __forceinline__ int score_bin(double v, double hi, double scale) {
+  const double f = (hi - v) * scale;
   int b = static_cast<int>(f);
   return b < kBins - 1 ? (b < 0 ? 0 : b) : kBins - 1;
 }
 
-// Keeps the best n_keep entries of the pool (exact), compacts it in pool order
-// and sets s.theta to the score of the last kept entry.
-__device__ void pool_select(SelMem &s, int K, int n_keep) {
-  const int tid = threadIdx.x;
-  const int n = s.sc[kNPool];
-  double smin, smax;
-  block_minmax(s, n, smin, smax);
-  const double scale = smax > smin ? static_cast<double>(kBins) / (smax - smin) : 0.0;
-  for (int i = tid; i <= kBins; i += kSelThreads) s.hist[i] = 0;
-  if (tid == 0) s.sc[kG] = 0;
+// Keeps the best n_keep alive entries of pool[0, n) (exact), marks the others
+// dead and returns the score of the last kept entry.  Requires more than
+// n_keep alive entries, all with scores in [lo, hi], and hist[] cleared (it
+// is left cleared).
+__device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, double hi) {
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
+  for (int i = tid; i < n; i += kSelThreads) {
+    const bool live = alive(s.p_info[i]);
+    const int bin = score_bin(s.p_score[i], hi, scale);
+    if (live) atomicAdd(&s.u.b.hist[bin], 1);
+  }
   __syncthreads();
-  for (int i = tid; i < n; i += kSelThreads)
-    atomicAdd(&s.hist[score_bin(s.p_score[i], smax, scale)], 1);
-  __syncthreads();
-  block_scan(s, s.hist, kBins + 1);   // hist[b] = entries in bins < b
-  for (int b = tid; b < kBins; b += kSelThreads)
-    if (s.hist[b] < n_keep && n_keep <= s.hist[b + 1]) {
-      s.sc[kBstar] = b;
-      s.sc[kA] = s.hist[b];
+  // wave 0: the bin holding the n_keep-th entry (bins are in descending score
+  // order), then clears the histogram for the next selection
+  if (wave == 0) {
+    constexpr int kPer = kBins / kWave;
+    int c[kPer], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      c[j] = s.u.b.hist[lane * kPer + j];
+      sum += c[j];
     }
+    int run = wave_incl_scan(sum) - sum;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      if (run < n_keep && n_keep <= run + c[j]) {
+        s.sc[kBstar] = lane * kPer + j;
+        s.sc[kA] = run;
+        s.sc[kBcnt] = c[j];
+      }
+      run += c[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) s.u.b.hist[lane * kPer + j] = 0;
+    if (lane == 0) {
+      s.sc[kG] = 0;
+      s.thkey = ~0ull;
+    }
+  }
   __syncthreads();
-  const int bstar = s.sc[kBstar], A = s.sc[kA];
-  // boundary bin members, then their exact ranks among themselves
-  for (int i = tid; i < n; i += kSelThreads)
-    if (score_bin(s.p_score[i], smax, scale) == bstar) s.map[atomicAdd(&s.sc[kG], 1)] = i;
+  // entries past the boundary bin die.  When the whole boundary bin is kept,
+  // theta is its smallest score; otherwise its members are listed and ranked.
+  const int bstar = s.sc[kBstar], need = n_keep - s.sc[kA];
+  const bool whole = s.sc[kBcnt] == need;
+  for (int i = tid; i < n; i += kSelThreads) {
+    const uint32_t info = s.p_info[i];
+    const double v = s.p_score[i];
+    const int bin = score_bin(v, hi, scale);
+    if (!alive(info)) continue;
+    if (bin > bstar) s.p_info[i] = info | kDead;
+    else if (bin == bstar) {
+      if (whole) atomicMin(&s.thkey, ordered_f64(v));
+      else s.map[atomicAdd(&s.sc[kG], 1)] = i;
+    }
+  }
   __syncthreads();
-  const int g = s.sc[kG], need = n_keep - A;
-  for (int i = tid; i <= n; i += kSelThreads)
-    s.aux[i] = i < n && score_bin(s.p_score[i], smax, scale) < bstar;
-  __syncthreads();
+  if (whole) return unordered_f64(s.thkey);
+  // exact ranks inside the boundary bin (only the dead bit of p_info changes
+  // here, and the comparisons read the other bits)
+  const int g = s.sc[kG];
   for (int j = tid; j < g; j += kSelThreads) {
     const int e = s.map[j];
     int rank = 0;
     for (int q = 0; q < g; ++q) rank += (q != j) && pool_before(s, K, s.map[q], e);
-    if (rank < need) s.aux[e] = 1;
+    if (rank >= need) atomicOr(&s.p_info[e], kDead);
     if (rank == need - 1) s.theta = s.p_score[e];
   }
   __syncthreads();
-  // stable compaction with parent remapping (parents are always kept)
-  double keep_s[kPoolCap / kSelThreads];
-  int32_t keep_i[kPoolCap / kSelThreads];
-  int keep_to[kPoolCap / kSelThreads];
-  block_scan(s, s.aux, n + 1);        // aux[i] = new index if kept; aux[n] = kept count
-  int c = 0;
+  return s.theta;
+}
+
+// Removes the dead entries of pool[0, n), keeping the order and remapping
+// parents (a kept entry's parent is kept).  Returns the new size; *x_lo is
+// moved to the new index of the first entry at or after it.
+__device__ int pool_compact(SelMem &s, int n, int *x_lo) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i <= n; i += kSelThreads) s.aux[i] = i < n && alive(s.p_info[i]);
+  __syncthreads();
+  const int kept = block_scan(s, s.aux, n + 1);   // aux[i] = new index if kept
+  double keep_s[kPerThread];
+  uint32_t keep_i[kPerThread];
+  int keep_to[kPerThread];
 #pragma unroll
-  for (int k = 0; k < kPoolCap / kSelThreads; ++k) {
+  for (int k = 0; k < kPerThread; ++k) {
     const int i = tid + k * kSelThreads;
     keep_to[k] = -1;
     if (i < n && s.aux[i + 1] != s.aux[i]) {
-      const int32_t info = s.p_info[i];
+      const uint32_t info = s.p_info[i];
       const int p = pi_parent(info);
       keep_s[k] = s.p_score[i];
-      keep_i[k] = pinfo(p < 0 ? -1 : s.aux[p], pi_depth(info), pi_slot(info), pi_expanded(info));
+      keep_i[k] = pinfo(p < 0 ? -1 : s.aux[p], pi_depth(info), pi_slot(info), pi_idr(info));
       keep_to[k] = s.aux[i];
-      ++c;
     }
   }
+  *x_lo = s.aux[*x_lo];
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < kPoolCap / kSelThreads; ++k)
+  for (int k = 0; k < kPerThread; ++k)
     if (keep_to[k] >= 0) {
       s.p_score[keep_to[k]] = keep_s[k];
       s.p_info[keep_to[k]] = keep_i[k];
     }
-  (void)c;
-  if (tid == 0) s.sc[kNPool] = n_keep;
   __syncthreads();
+  return kept;
 }
 
-// Parallel exact top-N for sequences whose edge scores are all <= 0.
-__device__ void select_parallel(SelMem &s, const SelectArgs &a, const float *ss,
-                                const uint8_t *sc, int n_target) {
-  const int tid = threadIdx.x;
-  const int L = a.L, K = a.K;
-  for (int r = tid; r < K; r += kSelThreads) {
-    s.p_score[r] = static_cast<double>(ss[r]);
-    s.p_info[r] = pinfo(-1, 1, sc[r], 0);
+// Ranked-row helpers for K % 4 == 0 with kv = K / 4 groups of four, KV the
+// next power of two >= kv.  Every load is issued unconditionally (clamped to
+// the row) before any use, so one memory round trip covers the row.
+
+// Number of children r < K with ps + row[r] >= theta.
+template <int KV>
+__device__ __forceinline__ int count_reach(const float *row, int kv, double ps, double theta,
+                                           float &last) {
+  const float4 *r4 = reinterpret_cast<const float4 *>(row);
+  float4 v[KV];
+#pragma unroll
+  for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
+  last = v[KV - 1].w;   // group kv - 1 (clamped), element K - 1
+  int c = 0;
+#pragma unroll
+  for (int q = 0; q < KV; ++q) {
+    const int g = (ps + static_cast<double>(v[q].x) >= theta) +
+                  (ps + static_cast<double>(v[q].y) >= theta) +
+                  (ps + static_cast<double>(v[q].z) >= theta) +
+                  (ps + static_cast<double>(v[q].w) >= theta);
+    c += q < kv ? g : 0;
   }
-  if (tid == 0) {
-    s.sc[kNPool] = K;
-    s.theta = -INFINITY;
+  return c;
+}
+
+// Adds the first cnt children of a row (scores ps + row[r]) to the histogram.
+template <int KV>
+__device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv, int cnt,
+                                             double ps, double hi, double scale) {
+  const float4 *r4 = reinterpret_cast<const float4 *>(row);
+  float4 v[KV];
+#pragma unroll
+  for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
+#pragma unroll
+  for (int q = 0; q < KV; ++q) {
+    if (q * 4 >= cnt) break;
+    const float f[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (q * 4 + k < cnt)
+        atomicAdd(&s.u.b.hist[score_bin(ps + static_cast<double>(f[k]), hi, scale)], 1);
+  }
+}
+
+// Appends the first cnt children of a row at dst (scores ps + row[r], info
+// with parent x at depth d + 1).
+template <int KV>
+__device__ __forceinline__ void append_children(SelMem &s, const float *row, const uint8_t *rowc,
+                                                int kv, int cnt, int dst, int x, int d,
+                                                double ps, const uint8_t *idr) {
+  const float4 *r4 = reinterpret_cast<const float4 *>(row);
+  const uint32_t *c4 = reinterpret_cast<const uint32_t *>(rowc);
+  float4 v[KV];
+  uint32_t w[KV];
+#pragma unroll
+  for (int q = 0; q < KV; ++q) {
+    v[q] = r4[q < kv ? q : kv - 1];
+    w[q] = c4[q < kv ? q : kv - 1];
+  }
+#pragma unroll
+  for (int q = 0; q < KV; ++q) {
+    if (q * 4 >= cnt) break;
+    const float f[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int r = q * 4 + k;
+      if (r < cnt) {
+        const int slot = static_cast<int>((w[q] >> (8 * k)) & 0xFF);
+        s.p_score[dst + r] = ps + static_cast<double>(f[k]);
+        s.p_info[dst + r] = pinfo(x, d + 1, slot, idr[slot]);
+      }
+    }
+  }
+}
+
+// Children of pool entry x (alive, depth < L) that reach theta, and the
+// smallest child score (+inf without children).
+struct Counted {
+  int c;
+  double vmin;
+};
+__device__ __forceinline__ Counted entry_count(const SelMem &s, const float *rs, int x, int L,
+                                               int K, int kv, int KVP, double theta) {
+  const uint32_t info = s.p_info[x];
+  const double ps = s.p_score[x];
+  if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
+  const float *row = rs + (pi_depth(info) * K + pi_slot(info)) * K;
+  float last = 0.f;
+  int c = 0;
+  if (KVP == 1) c = count_reach<1>(row, kv, ps, theta, last);
+  else if (KVP == 2) c = count_reach<2>(row, kv, ps, theta, last);
+  else if (KVP == 4) c = count_reach<4>(row, kv, ps, theta, last);
+  else if (KVP == 8) c = count_reach<8>(row, kv, ps, theta, last);
+  else if (KVP == 16) c = count_reach<16>(row, kv, ps, theta, last);
+  else {
+    for (int r = 0; r < K; ++r) c += ps + static_cast<double>(row[r]) >= theta;
+    last = row[K - 1];
+  }
+  return {c, ps + static_cast<double>(last)};
+}
+
+// A lower bound of the N-th best score, from a histogram over the alive pool
+// entries and the counted children (aux[i] of them) of every entry of
+// [x_lo, n): these are all distinct prefixes, so the score at the start of the
+// bin that holds the N-th of them bounds the final N-th score from below.
+// All the scores lie in [lo, hi]; hist[] is cleared before and after.
+template <bool kLds>
+__device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K, int kv, int KVP, int n, int x_lo,
+                              int i0, int per, int n_keep, double lo, double hi) {
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const float *rs = kLds ? s.rows : gs;
+  const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
+  for (int i = tid; i < n; i += kSelThreads) {
+    const bool live = alive(s.p_info[i]);
+    const int bin = score_bin(s.p_score[i], hi, scale);
+    if (live) atomicAdd(&s.u.b.hist[bin], 1);
+  }
+  const int m = n - x_lo;
+  for (int k = 0; k < per; ++k) {
+    const int i = i0 + k;
+    if (i >= m) break;
+    const int c = s.aux[i];
+    if (c == 0) continue;
+    const int x = x_lo + i;
+    const uint32_t info = s.p_info[x];
+    const float *row = rs + (pi_depth(info) * K + pi_slot(info)) * K;
+    const double ps = s.p_score[x];
+    if (KVP == 1) bin_children<1>(s, row, kv, c, ps, hi, scale);
+    else if (KVP == 2) bin_children<2>(s, row, kv, c, ps, hi, scale);
+    else if (KVP == 4) bin_children<4>(s, row, kv, c, ps, hi, scale);
+    else if (KVP == 8) bin_children<8>(s, row, kv, c, ps, hi, scale);
+    else if (KVP == 16) bin_children<16>(s, row, kv, c, ps, hi, scale);
+    else
+      for (int r = 0; r < c; ++r)
+        atomicAdd(&s.u.b.hist[score_bin(ps + static_cast<double>(row[r]), hi, scale)], 1);
   }
   __syncthreads();
-  for (;;) {
-    if (s.sc[kNPool] > n_target) pool_select(s, K, n_target);
-    const int n = s.sc[kNPool];
-    // unexpanded prefixes that can still grow
-    for (int i = tid; i < n; i += kSelThreads) {
-      const int32_t info = s.p_info[i];
-      s.aux[i] = !pi_expanded(info) && pi_depth(info) < L;
+  if (wave == 0) {
+    constexpr int kPer = kBins / kWave;
+    int c[kPer], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      c[j] = s.u.b.hist[lane * kPer + j];
+      sum += c[j];
     }
-    __syncthreads();
-    const int nx = block_scan(s, s.aux, n);
-    if (nx == 0) break;
-    for (int i = tid; i < n; i += kSelThreads) {
-      const int32_t info = s.p_info[i];
-      if (!pi_expanded(info) && pi_depth(info) < L) s.map[s.aux[i]] = i;
+    int run = wave_incl_scan(sum) - sum;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      if (run < n_keep && n_keep <= run + c[j]) s.sc[kBstar] = lane * kPer + j;
+      run += c[j];
     }
-    __syncthreads();
-    // children of X[j] reaching theta: a prefix of its ranked row; count them
-    const double theta = s.theta;
-    for (int j = tid; j <= nx; j += kSelThreads) s.aux[j] = 0;
-    __syncthreads();
-    for (int t = tid; t < nx * K; t += kSelThreads) {
-      const int j = t / K, r = t % K;
-      const int x = s.map[j];
-      const int32_t info = s.p_info[x];
-      const int64_t row = (static_cast<int64_t>(pi_depth(info)) * K + pi_slot(info)) * K;
-      const bool pass = s.p_score[x] + static_cast<double>(ss[row + r]) >= theta;
-      const bool next = r + 1 < K && s.p_score[x] + static_cast<double>(ss[row + r + 1]) >= theta;
-      if (pass && !next) s.aux[j] = r + 1;
-    }
-    __syncthreads();
-    // aux[nx] holds the sum; expand the longest prefix of X that fits
-    const int total = block_scan(s, s.aux, nx + 1);
-    const int room = kPoolCap - n;
-    if (tid == 0) s.sc[kXfit] = nx;
-    __syncthreads();
-    if (total > room)
-      for (int j = tid; j < nx; j += kSelThreads)
-        if (s.aux[j] <= room && s.aux[j + 1] > room) s.sc[kXfit] = j;
-    __syncthreads();
-    const int xfit = s.sc[kXfit];
-    const int added = s.aux[xfit];
-    for (int t = tid; t < xfit * K; t += kSelThreads) {
-      const int j = t / K, r = t % K;
-      const int cnt = s.aux[j + 1] - s.aux[j];
-      if (r >= cnt) continue;
-      const int x = s.map[j];
-      const int32_t info = s.p_info[x];
-      const int d = pi_depth(info);
-      const int64_t row = (static_cast<int64_t>(d) * K + pi_slot(info)) * K;
-      const int dst = n + s.aux[j] + r;
-      s.p_score[dst] = s.p_score[x] + static_cast<double>(ss[row + r]);
-      s.p_info[dst] = pinfo(x, d + 1, sc[row + r], 0);
-    }
-    __syncthreads();
-    for (int j = tid; j < xfit; j += kSelThreads) s.p_info[s.map[j]] |= 1 << 25;
-    if (tid == 0) s.sc[kNPool] = n + added;
-    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) s.u.b.hist[lane * kPer + j] = 0;
   }
+  __syncthreads();
+  if (scale == 0.0) return -INFINITY;
+  // every binned score in bins <= bstar exceeds hi - (bstar + 1) / scale up to
+  // rounding, which the margin covers
+  const double edge = hi - static_cast<double>(s.sc[kBstar] + 1) / scale;
+  return edge - 1e-9 * (fabs(edge) + fabs(hi) + 1.0);
+}
+
+// Appends the first cnt children of pool entry x at dst and lowers s.lomin
+// to the last (smallest) of them.
+__device__ __forceinline__ void entry_append(SelMem &s, const float *rs, const uint8_t *rc, int x,
+                                             int K, int kv, int KVP, int cnt, int dst) {
+  const uint32_t info = s.p_info[x];
+  const int d = pi_depth(info);
+  const int row = (d * K + pi_slot(info)) * K;
+  const double ps = s.p_score[x];
+  const uint8_t *idr = s.idr + d * K;
+  if (KVP == 1) append_children<1>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
+  else if (KVP == 2) append_children<2>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
+  else if (KVP == 4) append_children<4>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
+  else if (KVP == 8) append_children<8>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
+  else if (KVP == 16) append_children<16>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
+  else
+    for (int r = 0; r < cnt; ++r) {
+      const int slot = rc[row + r];
+      s.p_score[dst + r] = ps + static_cast<double>(rs[row + r]);
+      s.p_info[dst + r] = pinfo(x, d + 1, slot, idr[slot]);
+    }
+  atomicMin(&s.lomin, ordered_f64(ps + static_cast<double>(rs[row + cnt - 1])));
+}
+
+// Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
+// alive unexpanded entry lies in [x_lo, n).  kLds: the ranked rows are staged
+// in LDS (s.rows / s.rowc), else read from gs / gc.
+template <bool kLds>
+__device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, const float *gs,
+                               const uint8_t *gc, int n_target) {
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int L = a.L, K = a.K;
+  const float *rs = kLds ? s.rows : gs;
+  const uint8_t *rc = kLds ? s.rowc : gc;
+  // vector path: K % 4 == 0, kv = K / 4 groups, KVP = next power of two
+  const int kv = K / 4;
+  const int KVP = (K & 3) ? 0 : kv <= 1 ? 1 : kv <= 2 ? 2 : kv <= 4 ? 4 : kv <= 8 ? 8 : 16;
+  for (int r = tid; r < K; r += kSelThreads) {
+    const int slot = rc[r];
+    s.p_score[r] = static_cast<double>(rs[r]);
+    s.p_info[r] = pinfo(-1, 1, slot, s.idr[slot]);
+  }
+  for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
+  if (tid == 0) s.lomin = ordered_f64(static_cast<double>(rs[K - 1]));
+  __syncthreads();
+  // every prefix scores at most its depth-1 ancestor, so at most the best
+  // depth-1 prefix, which is never dropped
+  const double hi = static_cast<double>(rs[0]);
+  double theta = -INFINITY;
+  bool pruned = false;
+  int n = K, n_alive = K, x_lo = 0;
+  for (;;) {
+    if (n_alive > n_target) {
+      // all alive scores are >= theta (or >= the smallest appended score)
+      const double lo = theta > -INFINITY ? theta : unordered_f64(s.lomin);
+      theta = pool_select(s, K, n, n_target, lo, hi);
+      n_alive = n_target;
+    }
+    // children reaching theta of each entry of [x_lo, n): this thread counts
+    // a contiguous run of entries into aux, then a block scan gives offsets
+    const int m = n - x_lo;
+    const int per = (m + kSelThreads - 1) / kSelThreads;   // <= kPerThread
+    const int i0 = tid * per;
+    int sum = 0;
+    double vmin = INFINITY;
+    for (int k = 0; k < per; ++k) {
+      const int i = i0 + k;
+      if (i >= m) break;
+      const Counted e = entry_count(s, rs, x_lo + i, L, K, kv, KVP, theta);
+      s.aux[i] = e.c;
+      sum += e.c;
+      vmin = e.vmin < vmin ? e.vmin : vmin;
+    }
+    const int inc = wave_incl_scan(sum);
+    if (lane == kWave - 1) s.wsum[wave] = inc;
+    if (theta == -INFINITY) {
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const double ov = xor_lane_f64(vmin, o);
+        vmin = ov < vmin ? ov : vmin;
+      }
+      if (lane == 0) atomicMin(&s.lomin, ordered_f64(vmin));
+    }
+    __syncthreads();
+    int base = 0, added = 0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      const int v = s.wsum[w];
+      base += w < wave ? v : 0;
+      added += v;
+    }
+    if (added == 0) break;
+    if (!pruned && n_alive + added > n_target && (theta == -INFINITY || n + added > kPoolCap)) {
+      // many children: bound the N-th score by a histogram over the pool and
+      // the children, then count again against the tighter bound
+      const double lo = theta > -INFINITY ? theta : unordered_f64(s.lomin);
+      const double bound = prune_bound<kLds>(s, gs, K, kv, KVP, n, x_lo, i0, per, n_target, lo, hi);
+      pruned = true;
+      if (bound > theta) {
+        theta = bound;
+        continue;
+      }
+    }
+    pruned = false;
+    const bool fit = n + added <= kPoolCap;
+    if (!fit && n_alive < n) {
+      // the children do not fit: drop the dead entries and count again
+      __syncthreads();                                  // wsum is reused
+      n = pool_compact(s, n, &x_lo);
+      n_alive = n;
+      continue;
+    }
+    int lim = m, dst = n + base + inc - sum;
+    if (!fit) {
+      // expand the longest run of [x_lo, n) whose children fit
+      if (tid == 0) s.aux[m] = 0;
+      __syncthreads();
+      block_scan(s, s.aux, m + 1);                      // aux[i] = offset, aux[m] = total
+      const int room = kPoolCap - n;
+      if (tid == 0) s.sc[kXfit] = m;
+      __syncthreads();
+      for (int i = tid; i < m; i += kSelThreads)
+        if (s.aux[i] <= room && s.aux[i + 1] > room) s.sc[kXfit] = i;
+      __syncthreads();
+      lim = s.sc[kXfit];
+      dst = n + s.aux[i0 < m ? i0 : m];
+    }
+    const int grown = fit ? added : s.aux[lim];
+    if (grown == 0) {               // cannot happen with n_alive <= N_max <= kPoolCap / 4
+      if (tid == 0) atomicOr(a.error_flag, 2u);
+      break;
+    }
+    for (int k = 0; k < per; ++k) {
+      const int i = i0 + k;
+      if (i >= lim) break;
+      const int c = fit ? s.aux[i] : s.aux[i + 1] - s.aux[i];
+      if (c > 0) entry_append(s, rs, rc, x_lo + i, K, kv, KVP, c, dst);
+      dst += c;
+    }
+    __syncthreads();
+    n += grown;
+    n_alive += grown;
+    x_lo += lim;
+  }
+  if (tid == 0) s.sc[kNSel] = n_alive;
+  // cleared scratch for canon_preorder (the caller's barrier publishes it)
+  for (int i = tid; i < n; i += kSelThreads) s.aux[i] = 0;
+  for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
+  for (int i = tid; i < kMaxL; i += kSelThreads) s.dcnt[i] = 0;
+  return n;
+}
+
+// Canonical numbering for the parallel selector's pool, where the children of
+// a node occupy one contiguous run (dead entries included).  The canonical
+// order is depth ascending, then token path ascending; among nodes of one
+// depth the token-path order is the depth-first preorder that visits children
+// by increasing token id.  The preorder position of a node is the number of
+// its proper ancestors plus, over the node and its ancestors, the sizes of the
+// subtrees of their siblings with smaller token ids.  Needs aux[0, n),
+// hist[0, kBins) and dcnt[] cleared; leaves map[i] = canonical index.
+__device__ void canon_preorder(SelMem &s, int L, int K, int n, int n_sel) {
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  int32_t *bits = s.u.b.hist, *pcnt = s.u.b.pcnt;
+  // subtree sizes (aux) and nodes per depth
+  for (int i = tid; i < n; i += kSelThreads) {
+    const uint32_t info = s.p_info[i];
+    if (!alive(info)) continue;
+    atomicAdd(&s.dcnt[pi_depth(info) - 1], 1);
+    // parents precede their children in the pool
+    for (int j = i; j >= 0 && j <= i; j = pi_parent(s.p_info[j])) atomicAdd(&s.aux[j], 1);
+  }
+  __syncthreads();
+  // map[i] = sizes of the subtrees of i's siblings with smaller token ids;
+  // siblings lie within K entries of i
+  for (int i = tid; i < n; i += kSelThreads) {
+    const uint32_t info = s.p_info[i];
+    if (!alive(info)) continue;
+    const int p = pi_parent(info), mine = pi_idr(info);
+    const int lo = i - K + 1 > 0 ? i - K + 1 : 0, hi = i + K < n ? i + K : n;
+    int left = 0;
+    for (int j0 = lo; j0 < hi; j0 += 16) {
+      uint32_t o[16];
+      int z[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int j = j0 + k < hi ? j0 + k : i;
+        o[k] = s.p_info[j];
+        z[k] = s.aux[j];
+      }
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int sib = static_cast<int>(alive(o[k])) & static_cast<int>(pi_parent(o[k]) == p) &
+                        static_cast<int>(pi_idr(o[k]) < mine);
+        left += sib ? z[k] : 0;
+      }
+    }
+    s.map[i] = left;
+  }
+  __syncthreads();
+  // preorder positions; one bit per node in its depth's bitmap of positions
+  const int W = (n_sel + 31) / 32;                 // <= 32 words per depth
+  int pre[kPerThread];
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int i = tid + k * kSelThreads;
+    pre[k] = -1;
+    if (i >= n) continue;
+    const uint32_t info = s.p_info[i];
+    if (!alive(info)) continue;
+    int acc = pi_depth(info) - 1;
+    for (int j = i; j >= 0 && j <= i; j = pi_parent(s.p_info[j])) acc += s.map[j];
+    pre[k] = acc;
+    atomicOr(reinterpret_cast<uint32_t *>(&bits[(pi_depth(info) - 1) * W + (acc >> 5)]),
+             1u << (acc & 31));
+  }
+  __syncthreads();
+  // per depth: popcount prefix over its bitmap words (a half-wave per depth),
+  // and the first canonical index of each depth (wave 0)
+  for (int t = tid; t < L * 32; t += kSelThreads) {
+    const int d = t >> 5, w = t & 31;
+    const int c = w < W ? __popc(static_cast<uint32_t>(bits[d * W + w])) : 0;
+    const int incl = half_incl_scan(c);
+    if (w < W) pcnt[d * W + w] = incl - c;
+  }
+  if (wave == 0) {
+    const int c = lane < L ? s.dcnt[lane] : 0;
+    const int incl = wave_incl_scan(c);
+    if (lane < L) s.doff[lane] = incl - c;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    if (pre[k] < 0) continue;
+    const int i = tid + k * kSelThreads;
+    const int d0 = pi_depth(s.p_info[i]) - 1, q = pre[k];
+    const uint32_t word = static_cast<uint32_t>(bits[d0 * W + (q >> 5)]);
+    s.map[i] = s.doff[d0] + pcnt[d0 * W + (q >> 5)] + __popc(word & ((1u << (q & 31)) - 1u));
+  }
+  __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
@@ -322,18 +676,19 @@ __device__ void select_parallel(SelMem &s, const SelectArgs &a, const float *ss,
 // Heap entries point at a (parent, rank) stream; popped nodes are written to
 // the pool arrays in pop order (parents before children).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int32_t hinfo(int parent, int rank, int slot, int depth) {
-  return ((parent + 1) << 18) | (rank << 12) | (slot << 6) | (depth - 1);
+__device__ __forceinline__ uint32_t hinfo(int parent, int rank, int slot, int depth) {
+  return (static_cast<uint32_t>(parent + 1) << 18) | (static_cast<uint32_t>(rank) << 12) |
+         (static_cast<uint32_t>(slot) << 6) | static_cast<uint32_t>(depth - 1);
 }
-__device__ __forceinline__ int hi_parent(int32_t v) { return (v >> 18) - 1; }
-__device__ __forceinline__ int hi_rank(int32_t v) { return (v >> 12) & 63; }
-__device__ __forceinline__ int hi_slot(int32_t v) { return (v >> 6) & 63; }
-__device__ __forceinline__ int hi_depth(int32_t v) { return (v & 63) + 1; }
+__device__ __forceinline__ int hi_parent(uint32_t v) { return static_cast<int>(v >> 18) - 1; }
+__device__ __forceinline__ int hi_rank(uint32_t v) { return static_cast<int>((v >> 12) & 63); }
+__device__ __forceinline__ int hi_slot(uint32_t v) { return static_cast<int>((v >> 6) & 63); }
+__device__ __forceinline__ int hi_depth(uint32_t v) { return static_cast<int>(v & 63) + 1; }
 
 __device__ bool heap_before(const SelMem &s, int K, int a, int b) {
-  const double sa = s.h_score[a], sb = s.h_score[b];
+  const double sa = s.u.heap.score[a], sb = s.u.heap.score[b];
   if (sa != sb) return sa > sb;
-  const int32_t ia = s.h_info[a], ib = s.h_info[b];
+  const uint32_t ia = s.u.heap.info[a], ib = s.u.heap.info[b];
   const int da = hi_depth(ia), db = hi_depth(ib);
   if (da != db) return da < db;
   int ta = s.cand[(da - 1) * K + hi_slot(ia)], tb = s.cand[(db - 1) * K + hi_slot(ib)];
@@ -348,18 +703,18 @@ __device__ bool heap_before(const SelMem &s, int K, int a, int b) {
 }
 
 __device__ void heap_swap(SelMem &s, int i, int j) {
-  const double sc = s.h_score[i];
-  s.h_score[i] = s.h_score[j];
-  s.h_score[j] = sc;
-  const int32_t in = s.h_info[i];
-  s.h_info[i] = s.h_info[j];
-  s.h_info[j] = in;
+  const double sc = s.u.heap.score[i];
+  s.u.heap.score[i] = s.u.heap.score[j];
+  s.u.heap.score[j] = sc;
+  const uint32_t in = s.u.heap.info[i];
+  s.u.heap.info[i] = s.u.heap.info[j];
+  s.u.heap.info[j] = in;
 }
 
-__device__ void heap_push(SelMem &s, int K, int &n, double score, int32_t info) {
+__device__ void heap_push(SelMem &s, int K, int &n, double score, uint32_t info) {
   int i = n++;
-  s.h_score[i] = score;
-  s.h_info[i] = info;
+  s.u.heap.score[i] = score;
+  s.u.heap.info[i] = info;
   while (i > 0) {
     const int p = (i - 1) >> 1;
     if (!heap_before(s, K, i, p)) break;
@@ -371,8 +726,8 @@ __device__ void heap_push(SelMem &s, int K, int &n, double score, int32_t info) 
 __device__ void heap_pop_root(SelMem &s, int K, int &n) {
   --n;
   if (n == 0) return;
-  s.h_score[0] = s.h_score[n];
-  s.h_info[0] = s.h_info[n];
+  s.u.heap.score[0] = s.u.heap.score[n];
+  s.u.heap.info[0] = s.u.heap.info[n];
   int i = 0;
   for (;;) {
     const int l = 2 * i + 1, r = l + 1;
@@ -385,31 +740,80 @@ __device__ void heap_pop_root(SelMem &s, int K, int &n) {
   }
 }
 
-__device__ void select_serial(SelMem &s, const SelectArgs &a, const float *ss, const uint8_t *sc,
+__device__ void select_serial(SelMem &s, const SelectArgs &a, const float *rs, const uint8_t *rc,
                               int n_target) {
   const int L = a.L, K = a.K;
   int hn = 0, n_sel = 0;
-  if (n_target > 0) heap_push(s, K, hn, static_cast<double>(ss[0]), hinfo(-1, 0, sc[0], 1));
+  if (n_target > 0) heap_push(s, K, hn, static_cast<double>(rs[0]), hinfo(-1, 0, rc[0], 1));
   while (n_sel < n_target && hn > 0) {
-    const double score = s.h_score[0];
-    const int32_t info = s.h_info[0];
+    const double score = s.u.heap.score[0];
+    const uint32_t info = s.u.heap.info[0];
     heap_pop_root(s, K, hn);
     const int p = hi_parent(info), r = hi_rank(info), slot = hi_slot(info), d = hi_depth(info);
     const int i = n_sel++;
     s.p_score[i] = score;
-    s.p_info[i] = pinfo(p, d, slot, 1);
+    s.p_info[i] = pinfo(p, d, slot, s.idr[(d - 1) * K + slot]);
     if (r + 1 < K) {   // next sibling under the same parent
       const int pslot = p < 0 ? 0 : pi_slot(s.p_info[p]);
       const double pscore = p < 0 ? 0.0 : s.p_score[p];
-      const int64_t off = (static_cast<int64_t>(d - 1) * K + pslot) * K + (r + 1);
-      heap_push(s, K, hn, pscore + static_cast<double>(ss[off]), hinfo(p, r + 1, sc[off], d));
+      const int off = ((d - 1) * K + pslot) * K + (r + 1);
+      heap_push(s, K, hn, pscore + static_cast<double>(rs[off]), hinfo(p, r + 1, rc[off], d));
     }
     if (d < L) {       // best child of the new node
-      const int64_t off = (static_cast<int64_t>(d) * K + slot) * K;
-      heap_push(s, K, hn, score + static_cast<double>(ss[off]), hinfo(i, 0, sc[off], d + 1));
+      const int off = (d * K + slot) * K;
+      heap_push(s, K, hn, score + static_cast<double>(rs[off]), hinfo(i, 0, rc[off], d + 1));
     }
   }
   s.sc[kNPool] = n_sel;
+  s.sc[kNSel] = n_sel;
+}
+
+// Canonical numbering for the serial selector's pool (pop order, no dead
+// entries): depth by depth, a node's key is (rank of its parent within the
+// parent's depth, rank of its token id).  Keys are set in a bitmap; a node's
+// rank within its depth is the number of set bits below its key (prefix sum
+// of word popcounts).  aux[i] = rank within depth, map[i] = canonical index.
+__device__ void canon_by_depth(SelMem &s, int K, int n) {
+  const int tid = threadIdx.x;
+  int32_t *bits = s.u.b.hist, *pcnt = s.u.b.pcnt;
+  if (tid == 0) s.sc[kMaxDepth] = 0;
+  __syncthreads();
+  for (int i = tid; i < n; i += kSelThreads) atomicMax(&s.sc[kMaxDepth], pi_depth(s.p_info[i]));
+  __syncthreads();
+  const int max_depth = s.sc[kMaxDepth];
+  int offset = 0, n_prev = 1;
+  for (int d = 1; d <= max_depth; ++d) {
+    const int nwords = (n_prev * K + 31) / 32;
+    for (int w = tid; w < nwords; w += kSelThreads) bits[w] = 0;
+    if (tid == 0) s.sc[kDepthN] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += kSelThreads) {
+      const uint32_t info = s.p_info[i];
+      if (pi_depth(info) != d) continue;
+      const int p = pi_parent(info);
+      const int key = (p < 0 ? 0 : s.aux[p]) * K + pi_idr(info);
+      atomicOr(reinterpret_cast<uint32_t *>(&bits[key >> 5]), 1u << (key & 31));
+      atomicAdd(&s.sc[kDepthN], 1);
+    }
+    __syncthreads();
+    const int nd = s.sc[kDepthN];
+    for (int w = tid; w < nwords; w += kSelThreads) pcnt[w] = __popc(static_cast<uint32_t>(bits[w]));
+    __syncthreads();
+    block_scan(s, pcnt, nwords);
+    for (int i = tid; i < n; i += kSelThreads) {
+      const uint32_t info = s.p_info[i];
+      if (pi_depth(info) != d) continue;
+      const int p = pi_parent(info);
+      const int key = (p < 0 ? 0 : s.aux[p]) * K + pi_idr(info);
+      const uint32_t word = static_cast<uint32_t>(bits[key >> 5]);
+      const int rank = pcnt[key >> 5] + __popc(word & ((1u << (key & 31)) - 1u));
+      s.aux[i] = rank;          // parents (depth d-1) are not touched here
+      s.map[i] = offset + rank;
+    }
+    __syncthreads();
+    offset += nd;
+    n_prev = nd;
+  }
 }
 
 __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaParams sp,
@@ -421,36 +825,72 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaP
   const float *ss = a.sorted_score + static_cast<int64_t>(b) * L * K * K;
   const uint8_t *sc = a.sorted_child + static_cast<int64_t>(b) * L * K * K;
 
-  // candidates, their rank by token id, and the sign of the edge scores
-  for (int i = tid; i < L * K; i += kSelThreads)
-    s.cand[i] = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
-  if (tid == 0) s.sc[kMono] = 1;
-  __syncthreads();
+  // candidates and their rank by token id
   for (int i = tid; i < L * K; i += kSelThreads) {
-    const int l = i / K;
-    int r = 0;
-    for (int k = 0; k < K; ++k) r += s.cand[l * K + k] < s.cand[i];
-    s.idr[i] = static_cast<uint8_t>(r);
+    s.cand[i] = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
+    s.idr[i] = a.id_rank[static_cast<int64_t>(b) * L * K + i];
   }
-  for (int i = tid; i < L * K * K; i += kSelThreads) {
-    const int l = i / (K * K), p = (i / K) % K;
-    if ((l > 0 || p == 0) && ss[i] > 0.f) s.sc[kMono] = 0;
+  // waves 1.. stage the ranked rows (16-byte loads, all issued before the
+  // stores) while wave 0 computes the budget
+  const bool staged = L * K * K <= kStageRows;
+  constexpr int kStageThreads = kSelThreads - kWave;
+  if (staged && tid >= kWave && (L * K * K) % 16 != 0) {
+    for (int i = tid - kWave; i < L * K * K; i += kStageThreads) {
+      s.rows[i] = ss[i];
+      s.rowc[i] = sc[i];
+    }
+  } else if (staged && tid >= kWave) {
+    // L*K*K is a multiple of 16 here, so both sequences' bases are 16-byte aligned
+    constexpr int kF4 = (kStageRows / 4 + kStageThreads - 1) / kStageThreads;
+    constexpr int kB16 = (kStageRows / 16 + kStageThreads - 1) / kStageThreads;
+    const int t = tid - kWave;
+    const int nf4 = L * K * K / 4, nb16 = L * K * K / 16;
+    const float4 *src_f = reinterpret_cast<const float4 *>(ss);
+    const uint4 *src_b = reinterpret_cast<const uint4 *>(sc);
+    float4 vf[kF4];
+    uint4 vb[kB16];
+#pragma unroll
+    for (int k = 0; k < kF4; ++k) {
+      const int i = t + k * kStageThreads;
+      vf[k] = src_f[i < nf4 ? i : nf4 - 1];
+    }
+#pragma unroll
+    for (int k = 0; k < kB16; ++k) {
+      const int i = t + k * kStageThreads;
+      vb[k] = src_b[i < nb16 ? i : nb16 - 1];
+    }
+#pragma unroll
+    for (int k = 0; k < kF4; ++k)
+      if (t + k * kStageThreads < nf4) reinterpret_cast<float4 *>(s.rows)[t + k * kStageThreads] = vf[k];
+#pragma unroll
+    for (int k = 0; k < kB16; ++k)
+      if (t + k * kStageThreads < nb16) reinterpret_cast<uint4 *>(s.rowc)[t + k * kStageThreads] = vb[k];
   }
 
   // ---------------- SABA (wave 0) ----------------
   if (tid < kWave) {
+    const int lane = tid;
+    const bool pos = lane < L && a.positive[static_cast<int64_t>(b) * L + lane] != 0;
     double hist;
     if (a.hist) {
       hist = static_cast<double>(a.hist[b]);
     } else {
-      int64_t sum = 0;
-      for (int i = 0; i < a.window; ++i) sum += a.hist_ring[b * a.window + i];
-      hist = static_cast<double>(sum) / static_cast<double>(a.window);
+      int64_t v = lane < a.window ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1)
+        v += static_cast<int64_t>(xor_lane_u64(static_cast<uint64_t>(v), o));
+      hist = static_cast<double>(v) / static_cast<double>(a.window);
     }
     double conf = 0.0, ent = 0.0;
-    for (int l = 0; l < L; ++l) {
-      conf += static_cast<double>(a.row_stats[(static_cast<int64_t>(b) * L + l) * 3 + 1]);
-      ent += static_cast<double>(a.row_stats[(static_cast<int64_t>(b) * L + l) * 3 + 2]);
+    if (lane < L) {
+      const float *rs = a.row_stats + (static_cast<int64_t>(b) * L + lane) * 3;
+      conf = static_cast<double>(rs[1]);
+      ent = static_cast<double>(rs[2]);
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      conf += xor_lane_f64(conf, o);
+      ent += xor_lane_f64(ent, o);
     }
     conf /= static_cast<double>(L);
     ent /= static_cast<double>(L);
@@ -461,26 +901,33 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaP
             static_cast<double>(sp.phi[2]) * ent + static_cast<double>(sp.phi[3]) * hist;
       if (tau < static_cast<double>(sp.tau_min)) tau = static_cast<double>(sp.tau_min);
       const double prefix = a.prefix_len ? static_cast<double>(a.prefix_len[b]) : 0.0;
-      if (tid < sp.n_grid) {
-        const double B = static_cast<double>(sp.grid[tid]);
-        s.saba_u[tid] = (1.0 - exp(-B / tau)) /
-                        (static_cast<double>(sp.c0) + static_cast<double>(sp.c1) * B +
-                         static_cast<double>(sp.c2) * B * prefix);
+      // U of one grid budget per lane, then the first maximum: largest U,
+      // ties (and a non-number U) to the smaller grid index
+      double u = -INFINITY;
+      if (lane < sp.n_grid) {
+        const double B = static_cast<double>(sp.grid[lane]);
+        u = (1.0 - exp(-B / tau)) / (static_cast<double>(sp.c0) + static_cast<double>(sp.c1) * B +
+                                     static_cast<double>(sp.c2) * B * prefix);
+        if (!(u == u)) u = -INFINITY;
       }
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
-      budget = sp.grid[0];
-      double ub = s.saba_u[0];
-      for (int i = 1; i < sp.n_grid; ++i)
-        if (s.saba_u[i] > ub) {
-          ub = s.saba_u[i];
-          budget = sp.grid[i];
+      int best = lane;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const double ou = xor_lane_f64(u, o);
+        const int ob = static_cast<int>(xor_lane(static_cast<uint32_t>(best), o));
+        if (ou > u || (ou == u && ob < best)) {
+          u = ou;
+          best = ob;
         }
+      }
+      budget = sp.grid[best < sp.n_grid ? best : 0];
     } else {
       budget = a.fixed_budget[b];
     }
-    if (tid == 0) {
+    const bool mono = __ballot(pos) == 0ull;
+    if (lane == 0) {
       s.sc[kBudget] = budget;
+      s.sc[kMono] = mono ? 1 : 0;
       a.budget[b] = budget;
       if (a.saba_state) {
         a.saba_state[b * 4 + 0] = static_cast<float>(conf);
@@ -495,99 +942,78 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaP
   // ---------------- selection ----------------
   int n_target = s.sc[kBudget] < a.n_max ? s.sc[kBudget] : a.n_max;
   if (n_target < 0) n_target = 0;
-  if (s.sc[kMono]) {
+  const bool mono = s.sc[kMono] != 0;
+  if (mono) {
     if (n_target > 0) {
-      select_parallel(s, a, ss, sc, n_target);
+      const int n_pool = staged ? select_parallel<true>(s, a, ss, sc, n_target)
+                                : select_parallel<false>(s, a, ss, sc, n_target);
+      if (tid == 0) s.sc[kNPool] = n_pool;
     } else if (tid == 0) {
       s.sc[kNPool] = 0;
+      s.sc[kNSel] = 0;
     }
   } else if (tid == 0) {
-    select_serial(s, a, ss, sc, n_target);
+    if (staged) select_serial(s, a, s.rows, s.rowc, n_target);
+    else select_serial(s, a, ss, sc, n_target);
   }
   __syncthreads();
-  const int n = s.sc[kNPool];
-  if (tid == 0) a.n_nodes[b] = n;
+  const int n = s.sc[kNPool];       // pool entries, dead ones included
+  const int n_sel = s.sc[kNSel];    // selected nodes
+  if (tid == 0) a.n_nodes[b] = n_sel;
 
   // ---------------- canonical numbering ----------------
-  // Depth by depth: a node's key is (rank of its parent within the parent's
-  // depth, rank of its token among that depth's candidates).  Keys are set in
-  // a bitmap; a node's rank within its depth is the number of set bits below
-  // its key (prefix sum of word popcounts).  aux[i] = rank within depth,
-  // map[i] = canonical index.
-  if (tid == 0) s.sc[kMaxDepth] = 0;
-  __syncthreads();
-  for (int i = tid; i < n; i += kSelThreads) atomicMax(&s.sc[kMaxDepth], pi_depth(s.p_info[i]));
-  __syncthreads();
-  const int max_depth = s.sc[kMaxDepth];
-  int offset = 0, n_prev = 1;
-  for (int d = 1; d <= max_depth; ++d) {
-    const int nwords = (n_prev * K + 31) / 32;
-    for (int w = tid; w < nwords; w += kSelThreads) s.hist[w] = 0;
-    if (tid == 0) s.sc[kDepthN] = 0;
-    __syncthreads();
-    for (int i = tid; i < n; i += kSelThreads) {
-      const int32_t info = s.p_info[i];
-      if (pi_depth(info) != d) continue;
-      const int p = pi_parent(info);
-      const int key = (p < 0 ? 0 : s.aux[p]) * K + s.idr[(d - 1) * K + pi_slot(info)];
-      atomicOr(reinterpret_cast<uint32_t *>(&s.hist[key >> 5]), 1u << (key & 31));
-      atomicAdd(&s.sc[kDepthN], 1);
-    }
-    __syncthreads();
-    const int nd = s.sc[kDepthN];
-    for (int w = tid; w < nwords; w += kSelThreads)
-      s.pcnt[w] = __popc(static_cast<uint32_t>(s.hist[w]));
-    __syncthreads();
-    block_scan(s, s.pcnt, nwords);
-    for (int i = tid; i < n; i += kSelThreads) {
-      const int32_t info = s.p_info[i];
-      if (pi_depth(info) != d) continue;
-      const int p = pi_parent(info);
-      const int key = (p < 0 ? 0 : s.aux[p]) * K + s.idr[(d - 1) * K + pi_slot(info)];
-      const uint32_t word = static_cast<uint32_t>(s.hist[key >> 5]);
-      const int rank = s.pcnt[key >> 5] + __popc(word & ((1u << (key & 31)) - 1u));
-      s.aux[i] = rank;          // parents (depth d-1) are not touched here
-      s.map[i] = offset + rank;
-    }
-    __syncthreads();
-    offset += nd;
-    n_prev = nd;
-  }
+  if (mono) canon_preorder(s, L, K, n, n_sel);
+  else canon_by_depth(s, K, n);
 
   // ---------------- emission ----------------
   const int64_t ob = static_cast<int64_t>(b) * a.n_max;
   const int32_t base = a.base_pos[b];
-  for (int i = tid; i < a.n_max; i += kSelThreads) {
-    if (i < n) {
-      const int32_t info = s.p_info[i];
-      const int c = s.map[i];
-      const int p = pi_parent(info);
-      const int cp = p < 0 ? -1 : s.map[p];
-      a.tokens[ob + c] = ptoken(s, K, info);
-      a.parents[ob + c] = cp;
-      a.pos_ids[ob + c] = base + pi_depth(info);
-      if (a.node_scores) a.node_scores[ob + c] = s.p_score[i];
-      s.hist[c] = cp;           // canonical parents for the mask
-    } else {
-      a.tokens[ob + i] = -1;
-      a.parents[ob + i] = -1;
-      a.pos_ids[ob + i] = -1;
-      if (a.node_scores) a.node_scores[ob + i] = 0.0;
-    }
+  int32_t *cpar = s.u.b.hist;       // canonical parents, for the mask
+  for (int i = tid; i < n; i += kSelThreads) {
+    const uint32_t info = s.p_info[i];
+    if (!alive(info)) continue;
+    const int c = s.map[i];
+    const int p = pi_parent(info);
+    const int cp = p < 0 ? -1 : s.map[p];
+    a.tokens[ob + c] = ptoken(s, K, info);
+    a.parents[ob + c] = cp;
+    a.pos_ids[ob + c] = base + pi_depth(info);
+    if (a.node_scores) a.node_scores[ob + c] = s.p_score[i];
+    cpar[c] = cp;
+  }
+  for (int c = n_sel + tid; c < a.n_max; c += kSelThreads) {
+    a.tokens[ob + c] = -1;
+    a.parents[ob + c] = -1;
+    a.pos_ids[ob + c] = -1;
+    if (a.node_scores) a.node_scores[ob + c] = 0.0;
   }
   __syncthreads();
 
   // ---------------- ancestor mask ----------------
+  // One thread per row: a single walk up the canonical parents (which precede
+  // their children, so the indices decrease) emits the row's words from the
+  // highest down.
   if (a.mask) {
-    uint64_t *mrow = a.mask + static_cast<int64_t>(b) * a.n_max * a.words;
-    const int total = a.n_max * a.words;
-    for (int idx = tid; idx < total; idx += kSelThreads) {
-      const int r = idx / a.words, wd = idx % a.words;
-      uint64_t bits = 0;
-      if (r < n)
-        for (int j = r; j >= 0; j = s.hist[j])
-          if ((j >> 6) == wd) bits |= 1ull << (j & 63);
-      mrow[idx] = bits;
+    const int words = a.words;
+    for (int r = tid; r < a.n_max; r += kSelThreads) {
+      uint64_t *dst = a.mask + (static_cast<int64_t>(b) * a.n_max + r) * words;
+      int w = words - 1;
+      if (r < n_sel) {
+        for (; w > (r >> 6); --w) dst[w] = 0ull;
+        uint64_t bits = 0;
+        for (int j = r;;) {
+          bits |= 1ull << (j & 63);
+          const int pj = cpar[j];
+          if (pj < 0 || pj >= j) break;
+          for (; (pj >> 6) < w; --w) {
+            dst[w] = bits;
+            bits = 0;
+          }
+          j = pj;
+        }
+        dst[w--] = bits;
+      }
+      for (; w >= 0; --w) dst[w] = 0ull;
     }
   }
 }
@@ -607,6 +1033,8 @@ hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_t
   a.sorted_score = ctx->sorted_score;
   a.sorted_child = ctx->sorted_child;
   a.topk_ids = ctx->topk_ids;
+  a.id_rank = ctx->id_rank;
+  a.positive = ctx->positive;
   a.root_token = in->root_token;
   a.base_pos = in->base_pos;
   a.prefix_len = in->prefix_len;
@@ -621,6 +1049,7 @@ hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_t
   a.mask = out->mask;
   a.node_scores = out->node_scores;
   a.saba_state = out->saba_state;
+  a.error_flag = ctx->error_flag;
   const int use_saba = in->fixed_budget == nullptr;
   hipLaunchKernelGGL(select_kernel, dim3(in->batch), dim3(kSelThreads), 0, stream, a, ctx->saba,
                      use_saba);
