@@ -37,12 +37,66 @@ projection_kernel(const float *__restrict__ emb, const float *__restrict__ gp,
 }
 
 constexpr int kEdgeThreads = 64;   // one wave per (sequence, depth)
+constexpr int kGather = 8;         // projection loads (16 bytes) in flight per lane
 
-// Dynamic LDS layout: parents [K][m+1], children [K][m+1] (rows padded by one
-// float so that lanes reading different rows hit different banks), scores
-// [K][K], row means [K], tokens [K].
+// Division by a runtime divisor d <= 64 of numerators below 2^26: a shift for
+// powers of two, else the high half of n * ceil(2^32 / d), which is exact in
+// that range (the error term n * (M d - 2^32) / 2^32 stays below 1).
+struct FastDiv {
+  uint32_t d, m, shift;
+  int pow2;
+  __device__ __forceinline__ uint32_t div(uint32_t n) const {
+    return pow2 ? (n >> shift) : __umulhi(n, m);
+  }
+};
+FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f{d, 0u, 0u, 0};
+  if ((d & (d - 1)) == 0) {
+    f.pow2 = 1;
+    while ((1u << f.shift) < d) ++f.shift;
+  } else {
+    f.m = static_cast<uint32_t>(((1ull << 32) + d - 1) / d);
+  }
+  return f;
+}
+
+// Bitonic sort, descending, of the keys of each run of SEG consecutive lanes.
+template <int SEG>
+__device__ __forceinline__ uint64_t seg_sort_desc(uint64_t k) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int size = 2; size <= SEG; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const uint64_t o = xor_lane_u64(k, stride);
+      const bool lower = (lane & stride) == 0;
+      const bool desc = size == SEG || (lane & size) == 0;
+      const uint64_t mx = k > o ? k : o, mn = k > o ? o : k;
+      k = (lower == desc) ? mx : mn;
+    }
+  }
+  return k;
+}
+
+// Sum over each run of SEG consecutive lanes, in every lane of the run.
+template <int SEG>
+__device__ __forceinline__ float seg_sum(float v) {
+#pragma unroll
+  for (int stride = 1; stride < SEG; stride <<= 1)
+    v += __uint_as_float(xor_lane(__float_as_uint(v), stride));
+  return v;
+}
+
+// One wave per (sequence b, depth l).  Dynamic LDS: parents [K][mp],
+// children [K][mp] (rows of m floats padded to a multiple of 4 plus 4: 16-byte
+// aligned rows that start on different banks), depth embedding [m], log q [K],
+// token ids [K], their ranks by id [K], clamped child and parent ids [K].
+// The (parent, child) pairs are processed SEG lanes per parent (SEG = K
+// rounded up to a power of two): dot product, centering over the parent's
+// children, score, then a segmented sort ranks the children of the parent.
+template <int SEG>
 __global__ void __launch_bounds__(kEdgeThreads)
-edge_kernel(int L, int K, int m, int64_t V, const int32_t *__restrict__ topk_ids,
+edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__restrict__ topk_ids,
             const float *__restrict__ topk_logq, const int32_t *__restrict__ root_token,
             const float *__restrict__ P, const float *__restrict__ Q,
             const float *__restrict__ depth_emb, ScorerParams sp,
@@ -50,12 +104,15 @@ edge_kernel(int L, int K, int m, int64_t V, const int32_t *__restrict__ topk_ids
             uint8_t *__restrict__ id_rank, uint8_t *__restrict__ positive,
             float *__restrict__ edge_out, uint32_t *__restrict__ error_flag) {
   extern __shared__ float smem[];
-  const int mp = m + 1;
+  const int mp = ((m + 3) & ~3) + 4;
   float *s_par = smem;
   float *s_chd = s_par + K * mp;
-  float *s_score = s_chd + K * mp;
-  float *s_mean = s_score + K * K;
-  int32_t *s_tok = reinterpret_cast<int32_t *>(s_mean + K);
+  float *s_u = s_chd + K * mp;           // 16-byte aligned
+  float *s_lq = s_u + m;
+  int32_t *s_tok = reinterpret_cast<int32_t *>(s_lq + K);
+  int32_t *s_idr = s_tok + K;
+  int32_t *s_cid = s_idr + K;
+  int32_t *s_pid = s_cid + K;
 
   const int b = blockIdx.x / L;
   const int l = blockIdx.x % L;
@@ -68,73 +125,112 @@ edge_kernel(int L, int K, int m, int64_t V, const int32_t *__restrict__ topk_ids
     if (lane == 0) atomicOr(error_flag, 1u);
     root = 0;
   }
-  // stage projections (+ depth embedding) of parents and children
-  for (int i = lane; i < K * m; i += kEdgeThreads) {
-    const int c = i / m, j = i % m;
-    const float u = sp.has_depth_emb ? depth_emb[l * m + j] : 0.f;
-    int32_t ct = topk_ids[row * K + c];
-    if (ct < 0 || ct >= V) ct = 0;   // only with non-finite logits
-    s_chd[c * mp + j] = Q[static_cast<int64_t>(ct) * m + j] + u;
-    if (c < n_par) {
-      int32_t pt = (l == 0) ? root : topk_ids[(row - 1) * K + c];
-      if (pt < 0 || pt >= V) pt = 0;
-      s_par[c * mp + j] = P[static_cast<int64_t>(pt) * m + j] + u;
+  // token ids (clamped copies for the gathers; ids fall outside [0, V) only
+  // with non-finite logits), log q and the depth embedding
+  if (lane < K) {
+    const int32_t ct = topk_ids[row * K + lane];
+    const int32_t pt = (l == 0) ? root : topk_ids[(row - 1) * K + lane];
+    s_tok[lane] = ct;
+    s_lq[lane] = topk_logq[row * K + lane];
+    s_cid[lane] = (ct < 0 || ct >= V) ? 0 : ct;
+    s_pid[lane] = (pt < 0 || pt >= V) ? 0 : pt;
+  }
+  for (int j = lane; j < m; j += kEdgeThreads) s_u[j] = sp.has_depth_emb ? depth_emb[l * m + j] : 0.f;
+  __syncthreads();
+  // rank of each candidate's token id within the depth
+  if (lane < K) {
+    const int32_t tc = s_tok[lane];
+    int r = 0;
+#pragma unroll 8
+    for (int c2 = 0; c2 < K; ++c2) r += s_tok[c2] < tc;
+    s_idr[lane] = r;
+    id_rank[row * K + lane] = static_cast<uint8_t>(r);
+  }
+  // projections of children and parents plus the depth embedding, 16 bytes a
+  // load when m % 4 == 0; every load of a batch is issued before any store
+  if ((m & 3) == 0) {
+    const int m4 = m >> 2;
+    const int nq = K * m4, total = nq + n_par * m4;
+    for (int base = 0; base < total; base += kGather * kEdgeThreads) {
+      float4 v[kGather];
+#pragma unroll
+      for (int k = 0; k < kGather; ++k) {
+        int t = base + k * kEdgeThreads + lane;
+        t = t < total ? t : total - 1;
+        const int tt = t < nq ? t : t - nq;
+        const int r = static_cast<int>(mdiv4.div(static_cast<uint32_t>(tt))), j4 = tt - r * m4;
+        const float *src = t < nq ? Q + static_cast<int64_t>(s_cid[r]) * m
+                                  : P + static_cast<int64_t>(s_pid[r]) * m;
+        v[k] = reinterpret_cast<const float4 *>(src)[j4];
+      }
+#pragma unroll
+      for (int k = 0; k < kGather; ++k) {
+        const int t = base + k * kEdgeThreads + lane;
+        if (t >= total) continue;
+        const int tt = t < nq ? t : t - nq;
+        const int r = static_cast<int>(mdiv4.div(static_cast<uint32_t>(tt))), j4 = tt - r * m4;
+        const float4 u = reinterpret_cast<const float4 *>(s_u)[j4];
+        float4 *dst = reinterpret_cast<float4 *>((t < nq ? s_chd : s_par) + r * mp) + j4;
+        *dst = make_float4(v[k].x + u.x, v[k].y + u.y, v[k].z + u.z, v[k].w + u.w);
+      }
+    }
+  } else {
+    const int nq = K * m, total = nq + n_par * m;
+    for (int t = lane; t < total; t += kEdgeThreads) {
+      const int tt = t < nq ? t : t - nq;
+      const int r = tt / m, j = tt % m;
+      const float *src = t < nq ? Q + static_cast<int64_t>(s_cid[r]) * m
+                                : P + static_cast<int64_t>(s_pid[r]) * m;
+      (t < nq ? s_chd : s_par)[r * mp + j] = src[j] + s_u[j];
     }
   }
-  for (int c = lane; c < K; c += kEdgeThreads) s_tok[c] = topk_ids[row * K + c];
   __syncthreads();
 
-  // f(p, c) = s * <P[p] + u, Q[c] + u> / sqrt(m)
+  // per parent p (SEG lanes, child c = lane % SEG):
+  //   f = s * <P[p] + u, Q[c] + u> / sqrt(m),  S = log q(c) + beta * (f - mean_c f)
   const float fscale = sp.scale / sqrtf(static_cast<float>(m));
-  for (int i = lane; i < n_par * K; i += kEdgeThreads) {
-    const int p = i / K, c = i % K;
-    const float *pv = s_par + p * mp, *cv = s_chd + c * mp;
-    float acc = 0.f;
-    for (int j = 0; j < m; ++j) acc = __builtin_fmaf(pv[j], cv[j], acc);
-    s_score[i] = fscale * acc;
-  }
-  __syncthreads();
-  for (int p = lane; p < n_par; p += kEdgeThreads) {
-    float mean = 0.f;
-    if (sp.center) {
-      for (int c = 0; c < K; ++c) mean += s_score[p * K + c];
-      mean /= static_cast<float>(K);
-    }
-    s_mean[p] = mean;
-  }
-  __syncthreads();
-  // S = log q(c) + beta * (f - mean over the children of p)
-  for (int i = lane; i < n_par * K; i += kEdgeThreads) {
-    const int p = i / K, c = i % K;
-    const float lq = topk_logq[row * K + c];
-    s_score[i] = lq + sp.beta * (s_score[i] - s_mean[p]);
-  }
-  __syncthreads();
-  // rank the children of each parent; write the ranked rows, the optional
-  // table, the sign flag and the token-id rank of each candidate
+  constexpr int kRows = kEdgeThreads / SEG;
+  const int c = lane & (SEG - 1);
   const int64_t base = row * K * K;
   bool pos = false;
-  for (int i = lane; i < n_par * K; i += kEdgeThreads) {
-    const int p = i / K, c = i % K;
-    const float sc = s_score[i];
-    const int32_t tc = s_tok[c];
-    int rank = 0;
-    for (int c2 = 0; c2 < K; ++c2) {
-      const float o = s_score[p * K + c2];
-      rank += (o > sc) || (o == sc && s_tok[c2] < tc);
+  for (int p0 = 0; p0 < n_par; p0 += kRows) {
+    const int p = p0 + lane / SEG;
+    const bool valid = p < n_par && c < K;
+    const int pp = p < n_par ? p : 0, cc = c < K ? c : 0;
+    const float *pv = s_par + pp * mp, *cv = s_chd + cc * mp;
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    if ((m & 3) == 0) {
+      const float4 *p4 = reinterpret_cast<const float4 *>(pv);
+      const float4 *c4 = reinterpret_cast<const float4 *>(cv);
+#pragma unroll 4
+      for (int q = 0; q < (m >> 2); ++q) {
+        const float4 x = p4[q], y = c4[q];
+        a0 = __builtin_fmaf(x.x, y.x, a0);
+        a1 = __builtin_fmaf(x.y, y.y, a1);
+        a2 = __builtin_fmaf(x.z, y.z, a2);
+        a3 = __builtin_fmaf(x.w, y.w, a3);
+      }
+    } else {
+#pragma unroll 4
+      for (int j = 0; j < m; ++j) a0 = __builtin_fmaf(pv[j], cv[j], a0);
     }
-    sorted_score[base + p * K + rank] = sc;
-    sorted_child[base + p * K + rank] = static_cast<uint8_t>(c);
-    if (edge_out) edge_out[base + i] = sc;
-    pos |= sc > 0.f;
+    const float f = fscale * ((a0 + a1) + (a2 + a3));
+    float mean = 0.f;
+    if (sp.center) mean = seg_sum<SEG>(valid ? f : 0.f) / static_cast<float>(K);
+    const float S = (s_lq[cc] + sp.beta * (f - mean)) + 0.0f;   // -0 -> +0 for the key
+    if (valid && edge_out) edge_out[base + p * K + c] = S;
+    pos |= valid && S > 0.f;
+    // key: score, then smaller token id, then the child slot
+    const uint32_t lo = (static_cast<uint32_t>(63 - s_idr[cc]) << 6) | static_cast<uint32_t>(cc);
+    const uint64_t key = valid ? (static_cast<uint64_t>(ordered_f32(S)) << 32) | lo : 0ull;
+    const uint64_t sorted = seg_sort_desc<SEG>(key);
+    if (valid) {   // lane c of the run now holds the child ranked c
+      sorted_score[base + p * K + c] = unordered_f32(static_cast<uint32_t>(sorted >> 32));
+      sorted_child[base + p * K + c] = static_cast<uint8_t>(sorted & 63u);
+    }
   }
   if (edge_out && l == 0)
     for (int i = K + lane; i < K * K; i += kEdgeThreads) edge_out[base + i] = 0.f;
-  for (int c = lane; c < K; c += kEdgeThreads) {
-    int r = 0;
-    for (int c2 = 0; c2 < K; ++c2) r += s_tok[c2] < s_tok[c];
-    id_rank[row * K + c] = static_cast<uint8_t>(r);
-  }
   const bool any_pos = __ballot(pos) != 0ull;
   if (lane == 0) positive[row] = any_pos ? 1 : 0;
 }
@@ -155,13 +251,25 @@ hipError_t launch_edge_scores(graft_ctx *ctx, int batch, const int32_t *root_tok
                               float *edge_out, hipStream_t stream) {
   const graft_dims &d = ctx->dims;
   const int K = d.top_k, m = ctx->scorer.score_dim;
-  const size_t lds = sizeof(float) * (2 * static_cast<size_t>(K) * (m + 1) + K * K + K) +
-                     sizeof(int32_t) * K;
-  hipLaunchKernelGGL(edge_kernel, dim3(batch * d.num_pos), dim3(kEdgeThreads), lds, stream,
-                     d.num_pos, K, m, static_cast<int64_t>(d.vocab), ctx->topk_ids,
-                     ctx->topk_logq, root_token, ctx->proj_parent, ctx->proj_child,
-                     ctx->depth_emb, ctx->scorer, ctx->sorted_score, ctx->sorted_child,
-                     ctx->id_rank, ctx->positive, edge_out, ctx->error_flag);
+  const size_t mp = ((m + 3) & ~3) + 4;
+  const size_t lds = sizeof(float) * (2 * static_cast<size_t>(K) * mp + K + m) +
+                     sizeof(int32_t) * 4 * K;
+  const FastDiv mdiv4 = make_fastdiv(static_cast<uint32_t>(m >= 4 ? m / 4 : 1));
+  const dim3 grid(batch * d.num_pos), block(kEdgeThreads);
+#define GRAFT_EDGE(SEG)                                                                        \
+  hipLaunchKernelGGL(edge_kernel<SEG>, grid, block, lds, stream, d.num_pos, K, m,            \
+                     static_cast<int64_t>(d.vocab), mdiv4, ctx->topk_ids, ctx->topk_logq,     \
+                     root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
+                     ctx->scorer, ctx->sorted_score, ctx->sorted_child, ctx->id_rank,         \
+                     ctx->positive, edge_out, ctx->error_flag)
+  if (K <= 1) GRAFT_EDGE(1);
+  else if (K <= 2) GRAFT_EDGE(2);
+  else if (K <= 4) GRAFT_EDGE(4);
+  else if (K <= 8) GRAFT_EDGE(8);
+  else if (K <= 16) GRAFT_EDGE(16);
+  else if (K <= 32) GRAFT_EDGE(32);
+  else GRAFT_EDGE(64);
+#undef GRAFT_EDGE
   return hipGetLastError();
 }
 
