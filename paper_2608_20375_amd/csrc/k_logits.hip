@@ -30,6 +30,7 @@ constexpr double kLog2e = 1.44269504088896340735992468100;
 constexpr float kNegBig = -1e30f;                 // finite stand-in for -inf
 constexpr int kTargetBlocks = 1024;                // one residency round at 4 waves/SIMD
 constexpr int kMinSplitVec = 512;                 // >= 4096 elements per split
+constexpr int kRing = 64;                         // deferred groups per wave
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -67,6 +68,9 @@ struct WaveBuf {
   uint64_t *buf;   // LDS [CAP]
   int count;       // wave-uniform
   float thr;       // wave-uniform: a candidate needs value >= thr
+  uint4 *rq;       // LDS [kRing]: deferred groups of 8 raw bf16 values
+  uint32_t *rid;   // LDS [kRing]: element id of each group's first value
+  int rcount;      // wave-uniform
 };
 
 struct Compacted {
@@ -167,6 +171,38 @@ __device__ __forceinline__ void unpack8(const uint4 q, float (&v)[8]) {
   }
 }
 
+// Offers the deferred groups (one per lane) against the current threshold.
+// A group was deferred when its largest value reached the threshold of the
+// time; the threshold only rises, so comparing now drops nothing that belongs
+// to the top K.  Out of line, with the buffer state passed by value.
+template <int CAP>
+__device__ __noinline__ Compacted flush_ool(uint64_t *buf, int count, float thr, const uint4 *rq,
+                                            const uint32_t *rid, int rcount, int K) {
+  const int lane = lane_id();
+  WaveBuf<CAP> w{buf, count, thr, nullptr, nullptr, 0};
+  const bool have = lane < rcount;
+  uint4 r = make_uint4(0, 0, 0, 0);
+  uint32_t id0 = 0;
+  if (have) {
+    r = rq[lane];
+    id0 = rid[lane];
+  }
+  float v[8];
+  unpack8(r, v);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) wave_offer<CAP>(w, K, v[e], id0 + e, have);
+  return {w.count, w.thr};
+}
+
+// Empties the wave's ring of deferred groups into its candidate buffer.
+template <int CAP>
+__device__ __forceinline__ void wave_flush(WaveBuf<CAP> &w, int K) {
+  const Compacted c = flush_ool<CAP>(w.buf, w.count, w.thr, w.rq, w.rid, w.rcount, K);
+  w.count = __builtin_amdgcn_readfirstlane(c.count);
+  w.thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(c.thr)));
+  w.rcount = 0;
+}
+
 // Loads one tile: lane handles vectors tile_vec + u*64 + lane, u < kUnroll.
 template <bool MASKED>
 __device__ __forceinline__ void load_tile(const uint4 *__restrict__ vec, int64_t tile_vec,
@@ -210,17 +246,24 @@ __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t 
   }
   const float tmax = fmaxf(fmaxf(sub[0], sub[1]), fmaxf(sub[2], sub[3]));
 
-  // top-K candidates; any wave's threshold bounds the block's K-th value
+  // top-K candidates; any wave's threshold bounds the block's K-th value.
+  // A group of 8 whose largest value reaches the threshold is copied raw to
+  // the wave's ring; the ring is offered element by element when it fills.
   if (shared_thr > w.thr) w.thr = shared_thr;
   if (__ballot(tmax >= w.thr) != 0ull) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      if (__ballot(ok[u] && sub[u] >= w.thr) != 0ull) {
-        const int64_t id0 = elem0 + (tile_vec + u * kWave + lane) * 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          wave_offer<CAP>(w, K, v[u][e], static_cast<uint32_t>(id0 + e), ok[u]);
+      const bool pass = ok[u] && sub[u] >= w.thr;
+      const uint64_t m = __ballot(pass);
+      if (m == 0ull) continue;
+      const int n = __popcll(m);
+      if (w.rcount + n > kRing) wave_flush<CAP>(w, K);
+      if (pass) {
+        const int slot = w.rcount + lanes_below(m);
+        w.rq[slot] = q[u];
+        w.rid[slot] = static_cast<uint32_t>(elem0 + (tile_vec + u * kWave + lane) * 8);
       }
+      w.rcount = __builtin_amdgcn_readfirstlane(w.rcount + n);
     }
   }
 
@@ -373,7 +416,9 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
 
   LaneStats st;
   stats_init(st);
-  WaveBuf<CAP> w{s_buf[wave], 0, -INFINITY};
+  __shared__ uint4 s_rq[kWaves][kRing];
+  __shared__ uint32_t s_rid[kWaves][kRing];
+  WaveBuf<CAP> w{s_buf[wave], 0, -INFINITY, s_rq[wave], s_rid[wave], 0};
 
   // Tiles interleaved over the waves of the block; the next tile's loads are
   // issued before the current tile is processed.
@@ -411,20 +456,28 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     wave_sort_desc<1>(k1);
     if (lane < K) s_init[wave * K + lane] = k1[0];
     __syncthreads();
-    constexpr int E2 = CAP / kWave;   // 4 waves x K <= CAP lane maxima
-    uint64_t k2[E2];
+    // the K-th of the union of the waves' K best (4 K <= CAP keys)
+    uint64_t kth;
+    if (kWaves * K <= kWave) {
+      uint64_t k2[1] = {lane < kWaves * K ? s_init[lane] : 0ull};
+      wave_sort_desc<1>(k2);
+      kth = k2[0];
+    } else {
+      constexpr int E2 = CAP / kWave;
+      uint64_t k2[E2];
 #pragma unroll
-    for (int e = 0; e < E2; ++e) {
-      const int i = e * kWave + lane;
-      k2[e] = i < kWaves * K ? s_init[i] : 0ull;
+      for (int e = 0; e < E2; ++e) {
+        const int i = e * kWave + lane;
+        k2[e] = i < kWaves * K ? s_init[i] : 0ull;
+      }
+      wave_sort_desc<E2>(k2);
+      const int src_e = (K - 1) / kWave;
+      kth = 0;
+#pragma unroll
+      for (int e = 0; e < E2; ++e)
+        if (e == src_e) kth = k2[e];
     }
-    wave_sort_desc<E2>(k2);
-    const int src_e = (K - 1) / kWave, src_l = (K - 1) % kWave;
-    uint64_t kth = 0;
-#pragma unroll
-    for (int e = 0; e < E2; ++e)
-      if (e == src_e) kth = k2[e];
-    const uint32_t hi = __shfl(static_cast<uint32_t>(kth >> 32), src_l);
+    const uint32_t hi = __shfl(static_cast<uint32_t>(kth >> 32), (K - 1) % kWave);
     w.thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(unordered_f32(hi))));
     if (w.thr < -1e29f) w.thr = -INFINITY;   // fewer than K real elements seen
   }
@@ -464,6 +517,7 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     }
   }
 
+  if (w.rcount > 0) wave_flush<CAP>(w, K);
   wave_compact<CAP>(w, K);
   stats_wave_reduce(st);
   if (lane == 0) {
@@ -480,14 +534,25 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
   // Block merge in wave 0: statistics and the 4 waves' top-K lists.
   double mL = s_stats[0][0], S = s_stats[0][1], T2 = s_stats[0][2];
   for (int i = 1; i < kWaves; ++i) stats_merge(mL, S, T2, s_stats[i][0], s_stats[i][1], s_stats[i][2]);
-  constexpr int E = CAP / kWave;
-  {
+  // key i = wave * K + rank of the waves' lists (no division: at most 3 steps)
+  auto merged_key = [&](int i) -> uint64_t {
+    if (i >= kWaves * K) return 0ull;
+    int wv = 0, r = i;
+    while (r >= K) {
+      r -= K;
+      ++wv;
+    }
+    return s_buf[wv][r];
+  };
+  if (kWaves * K <= kWave) {
+    uint64_t k[1] = {merged_key(lane)};
+    wave_sort_desc<1>(k);
+    if (lane < K) s_buf[0][lane] = k[0];
+  } else {
+    constexpr int E = CAP / kWave;
     uint64_t k[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int i = e * kWave + lane;   // i = wave * K + rank
-      k[e] = (i < kWaves * K) ? s_buf[i / K][i % K] : 0ull;
-    }
+    for (int e = 0; e < E; ++e) k[e] = merged_key(e * kWave + lane);
     wave_sort_desc<E>(k);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -523,7 +588,7 @@ merge_kernel(int splits, int K, const double *__restrict__ part_stats,
   const double *ps = part_stats + row * splits * 3;
   double mL = ps[0], S = ps[1], T2 = ps[2];
   for (int i = 1; i < splits; ++i) stats_merge(mL, S, T2, ps[3 * i], ps[3 * i + 1], ps[3 * i + 2]);
-  WaveBuf<CAP> m{s_buf, 0, -INFINITY};
+  WaveBuf<CAP> m{s_buf, 0, -INFINITY, nullptr, nullptr, 0};
   const uint64_t *pk = part_keys + row * splits * K;
   const int total = splits * K;
   for (int base = 0; base < total; base += kWave) {
