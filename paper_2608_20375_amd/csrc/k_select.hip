@@ -157,6 +157,11 @@ __device__ int block_scan(SelMem &s, int32_t *data, int n) {
   return total;
 }
 
+static_assert(kBins == 32 * kWave, "one run of 32 bins per lane of a wave");
+// Histogram slot of a bin: bin 32 l + j of lane l's run is stored at j * 64 + l,
+// so the scan's reads (lane l, run position j) hit consecutive words.
+__device__ __forceinline__ int hslot(int bin) { return ((bin & 31) << 6) | (bin >> 5); }
+
 __device__ __forceinline__ int score_bin(double v, double hi, double scale) {
   const double f = (hi - v) * scale;
   int b = static_cast<int>(f);
@@ -173,7 +178,7 @@ __device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, do
   for (int i = tid; i < n; i += kSelThreads) {
     const bool live = alive(s.p_info[i]);
     const int bin = score_bin(s.p_score[i], hi, scale);
-    if (live) atomicAdd(&s.u.b.hist[bin], 1);
+    if (live) atomicAdd(&s.u.b.hist[hslot(bin)], 1);
   }
   __syncthreads();
   // wave 0: the bin holding the n_keep-th entry (bins are in descending score
@@ -183,7 +188,7 @@ __device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, do
     int c[kPer], sum = 0;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-      c[j] = s.u.b.hist[lane * kPer + j];
+      c[j] = s.u.b.hist[j * kWave + lane];
       sum += c[j];
     }
     int run = wave_incl_scan(sum) - sum;
@@ -197,7 +202,7 @@ __device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, do
       run += c[j];
     }
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) s.u.b.hist[lane * kPer + j] = 0;
+    for (int j = 0; j < kPer; ++j) s.u.b.hist[j * kWave + lane] = 0;
     if (lane == 0) {
       s.sc[kG] = 0;
       s.thkey = ~0ull;
@@ -310,7 +315,7 @@ __device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv
 #pragma unroll
     for (int k = 0; k < 4; ++k)
       if (q * 4 + k < cnt)
-        atomicAdd(&s.u.b.hist[score_bin(ps + static_cast<double>(f[k]), hi, scale)], 1);
+        atomicAdd(&s.u.b.hist[hslot(score_bin(ps + static_cast<double>(f[k]), hi, scale))], 1);
   }
 }
 
@@ -333,13 +338,17 @@ __device__ __forceinline__ void append_children(SelMem &s, const float *row, con
   for (int q = 0; q < KV; ++q) {
     if (q * 4 >= cnt) break;
     const float f[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+    int slot[4], rk[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) slot[k] = static_cast<int>((w[q] >> (8 * k)) & 0xFF);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) rk[k] = idr[slot[k]];   // every slot of the row is < K
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int r = q * 4 + k;
       if (r < cnt) {
-        const int slot = static_cast<int>((w[q] >> (8 * k)) & 0xFF);
         s.p_score[dst + r] = ps + static_cast<double>(f[k]);
-        s.p_info[dst + r] = pinfo(x, d + 1, slot, idr[slot]);
+        s.p_info[dst + r] = pinfo(x, d + 1, slot[k], rk[k]);
       }
     }
   }
@@ -385,7 +394,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
   for (int i = tid; i < n; i += kSelThreads) {
     const bool live = alive(s.p_info[i]);
     const int bin = score_bin(s.p_score[i], hi, scale);
-    if (live) atomicAdd(&s.u.b.hist[bin], 1);
+    if (live) atomicAdd(&s.u.b.hist[hslot(bin)], 1);
   }
   const int m = n - x_lo;
   for (int k = 0; k < per; ++k) {
@@ -404,7 +413,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
     else if (KVP == 16) bin_children<16>(s, row, kv, c, ps, hi, scale);
     else
       for (int r = 0; r < c; ++r)
-        atomicAdd(&s.u.b.hist[score_bin(ps + static_cast<double>(row[r]), hi, scale)], 1);
+        atomicAdd(&s.u.b.hist[hslot(score_bin(ps + static_cast<double>(row[r]), hi, scale))], 1);
   }
   __syncthreads();
   if (wave == 0) {
@@ -412,7 +421,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
     int c[kPer], sum = 0;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-      c[j] = s.u.b.hist[lane * kPer + j];
+      c[j] = s.u.b.hist[j * kWave + lane];
       sum += c[j];
     }
     int run = wave_incl_scan(sum) - sum;
@@ -422,7 +431,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
       run += c[j];
     }
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) s.u.b.hist[lane * kPer + j] = 0;
+    for (int j = 0; j < kPer; ++j) s.u.b.hist[j * kWave + lane] = 0;
   }
   __syncthreads();
   if (scale == 0.0) return -INFINITY;
@@ -990,30 +999,49 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaP
   __syncthreads();
 
   // ---------------- ancestor mask ----------------
-  // One thread per row: a single walk up the canonical parents (which precede
-  // their children, so the indices decrease) emits the row's words from the
-  // highest down.
+  // Each wave takes 64 rows at a time, one per lane: a single walk up the
+  // canonical parents (which precede their children, so the indices
+  // decrease) emits the row's words from the highest down into LDS (rows
+  // padded by one word against bank conflicts); the wave then copies the 64
+  // rows out with consecutive lanes on consecutive words.  The pool arrays
+  // are free by now and hold the staging rows.
   if (a.mask) {
-    const int words = a.words;
-    for (int r = tid; r < a.n_max; r += kSelThreads) {
-      uint64_t *dst = a.mask + (static_cast<int64_t>(b) * a.n_max + r) * words;
+    const int words = a.words, pitch = words + 1;
+    const int lane = lane_id(), wave = tid / kWave;
+    const uint32_t recip = (65536u + words - 1) / words;   // t / words for t < 64 * 16
+    uint64_t *stage = reinterpret_cast<uint64_t *>(s.p_score) + wave * kWave * pitch;
+    uint64_t *mseq = a.mask + static_cast<int64_t>(b) * a.n_max * words;
+    for (int base = wave * kWave; base < a.n_max; base += kSelThreads) {
+      const int r = base + lane;
+      uint64_t *my = stage + lane * pitch;
       int w = words - 1;
       if (r < n_sel) {
-        for (; w > (r >> 6); --w) dst[w] = 0ull;
+        for (; w > (r >> 6); --w) my[w] = 0ull;
         uint64_t bits = 0;
         for (int j = r;;) {
           bits |= 1ull << (j & 63);
           const int pj = cpar[j];
           if (pj < 0 || pj >= j) break;
           for (; (pj >> 6) < w; --w) {
-            dst[w] = bits;
+            my[w] = bits;
             bits = 0;
           }
           j = pj;
         }
-        dst[w--] = bits;
+        my[w--] = bits;
       }
-      for (; w >= 0; --w) dst[w] = 0ull;
+      for (; w >= 0; --w) my[w] = 0ull;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const int rows = a.n_max - base < kWave ? a.n_max - base : kWave;
+      for (int t = lane; t < rows * words; t += kWave) {
+        const int rr = static_cast<int>((static_cast<uint32_t>(t) * recip) >> 16);
+        mseq[static_cast<int64_t>(base) * words + t] = stage[t + rr];
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
   }
 }
