@@ -124,6 +124,40 @@ __device__ __forceinline__ double xor_lane_f64(double v, int m) {
 // Bitonic sort of 64*E keys held by one wave, element index i = e*64 + lane;
 // afterwards the keys are in descending order of i.
 template <int E>
+__device__ __forceinline__ void wave_sort_desc_u32(uint32_t (&k)[E]) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int size = 2; size <= 64 * E; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride >= 64) {
+        const int es = stride / 64;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          if ((e & es) == 0) {
+            const int p = e | es;
+            const bool desc = ((e * 64 + lane) & size) == 0;
+            const uint32_t a = k[e], b = k[p];
+            const bool sw = desc ? (a < b) : (a > b);
+            k[e] = sw ? b : a;
+            k[p] = sw ? a : b;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const uint32_t o = xor_lane(k[e], stride);
+          const bool lower = (lane & stride) == 0;
+          const bool desc = ((e * 64 + lane) & size) == 0;
+          const uint32_t mx = k[e] > o ? k[e] : o, mn = k[e] > o ? o : k[e];
+          k[e] = (lower == desc) ? mx : mn;
+        }
+      }
+    }
+  }
+}
+
+template <int E>
 __device__ __forceinline__ void wave_sort_desc(uint64_t (&k)[E]) {
   const int lane = lane_id();
 #pragma unroll

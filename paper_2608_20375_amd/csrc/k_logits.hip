@@ -35,10 +35,10 @@ constexpr int kRing = 64;                         // deferred groups per wave
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 struct LaneStats {
-  float mx;      // largest logit seen
-  float mL;      // fp32 offset actually used: fl(mx * log2 e)
-  double S;      // sum 2^(x*log2e - mL)
-  double T2;     // sum 2^y * y
+  float mx;      // wave-uniform: largest logit the wave has seen
+  float mL;      // wave-uniform fp32 offset: fl(mx * log2 e)
+  double S;      // per lane: sum 2^(x*log2e - mL)
+  double T2;     // per lane: sum 2^y * y
 };
 
 __device__ __forceinline__ void stats_init(LaneStats &s) {
@@ -48,19 +48,23 @@ __device__ __forceinline__ void stats_init(LaneStats &s) {
   s.T2 = 0.0;
 }
 
-// Moves the offset to a larger maximum and rescales S and T2.  The factor
+// Moves the wave's offset to its new maximum when some lane's value exceeds
+// the old one, and rescales every lane's S and T2.  The factor
 // 2^(mL_old - mL_new) is one v_exp_f32 of an fp32 difference (exact for offsets
 // within a factor two of each other, and 0 for the initial finite stand-in).
-__device__ __forceinline__ void stats_raise(LaneStats &s, float new_mx) {
-  if (new_mx > s.mx) {
-    const float nL = new_mx * kL2E;
-    const float d = s.mL - nL;
-    const double a = static_cast<double>(__builtin_amdgcn_exp2f(d));
-    s.T2 = a * (s.T2 + static_cast<double>(d) * s.S);
-    s.S = a * s.S;
-    s.mL = nL;
-    s.mx = new_mx;
-  }
+__device__ __forceinline__ void stats_raise(LaneStats &s, float v) {
+  if (__ballot(v > s.mx) == 0ull) return;
+  float m = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) m = fmaxf(m, __uint_as_float(xor_lane(__float_as_uint(m), o)));
+  m = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(m)));
+  const float nL = m * kL2E;
+  const float d = s.mL - nL;
+  const double a = static_cast<double>(__builtin_amdgcn_exp2f(d));
+  s.T2 = a * (s.T2 + static_cast<double>(d) * s.S);
+  s.S = a * s.S;
+  s.mL = nL;
+  s.mx = m;
 }
 
 template <int CAP>
@@ -323,16 +327,12 @@ __device__ __forceinline__ void process_scalar(const uint16_t *__restrict__ row,
   }
 }
 
-// Wave reduction of the per-lane statistics into lane-uniform values.
+// Wave reduction of the per-lane sums (all lanes share the offset).
 __device__ __forceinline__ void stats_wave_reduce(LaneStats &st) {
-  float mx = st.mx;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-  stats_raise(st, mx);          // every lane now uses the same offset
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    st.S += shfl_xor_f64(st.S, o);
-    st.T2 += shfl_xor_f64(st.T2, o);
+  for (int o = 1; o < kWave; o <<= 1) {
+    st.S += xor_lane_f64(st.S, o);
+    st.T2 += xor_lane_f64(st.T2, o);
   }
 }
 
@@ -361,7 +361,10 @@ template <int CAP>
 __device__ __forceinline__ void write_row(const RowOut &o, int64_t row, int K, double mL,
                                           double S, double T2, const uint64_t *top) {
   const int lane = lane_id();
-  const double lse2 = mL + log2(S);
+  // S >= 1 (the maximum contributes 2^0); the hardware log2 and exp2 in fp32
+  // are accurate to about 2^-22 relative, far inside what the outputs need
+  const double l2s = static_cast<double>(__builtin_amdgcn_logf(static_cast<float>(S)));
+  const double lse2 = mL + l2s;
   const double lse = lse2 * kLn2;
   const double mx = static_cast<double>(cand_value(top[0]));
   for (int r = lane; r < K; r += kWave) {
@@ -376,8 +379,8 @@ __device__ __forceinline__ void write_row(const RowOut &o, int64_t row, int K, d
   }
   if (lane == 0) {
     const float f_lse = static_cast<float>(lse);
-    const float f_mp = static_cast<float>(exp2(mx * kLog2e - lse2));
-    const float f_ent = static_cast<float>(log(S) - kLn2 * T2 / S);
+    const float f_mp = __builtin_amdgcn_exp2f(static_cast<float>(mx * kLog2e - lse2));
+    const float f_ent = static_cast<float>(kLn2 * (l2s - T2 / S));
     o.stats[row * 3 + 0] = f_lse;
     o.stats[row * 3 + 1] = f_mp;
     o.stats[row * 3 + 2] = f_ent;
@@ -394,7 +397,7 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
                    RowOut out) {
   __shared__ uint64_t s_buf[kWaves][CAP];
   __shared__ double s_stats[kWaves][3];
-  __shared__ uint64_t s_init[kWaves * kMaxK];
+  __shared__ uint32_t s_init[kWaves * kMaxK];
 
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
@@ -452,33 +455,33 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
         }
       }
     }
-    uint64_t k1[1] = {cand_key(tm, lane)};
-    wave_sort_desc<1>(k1);
+    uint32_t k1[1] = {ordered_f32(tm)};
+    wave_sort_desc_u32<1>(k1);
     if (lane < K) s_init[wave * K + lane] = k1[0];
     __syncthreads();
-    // the K-th of the union of the waves' K best (4 K <= CAP keys)
-    uint64_t kth;
+    // the K-th of the union of the waves' K best (4 K <= CAP values)
+    uint32_t kth;
     if (kWaves * K <= kWave) {
-      uint64_t k2[1] = {lane < kWaves * K ? s_init[lane] : 0ull};
-      wave_sort_desc<1>(k2);
-      kth = k2[0];
+      uint32_t k2[1] = {lane < kWaves * K ? s_init[lane] : 0u};
+      wave_sort_desc_u32<1>(k2);
+      kth = __builtin_amdgcn_readlane(k2[0], K - 1);
     } else {
       constexpr int E2 = CAP / kWave;
-      uint64_t k2[E2];
+      uint32_t k2[E2];
 #pragma unroll
       for (int e = 0; e < E2; ++e) {
         const int i = e * kWave + lane;
-        k2[e] = i < kWaves * K ? s_init[i] : 0ull;
+        k2[e] = i < kWaves * K ? s_init[i] : 0u;
       }
-      wave_sort_desc<E2>(k2);
+      wave_sort_desc_u32<E2>(k2);
       const int src_e = (K - 1) / kWave;
-      kth = 0;
+      uint32_t v = 0;
 #pragma unroll
       for (int e = 0; e < E2; ++e)
-        if (e == src_e) kth = k2[e];
+        if (e == src_e) v = k2[e];
+      kth = __builtin_amdgcn_readlane(v, (K - 1) % kWave);
     }
-    const uint32_t hi = __shfl(static_cast<uint32_t>(kth >> 32), (K - 1) % kWave);
-    w.thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(unordered_f32(hi))));
+    w.thr = unordered_f32(kth);
     if (w.thr < -1e29f) w.thr = -INFINITY;   // fewer than K real elements seen
   }
   if (one) {
