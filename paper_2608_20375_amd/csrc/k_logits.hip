@@ -5,16 +5,19 @@
 // probability).
 //
 // One pass over the bf16 logits, HBM-bound.  Each workgroup (4 waves) streams
-// one chunk of a row with 16-byte loads, 4 loads in flight per lane.  Per lane
-// it keeps an online softmax in log2 units: offset mL (fp32, = max * log2 e),
-// S = sum 2^y and T2 = sum 2^y * y with y = x * log2 e - mL, accumulated per
-// tile in fp32 and across tiles in fp64.  Top-K: every wave keeps a threshold
-// (the K-th best value it has buffered); a tile whose maximum falls below it
-// costs nothing more, otherwise its passing elements are appended to a per-wave
-// LDS buffer with ballot/mbcnt and the buffer is compacted by a wave bitonic
-// sort of (value desc, id asc) keys when full.  When there are too few rows to
-// fill the chip, rows are split over several workgroups whose partial results
-// a second small kernel merges.
+// one chunk of a row with 16-byte loads, 4 loads in flight per lane.  Each
+// wave keeps an online softmax in log2 units: a wave-uniform offset mL (fp32,
+// = max * log2 e) and per lane S = sum 2^y and T2 = sum 2^y * y with
+// y = x * log2 e - mL, accumulated per tile in fp32 and across tiles in fp64.
+// Top-K: every wave keeps a threshold (initially the K-th of the block's lane
+// maxima over the first tiles, later the K-th value it has buffered, shared
+// with the other waves); a tile whose maximum falls below it costs one
+// ballot; a group of 8 values whose maximum reaches it is copied raw to a
+// per-wave LDS ring, whose elements are offered to the wave's candidate
+// buffer (ballot/mbcnt appends, a wave bitonic sort of (value desc, id asc)
+// keys when full) only when the ring fills and at the end.  When there are
+// too few rows to fill the chip, rows are split over several workgroups whose
+// partial results a second small kernel merges.
 #include "graft_internal.h"
 
 namespace graft {
