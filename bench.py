@@ -241,7 +241,7 @@ def main():
             "global_batch": w.batch,
             "mean_budget": budgets,
             "mean_nodes": nodes,
-            "stage_us": {"logits_pass": 1e3 * stage_avg[0], "edge_scores": 1e3 * stage_avg[1],
+            "stage_us": {"logits_pass": 1e3 * stage_avg[0], "edge_scores_and_saba": 1e3 * stage_avg[1],
                          "select_emit_mask": 1e3 * stage_avg[2], "accept": 1e3 * stage_avg[3]},
         },
         "roofline": {

@@ -260,7 +260,7 @@ class Context:
         _check(lib().graft_profile_begin(self._h, int(max_calls)), "graft_profile_begin")
 
     def profile_end(self):
-        """(summed ms, timed launches) per stage: logits, edges, select, accept."""
+        """(summed ms, timed launches) per stage: logits, edges + budget, select, accept."""
         ms = (C.c_double * 4)()
         n = (C.c_int32 * 4)()
         _check(lib().graft_profile_end(self._h, ms, n), "graft_profile_end")

@@ -260,8 +260,8 @@ int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_
   hipError_t e = graft::launch_logits_pass(ctx, in->batch, in->logits, out, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: logits pass");
   if (ev) (void)hipEventRecord(ev[1], s);
-  e = graft::launch_edge_scores(ctx, in->batch, in->root_token, out->edge_scores, s);
-  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: edge scores");
+  e = graft::launch_edge_scores(ctx, in, out, s);
+  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: edge scores and budget");
   if (ev) (void)hipEventRecord(ev[2], s);
   e = graft::launch_select(ctx, in, out, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: selection");

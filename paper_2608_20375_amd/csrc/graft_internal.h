@@ -255,8 +255,8 @@ namespace graft {
 hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
                               const graft_tree_out *out, hipStream_t stream);
 hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStream_t stream);
-hipError_t launch_edge_scores(graft_ctx *ctx, int batch, const int32_t *root_token,
-                              float *edge_out, hipStream_t stream);
+hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+                              hipStream_t stream);
 hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
                          hipStream_t stream);
 hipError_t launch_accept(graft_ctx *ctx, int batch, const int32_t *n_nodes,

@@ -11,7 +11,8 @@
 //   then ranks the children of every parent by (score desc, token id asc) so
 //   that selection can expand a parent's children lazily in order.
 // The K x m x K contraction is at most 64 x 64 x 64 per (sequence, depth):
-// VALU work on LDS-staged rows; there is no dense tile to feed MFMA.
+// VALU work on LDS-staged rows; there is no dense tile to feed MFMA.  The
+// depth-1 block of each sequence also computes its SABA budget.
 #include "graft_internal.h"
 
 namespace graft {
@@ -60,6 +61,94 @@ FastDiv make_fastdiv(uint32_t d) {
   return f;
 }
 
+// SABA inputs and outputs of one round (Sec. "State-Aware Budget Allocation").
+struct SabaArgs {
+  const float *row_stats;       // [B, L, 3]: lse, maxprob, entropy
+  const float *hist;            // [B] caller's hist_t, or nullptr: the device ring
+  const int32_t *hist_ring;     // [B, window]
+  const int32_t *prefix_len;    // [B] or nullptr (0)
+  const int32_t *fixed_budget;  // [B]: budgets given by the caller, or nullptr: SABA
+  int window;
+  int32_t *budget;              // [B] out
+  float *saba_state;            // [B, 4] out (conf, ent, hist, tau) or nullptr
+};
+
+// B_t of sequence b by one wave: conf and ent are the means of the rows'
+// top-1 probability and entropy, hist the caller's value or the ring's mean;
+// tau = max(phi . [1, conf, ent, hist], tau_min); U(B) = (1 - exp(-B/tau)) /
+// (c0 + c1 B + c2 B prefix) (eqs. saba-gain, saba-cost) for every grid budget,
+// one lane each in fp64; B_t = the smallest budget with the largest U
+// (eq. saba-objective).
+__device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int L) {
+  const int lane = lane_id();
+  // every global load first
+  const float *rs = a.row_stats + (static_cast<int64_t>(b) * L + (lane < L ? lane : 0)) * 3;
+  const float f_conf = rs[1], f_ent = rs[2];
+  const float f_hist = a.hist ? a.hist[b] : 0.f;
+  const int32_t ring =
+      (!a.hist && lane < a.window) ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
+  const int32_t prefix_i = a.prefix_len ? a.prefix_len[b] : 0;
+  const int32_t fixed = a.fixed_budget ? a.fixed_budget[b] : 0;
+  const int32_t grid = lane < sp.n_grid ? sp.grid[lane] : 0;
+  double hist;
+  if (a.hist) {
+    hist = static_cast<double>(f_hist);
+  } else {
+    int64_t v = ring;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1)
+      v += static_cast<int64_t>(xor_lane_u64(static_cast<uint64_t>(v), o));
+    hist = static_cast<double>(v) / static_cast<double>(a.window);
+  }
+  double conf = lane < L ? static_cast<double>(f_conf) : 0.0;
+  double ent = lane < L ? static_cast<double>(f_ent) : 0.0;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    conf += xor_lane_f64(conf, o);
+    ent += xor_lane_f64(ent, o);
+  }
+  conf /= static_cast<double>(L);
+  ent /= static_cast<double>(L);
+  double tau = 0.0;
+  int budget;
+  if (!a.fixed_budget) {
+    tau = static_cast<double>(sp.phi[0]) + static_cast<double>(sp.phi[1]) * conf +
+          static_cast<double>(sp.phi[2]) * ent + static_cast<double>(sp.phi[3]) * hist;
+    if (tau < static_cast<double>(sp.tau_min)) tau = static_cast<double>(sp.tau_min);
+    const double prefix = static_cast<double>(prefix_i);
+    // the first maximum: largest U, ties (and a non-number U) to the smaller index
+    double u = -INFINITY;
+    if (lane < sp.n_grid) {
+      const double B = static_cast<double>(grid);
+      u = (1.0 - exp(-B / tau)) / (static_cast<double>(sp.c0) + static_cast<double>(sp.c1) * B +
+                                   static_cast<double>(sp.c2) * B * prefix);
+      if (!(u == u)) u = -INFINITY;
+    }
+    int best = lane;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const double ou = xor_lane_f64(u, o);
+      const int ob = static_cast<int>(xor_lane(static_cast<uint32_t>(best), o));
+      if (ou > u || (ou == u && ob < best)) {
+        u = ou;
+        best = ob;
+      }
+    }
+    budget = __builtin_amdgcn_readlane(grid, best < sp.n_grid ? best : 0);
+  } else {
+    budget = fixed;
+  }
+  if (lane == 0) {
+    a.budget[b] = budget;
+    if (a.saba_state) {
+      a.saba_state[b * 4 + 0] = static_cast<float>(conf);
+      a.saba_state[b * 4 + 1] = static_cast<float>(ent);
+      a.saba_state[b * 4 + 2] = static_cast<float>(hist);
+      a.saba_state[b * 4 + 3] = static_cast<float>(tau);
+    }
+  }
+}
+
 // Bitonic sort, descending, of the keys of each run of SEG consecutive lanes.
 template <int SEG>
 __device__ __forceinline__ uint64_t seg_sort_desc(uint64_t k) {
@@ -102,7 +191,8 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
             const float *__restrict__ depth_emb, ScorerParams sp,
             float *__restrict__ sorted_score, uint8_t *__restrict__ sorted_child,
             uint8_t *__restrict__ id_rank, uint8_t *__restrict__ positive,
-            float *__restrict__ edge_out, uint32_t *__restrict__ error_flag) {
+            float *__restrict__ edge_out, uint32_t *__restrict__ error_flag, SabaArgs sa,
+            SabaParams sp_saba) {
   extern __shared__ float smem[];
   const int mp = ((m + 3) & ~3) + 4;
   float *s_par = smem;
@@ -233,6 +323,8 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
     for (int i = K + lane; i < K * K; i += kEdgeThreads) edge_out[base + i] = 0.f;
   const bool any_pos = __ballot(pos) != 0ull;
   if (lane == 0) positive[row] = any_pos ? 1 : 0;
+  // the depth-1 block (one parent, the lightest) also computes the budget
+  if (l == 0) saba_budget(sa, sp_saba, b, L);
 }
 
 }  // namespace
@@ -247,9 +339,21 @@ hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_edge_scores(graft_ctx *ctx, int batch, const int32_t *root_token,
-                              float *edge_out, hipStream_t stream) {
+hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+                              hipStream_t stream) {
   const graft_dims &d = ctx->dims;
+  const int batch = in->batch;
+  const int32_t *root_token = in->root_token;
+  float *edge_out = out->edge_scores;
+  SabaArgs sa;
+  sa.row_stats = ctx->row_stats;
+  sa.hist = in->hist;
+  sa.hist_ring = ctx->hist_ring;
+  sa.prefix_len = in->prefix_len;
+  sa.fixed_budget = in->fixed_budget;
+  sa.window = d.hist_window;
+  sa.budget = out->budget;
+  sa.saba_state = out->saba_state;
   const int K = d.top_k, m = ctx->scorer.score_dim;
   const size_t mp = ((m + 3) & ~3) + 4;
   const size_t lds = sizeof(float) * (2 * static_cast<size_t>(K) * mp + K + m) +
@@ -261,7 +365,7 @@ hipError_t launch_edge_scores(graft_ctx *ctx, int batch, const int32_t *root_tok
                      static_cast<int64_t>(d.vocab), mdiv4, ctx->topk_ids, ctx->topk_logq,     \
                      root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
                      ctx->scorer, ctx->sorted_score, ctx->sorted_child, ctx->id_rank,         \
-                     ctx->positive, edge_out, ctx->error_flag)
+                     ctx->positive, edge_out, ctx->error_flag, sa, ctx->saba)
   if (K <= 1) GRAFT_EDGE(1);
   else if (K <= 2) GRAFT_EDGE(2);
   else if (K <= 4) GRAFT_EDGE(4);

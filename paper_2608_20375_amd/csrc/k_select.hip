@@ -1,11 +1,6 @@
-// k_select.hip -- SABA budget, budgeted best-first selection, canonical
-// emission and the ancestor mask; one workgroup per sequence.
-//
-// SABA (Sec. "State-Aware Budget Allocation"): tau = max(phi . [1, conf, ent,
-//   hist], tau_min); U(B) = (1 - exp(-B/tau)) / (c0 + c1 B + c2 B prefix)
-//   (eqs. saba-gain, saba-cost) is evaluated for every grid budget by one lane
-//   each in fp64; B_t = the smallest budget with the largest U
-//   (eq. saba-objective).
+// k_select.hip -- budgeted best-first selection, canonical emission and the
+// ancestor mask; one workgroup per sequence.  The budget B_t comes from the
+// edge stage (SABA).
 //
 // Selection (DDTree paragraph; TDES "Inference", eq. tdes-path-score): prefixes
 //   are ranked by their path score, the fp64 sum of fp32 edge scores from the
@@ -46,20 +41,17 @@ constexpr int kBins = 2048;
 constexpr int kStageRows = 4096;   // L * K * K edges staged in LDS up to this size
 
 struct SelectArgs {
-  int L, K, n_max, words, window;
-  const float *row_stats;       // [B, L, 3]
+  int L, K, n_max, words;
   const float *sorted_score;    // [B, L, K, K]
   const uint8_t *sorted_child;  // [B, L, K, K]
   const int32_t *topk_ids;      // [B, L, K]
   const uint8_t *id_rank;       // [B, L, K] rank of each candidate's token id in its depth
   const uint8_t *positive;      // [B, L] some edge score of that depth is > 0
-  const int32_t *root_token, *base_pos, *prefix_len, *fixed_budget;
-  const float *hist;
-  const int32_t *hist_ring;     // [B, window] (used when hist == nullptr)
-  int32_t *budget, *n_nodes, *tokens, *parents, *pos_ids;
+  const int32_t *base_pos;
+  const int32_t *budget;        // [B] from the edge stage
+  int32_t *n_nodes, *tokens, *parents, *pos_ids;
   uint64_t *mask;
   double *node_scores;
-  float *saba_state;
   uint32_t *error_flag;
 };
 
@@ -825,8 +817,7 @@ __device__ void canon_by_depth(SelMem &s, int K, int n) {
   }
 }
 
-__global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaParams sp,
-                                                             int use_saba) {
+__global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   __shared__ SelMem s;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -876,74 +867,14 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a, SabaP
       if (t + k * kStageThreads < nb16) reinterpret_cast<uint4 *>(s.rowc)[t + k * kStageThreads] = vb[k];
   }
 
-  // ---------------- SABA (wave 0) ----------------
+  // ---------------- budget (computed by the edge stage) and sign flags ----------------
   if (tid < kWave) {
     const int lane = tid;
     const bool pos = lane < L && a.positive[static_cast<int64_t>(b) * L + lane] != 0;
-    double hist;
-    if (a.hist) {
-      hist = static_cast<double>(a.hist[b]);
-    } else {
-      int64_t v = lane < a.window ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1)
-        v += static_cast<int64_t>(xor_lane_u64(static_cast<uint64_t>(v), o));
-      hist = static_cast<double>(v) / static_cast<double>(a.window);
-    }
-    double conf = 0.0, ent = 0.0;
-    if (lane < L) {
-      const float *rs = a.row_stats + (static_cast<int64_t>(b) * L + lane) * 3;
-      conf = static_cast<double>(rs[1]);
-      ent = static_cast<double>(rs[2]);
-    }
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      conf += xor_lane_f64(conf, o);
-      ent += xor_lane_f64(ent, o);
-    }
-    conf /= static_cast<double>(L);
-    ent /= static_cast<double>(L);
-    double tau = 0.0;
-    int budget;
-    if (use_saba) {
-      tau = static_cast<double>(sp.phi[0]) + static_cast<double>(sp.phi[1]) * conf +
-            static_cast<double>(sp.phi[2]) * ent + static_cast<double>(sp.phi[3]) * hist;
-      if (tau < static_cast<double>(sp.tau_min)) tau = static_cast<double>(sp.tau_min);
-      const double prefix = a.prefix_len ? static_cast<double>(a.prefix_len[b]) : 0.0;
-      // U of one grid budget per lane, then the first maximum: largest U,
-      // ties (and a non-number U) to the smaller grid index
-      double u = -INFINITY;
-      if (lane < sp.n_grid) {
-        const double B = static_cast<double>(sp.grid[lane]);
-        u = (1.0 - exp(-B / tau)) / (static_cast<double>(sp.c0) + static_cast<double>(sp.c1) * B +
-                                     static_cast<double>(sp.c2) * B * prefix);
-        if (!(u == u)) u = -INFINITY;
-      }
-      int best = lane;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const double ou = xor_lane_f64(u, o);
-        const int ob = static_cast<int>(xor_lane(static_cast<uint32_t>(best), o));
-        if (ou > u || (ou == u && ob < best)) {
-          u = ou;
-          best = ob;
-        }
-      }
-      budget = sp.grid[best < sp.n_grid ? best : 0];
-    } else {
-      budget = a.fixed_budget[b];
-    }
     const bool mono = __ballot(pos) == 0ull;
     if (lane == 0) {
-      s.sc[kBudget] = budget;
+      s.sc[kBudget] = a.budget[b];
       s.sc[kMono] = mono ? 1 : 0;
-      a.budget[b] = budget;
-      if (a.saba_state) {
-        a.saba_state[b * 4 + 0] = static_cast<float>(conf);
-        a.saba_state[b * 4 + 1] = static_cast<float>(ent);
-        a.saba_state[b * 4 + 2] = static_cast<float>(hist);
-        a.saba_state[b * 4 + 3] = static_cast<float>(tau);
-      }
     }
   }
   __syncthreads();
@@ -1056,19 +987,12 @@ hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_t
   a.K = d.top_k;
   a.n_max = d.max_nodes;
   a.words = (d.max_nodes + 63) / 64;
-  a.window = d.hist_window;
-  a.row_stats = ctx->row_stats;
   a.sorted_score = ctx->sorted_score;
   a.sorted_child = ctx->sorted_child;
   a.topk_ids = ctx->topk_ids;
   a.id_rank = ctx->id_rank;
   a.positive = ctx->positive;
-  a.root_token = in->root_token;
   a.base_pos = in->base_pos;
-  a.prefix_len = in->prefix_len;
-  a.fixed_budget = in->fixed_budget;
-  a.hist = in->hist;
-  a.hist_ring = ctx->hist_ring;
   a.budget = out->budget;
   a.n_nodes = out->n_nodes;
   a.tokens = out->tokens;
@@ -1076,11 +1000,8 @@ hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_t
   a.pos_ids = out->pos_ids;
   a.mask = out->mask;
   a.node_scores = out->node_scores;
-  a.saba_state = out->saba_state;
   a.error_flag = ctx->error_flag;
-  const int use_saba = in->fixed_budget == nullptr;
-  hipLaunchKernelGGL(select_kernel, dim3(in->batch), dim3(kSelThreads), 0, stream, a, ctx->saba,
-                     use_saba);
+  hipLaunchKernelGGL(select_kernel, dim3(in->batch), dim3(kSelThreads), 0, stream, a);
   return hipGetLastError();
 }
 
