@@ -271,7 +271,7 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
 // next power of two >= kv.  Every load is issued unconditionally (clamped to
 // the row) before any use, so one memory round trip covers the row.
 
-// Number of children r < K with ps + row[r] >= theta.
+// Number of children r < K with ps + row[r] >= theta (fp64 sums).
 template <int KV>
 __device__ __forceinline__ int count_reach(const float *row, int kv, double ps, double theta,
                                            float &last) {
@@ -825,6 +825,13 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   const float *ss = a.sorted_score + static_cast<int64_t>(b) * L * K * K;
   const uint8_t *sc = a.sorted_child + static_cast<int64_t>(b) * L * K * K;
 
+  // wave 0: the budget (computed by the edge stage) and the sign flags
+  int budget0 = 0;
+  bool pos0 = false;
+  if (tid < kWave) {
+    budget0 = a.budget[b];
+    pos0 = tid < L && a.positive[static_cast<int64_t>(b) * L + tid] != 0;
+  }
   // candidates and their rank by token id
   for (int i = tid; i < L * K; i += kSelThreads) {
     s.cand[i] = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
@@ -867,13 +874,11 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
       if (t + k * kStageThreads < nb16) reinterpret_cast<uint4 *>(s.rowc)[t + k * kStageThreads] = vb[k];
   }
 
-  // ---------------- budget (computed by the edge stage) and sign flags ----------------
+  // ---------------- budget and sign flags ----------------
   if (tid < kWave) {
-    const int lane = tid;
-    const bool pos = lane < L && a.positive[static_cast<int64_t>(b) * L + lane] != 0;
-    const bool mono = __ballot(pos) == 0ull;
-    if (lane == 0) {
-      s.sc[kBudget] = a.budget[b];
+    const bool mono = __ballot(pos0) == 0ull;
+    if (tid == 0) {
+      s.sc[kBudget] = budget0;
       s.sc[kMono] = mono ? 1 : 0;
     }
   }
