@@ -196,8 +196,21 @@ __device__ __noinline__ Compacted flush_ool(uint64_t *buf, int count, float thr,
   }
   float v[8];
   unpack8(r, v);
+  float gm = fmaxf(fmaxf(fmaxf(v[0], v[1]), v[2]), v[3]);
+  gm = fmaxf(fmaxf(fmaxf(gm, v[4]), v[5]), fmaxf(v[6], v[7]));
+  // The K-th largest group maximum is a lower bound of the wave's K-th value
+  // (K distinct groups reach it): raise the threshold before offering.
+  if (K <= kWave && rcount >= K) {
+    uint32_t key[1] = {have ? ordered_f32(gm) : 0u};
+    wave_sort_desc_u32<1>(key);
+    const float tau = unordered_f32(__builtin_amdgcn_readlane(key[0], K - 1));
+    if (tau > w.thr) w.thr = tau;
+  }
+  const bool live = have && gm >= w.thr;
+  if (__ballot(live) != 0ull) {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) wave_offer<CAP>(w, K, v[e], id0 + e, have);
+    for (int e = 0; e < 8; ++e) wave_offer<CAP>(w, K, v[e], id0 + e, live);
+  }
   return {w.count, w.thr};
 }
 
@@ -244,14 +257,16 @@ __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t 
       for (int e = 0; e < 8; ++e) v[u][e] = kNegBig;
     }
   }
+  // group maxima as chains of 3-input maxima (v_max3_f32)
   float sub[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
-    float a = fmaxf(fmaxf(v[u][0], v[u][1]), fmaxf(v[u][2], v[u][3]));
-    float b = fmaxf(fmaxf(v[u][4], v[u][5]), fmaxf(v[u][6], v[u][7]));
-    sub[u] = fmaxf(a, b);
+    const float a = fmaxf(fmaxf(v[u][0], v[u][1]), v[u][2]);
+    const float b = fmaxf(fmaxf(a, v[u][3]), v[u][4]);
+    const float c = fmaxf(fmaxf(b, v[u][5]), v[u][6]);
+    sub[u] = fmaxf(c, v[u][7]);
   }
-  const float tmax = fmaxf(fmaxf(sub[0], sub[1]), fmaxf(sub[2], sub[3]));
+  const float tmax = fmaxf(fmaxf(fmaxf(sub[0], sub[1]), sub[2]), sub[3]);
 
   // top-K candidates; any wave's threshold bounds the block's K-th value.
   // A group of 8 whose largest value reaches the threshold is copied raw to
@@ -277,18 +292,25 @@ __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t 
   // softmax statistics
   stats_raise(st, tmax);
   const float mL = st.mL;
+  // all arguments, then all exponentials, then the sums: no exp result is
+  // consumed by the instruction right after it
   float s[kUnroll], t[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
-    s[u] = 0.f;
-    t[u] = 0.f;
+    float y[8], ex[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = __builtin_fmaf(v[u][e], kL2E, -mL);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float y = __builtin_fmaf(v[u][e], kL2E, -mL);
-      float ex = __builtin_amdgcn_exp2f(y);
-      if (MASKED) ex = ok[u] ? ex : 0.f;
-      s[u] += ex;
-      t[u] = __builtin_fmaf(ex, y, t[u]);
+      ex[e] = __builtin_amdgcn_exp2f(y[e]);
+      if (MASKED) ex[e] = ok[u] ? ex[e] : 0.f;
+    }
+    s[u] = ex[0];
+    t[u] = ex[0] * y[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) {
+      s[u] += ex[e];
+      t[u] = __builtin_fmaf(ex[e], y[e], t[u]);
     }
   }
   st.S += static_cast<double>((s[0] + s[1]) + (s[2] + s[3]));
@@ -402,7 +424,7 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
   __shared__ double s_stats[kWaves][3];
   __shared__ uint32_t s_init[kWaves * kMaxK];
 
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = lane_id();
   const int64_t row = blockIdx.x / splits;
   const int split = blockIdx.x % splits;
