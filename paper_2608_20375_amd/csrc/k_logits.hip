@@ -317,6 +317,45 @@ __device__ __forceinline__ void process_tile(const uint4 (&q)[kUnroll], int64_t 
   st.T2 += static_cast<double>((t[0] + t[1]) + (t[2] + t[3]));
 }
 
+// One vector per lane (valid lanes only): statistics and top-K candidates.
+template <int CAP>
+__device__ __forceinline__ void process_vec(const uint4 q, int64_t vi, bool valid, int64_t elem0,
+                                            LaneStats &st, WaveBuf<CAP> &w, int K) {
+  float v[8];
+  unpack8(q, v);
+  if (!valid) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = kNegBig;
+  }
+  const float a = fmaxf(fmaxf(v[0], v[1]), v[2]);
+  const float b = fmaxf(fmaxf(a, v[3]), v[4]);
+  const float c = fmaxf(fmaxf(b, v[5]), v[6]);
+  const float g = fmaxf(c, v[7]);
+  const bool pass = valid && g >= w.thr;
+  const uint64_t m = __ballot(pass);
+  if (m != 0ull) {
+    const int n = __popcll(m);
+    if (w.rcount + n > kRing) wave_flush<CAP>(w, K);
+    if (pass) {
+      const int slot = w.rcount + lanes_below(m);
+      w.rq[slot] = q;
+      w.rid[slot] = static_cast<uint32_t>(elem0 + vi * 8);
+    }
+    w.rcount = __builtin_amdgcn_readfirstlane(w.rcount + n);
+  }
+  stats_raise(st, g);
+  float s = 0.f, t = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float y = __builtin_fmaf(v[e], kL2E, -st.mL);
+    const float ex = valid ? __builtin_amdgcn_exp2f(y) : 0.f;
+    s += ex;
+    t = __builtin_fmaf(ex, y, t);
+  }
+  st.S += static_cast<double>(s);
+  st.T2 += static_cast<double>(t);
+}
+
 // One full tile with the block-shared threshold (other waves update their
 // entries without a barrier; relaxed atomic reads keep the LDS addressing).
 template <int CAP>
@@ -461,6 +500,18 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     load_tile<false>(vec, t * kTileVec, n_vec, cur);
     load_tile<false>(vec, (two ? t + kWaves : t) * kTileVec, n_vec, nxt);
   }
+  // The vectors past the full tiles (fewer than kTileVec) are spread over the
+  // block, one per lane, and loaded with the first tiles; surplus lanes read
+  // the last vector and are masked.
+  const bool partial = n_full * kTileVec < n_vec;
+  const int64_t pv = n_full * kTileVec + static_cast<int64_t>(wave) * kWave + lane;
+  const bool pvalid = partial && pv < n_vec;
+  uint4 extra = make_uint4(0, 0, 0, 0);
+  if (partial) {
+    const u32x4 x =
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(vec) + (pvalid ? pv : n_vec - 1));
+    extra = make_uint4(x.x, x.y, x.z, x.w);
+  }
   // Initial threshold, block wide: the K-th largest of the 256 lane maxima
   // over the waves' first two tiles.  K elements reach it, so it is a lower
   // bound of the row's K-th largest value.
@@ -479,6 +530,12 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
           for (int e = 0; e < 8; ++e) tm = fmaxf(tm, vv[e]);
         }
       }
+    }
+    if (pvalid) {
+      float vv[8];
+      unpack8(extra, vv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) tm = fmaxf(tm, vv[e]);
     }
     uint32_t k1[1] = {ordered_f32(tm)};
     wave_sort_desc_u32<1>(k1);
@@ -509,6 +566,7 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     w.thr = unordered_f32(kth);
     if (w.thr < -1e29f) w.thr = -INFINITY;   // fewer than K real elements seen
   }
+  if (partial) process_vec<CAP>(extra, pv, pvalid, elem0, st, w, K);
   if (one) {
     // ping-pong between two register buffers: the loads of tile t + kWaves are
     // in flight while tile t is processed
@@ -528,11 +586,6 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
       load_tile<false>(vec, tl * kTileVec, n_vec, nxt);
       step_tile<CAP>(cur, t, n_vec, elem0, st, w, K, s_thr, wave);
     }
-  }
-  if (t == n_full && n_full * kTileVec < n_vec) {
-    uint4 cur[kUnroll];
-    load_tile<true>(vec, t * kTileVec, n_vec, cur);
-    process_tile<CAP, true>(cur, t * kTileVec, n_vec, elem0, st, w, K, -INFINITY);
   }
   // Misaligned head [0, a0) and tail [a0 + 8 nv_row, V): split 0, wave 0.
   if (split == 0 && wave == 0) {
