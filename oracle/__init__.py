@@ -50,7 +50,8 @@ class Params(C.Structure):
 
 class SeqIn(C.Structure):
     _fields_ = [("logits", C.c_void_p), ("root_token", C.c_int32), ("base_pos", C.c_int32),
-                ("prefix_len", C.c_int32), ("fixed_budget", C.c_int32), ("hist", C.c_double)]
+                ("prefix_len", C.c_int32), ("fixed_budget", C.c_int32), ("hist", C.c_double),
+                ("hidden", C.c_void_p), ("hidden_dim", C.c_int32)]
 
 
 class SeqOut(C.Structure):
@@ -62,6 +63,7 @@ class SeqOut(C.Structure):
         ("n_nodes", C.c_int32), ("tokens", C.c_void_p), ("parents", C.c_void_p),
         ("pos_ids", C.c_void_p), ("depth", C.c_void_p), ("node_scores", C.c_void_p),
         ("mask", C.c_void_p), ("boundary_gap", C.c_double), ("min_pop_gap", C.c_double),
+        ("degen", C.c_double), ("adj_cos", C.c_void_p),
     ]
 
 
@@ -84,6 +86,8 @@ def lib():
                                       C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_double),
                                       C.c_void_p]
             L.oracle_saba.restype = C.c_int32
+            L.oracle_degen.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]
+            L.oracle_degen.restype = C.c_double
             L.oracle_build_sequence.argtypes = [C.POINTER(Params), C.POINTER(SeqIn),
                                                 C.POINTER(SeqOut)]
             L.oracle_build_sequence.restype = C.c_int
@@ -175,17 +179,28 @@ def edge_scores(P: Params, cand: np.ndarray, logq: np.ndarray, root: int):
     return edge, f
 
 
-def saba(P: Params, conf: float, ent: float, hist: float, prefix: int):
+def saba(P: Params, conf: float, feat: float, hist: float, prefix: int):
+    """feat: the state's second feature (degen, or the mean entropy)."""
     tau, rel = C.c_double(), C.c_double()
     util = np.empty(P.n_grid, np.float64)
-    b = lib().oracle_saba(C.byref(P), conf, ent, hist, int(prefix), C.byref(tau), C.byref(rel),
+    b = lib().oracle_saba(C.byref(P), conf, feat, hist, int(prefix), C.byref(tau), C.byref(rel),
                           _p(util))
     return int(b), tau.value, rel.value, util
 
 
+def degen(hidden: np.ndarray):
+    """O5a on hidden states [L, H] bf16 bits: (degen, r[L-1])."""
+    hidden = _c(hidden, np.uint16)
+    L, H = hidden.shape
+    r = np.empty(max(L - 1, 1), np.float64)
+    d = lib().oracle_degen(_p(hidden), int(L), int(H), _p(r))
+    return float(d), r[:max(L - 1, 0)].copy()
+
+
 def _alloc_out(L, K, n_max):
     words = (n_max + 63) // 64
-    a = dict(topk_ids=np.empty((L, K), np.int32), topk_logq=np.empty((L, K), np.float64),
+    a = dict(adj_cos=np.empty(max(L - 1, 1)),
+             topk_ids=np.empty((L, K), np.int32), topk_logq=np.empty((L, K), np.float64),
              row_lse=np.empty(L), row_maxprob=np.empty(L), row_entropy=np.empty(L),
              edge=np.empty((L, K, K)), tokens=np.empty(n_max, np.int32),
              parents=np.empty(n_max, np.int32), pos_ids=np.empty(n_max, np.int32),
@@ -200,17 +215,22 @@ def _alloc_out(L, K, n_max):
 def _collect(o: SeqOut, a: dict) -> dict:
     a = dict(a)
     for k in ("conf", "ent", "tau", "budget", "saba_relgap", "n_nodes", "boundary_gap",
-              "min_pop_gap"):
+              "min_pop_gap", "degen"):
         a[k] = getattr(o, k)
+    a["adj_cos"] = a["adj_cos"][:max(len(a["row_lse"]) - 1, 0)]
     return a
 
 
 def build_sequence(P: Params, logits: np.ndarray, root: int, base_pos: int, prefix: int = 0,
-                   fixed_budget: int = 0, hist: float = 0.0) -> dict:
-    """O2..O7 for one sequence; logits [L, V] bf16 bits."""
+                   fixed_budget: int = 0, hist: float = 0.0, hidden=None) -> dict:
+    """O2..O7 for one sequence; logits [L, V] bf16 bits, hidden [L, H] bf16 bits or None."""
     logits = _c(logits, np.uint16)
     assert logits.shape == (P.L, P.V)
-    si = SeqIn(_p(logits), int(root), int(base_pos), int(prefix), int(fixed_budget), float(hist))
+    hid = _c(hidden, np.uint16)
+    if hid is not None:
+        assert hid.ndim == 2 and hid.shape[0] == P.L
+    si = SeqIn(_p(logits), int(root), int(base_pos), int(prefix), int(fixed_budget), float(hist),
+               _p(hid), 0 if hid is None else int(hid.shape[1]))
     o, a = _alloc_out(P.L, P.K, P.n_max)
     rc = lib().oracle_build_sequence(C.byref(P), C.byref(si), C.byref(o))
     if rc:
@@ -257,10 +277,13 @@ def build_round(w, inputs: dict, scorer: dict, saba_p: dict | None, seqs=None,
     seqs = list(range(w.batch)) if seqs is None else list(seqs)
     fb = inputs.get("fixed_budget")
 
+    hid = inputs.get("hidden")
+
     def one(b):
         return build_sequence(P, inputs["logits"][b], inputs["root_token"][b],
                               inputs["base_pos"][b], inputs["prefix_len"][b],
-                              0 if fb is None else fb[b], float(inputs["hist"][b]))
+                              0 if fb is None else fb[b], float(inputs["hist"][b]),
+                              None if hid is None else hid[b])
 
     if threads > 1:
         with ThreadPoolExecutor(threads) as ex:

@@ -15,7 +15,9 @@
  *   O4  TDES edge scores (Sec. "Target-Distilled Edge Scoring",
  *       eqs. tdes-score, tdes-center, tdes-bitower)
  *   O5  SABA budget (Sec. "State-Aware Budget Allocation",
- *       eqs. saba-objective, saba-gain, saba-cost; budget grid)
+ *       eqs. saba-objective, saba-gain, saba-cost; budget grid), with the
+ *       representation-degeneration signal of the decoding state when the
+ *       drafter's hidden states are given (same section, degen_t)
  *   O6  best-first selection over a max-heap of candidate prefixes ranked by
  *       the path score (DDTree paragraph, eq. ddtree-path-score; TDES
  *       "Inference", eq. tdes-path-score)
@@ -33,9 +35,13 @@
  *     path lexicographically ascending);
  *   - depth-1 edges have the root token as parent; the children set of every
  *     parent is all K candidates of the next depth;
- *   - the SABA state is s = [1, conf, ent, hist] (mean per-depth entropy stands
- *     in for the degeneration signal, which needs drafter hidden states);
- *     tau = max(phi . s, tau_min); ties in the utility go to the smaller budget;
+ *   - the SABA state is s = [1, conf, degen, hist] when hidden states are
+ *     given and s = [1, conf, ent, hist] otherwise (mean per-depth entropy
+ *     stands in for degen); tau = max(phi . s, tau_min); ties in the utility
+ *     go to the smaller budget;
+ *   - degen uses D = L hidden states h_1..h_L (one per drafted position); a
+ *     cosine with a zero vector is 0; with L = 1 there is no adjacent pair and
+ *     degen = 0;
  *   - acc_len excludes the bonus token.
  *
  * Parity pins: see tests/test_oracle_*.py.  The paper's trained TDES scorer is
@@ -135,7 +141,7 @@ typedef struct {
     int32_t use_saba;
     const int32_t *grid;     /* candidate budgets, ascending */
     int32_t n_grid;
-    double phi[4];           /* tau = phi . [1, conf, ent, hist] */
+    double phi[4];           /* tau = phi . [1, conf, degen (or ent), hist] */
     double tau_min, c0, c1, c2;
 } oracle_params;
 
@@ -143,6 +149,8 @@ typedef struct {
     const uint16_t *logits;  /* [L, V] bf16 bits */
     int32_t root_token, base_pos, prefix_len, fixed_budget;
     double hist;
+    const uint16_t *hidden;  /* [L, H] bf16 bits of the drafter's hidden states, or NULL */
+    int32_t hidden_dim;      /* H */
 } oracle_seq_in;
 
 typedef struct {
@@ -162,6 +170,9 @@ typedef struct {
     /* audit of the floating-point decisions */
     double boundary_gap;     /* S(last selected) - S(best unselected frontier prefix) */
     double min_pop_gap;      /* min over pops of S(popped) - S(next best in heap) */
+    /* representation degeneration (hidden states given) */
+    double degen;
+    double *adj_cos;         /* [L - 1] r_d, or NULL */
 } oracle_seq_out;
 
 /* ------------------------------------------------------------------------- */
@@ -238,17 +249,46 @@ ORACLE_EXPORT int oracle_edge_scores(const oracle_params *P, const int32_t *cand
 }
 
 /* ------------------------------------------------------------------------- */
+/* O5a: representation degeneration of the SABA decoding state.               */
+/*   r_d = cos(h_d, h_{d+1}) for d = 1..D-1 (D = L hidden states, row-major    */
+/*   [L, H] bf16), degen = (1/(D-1)) sum_d r_d + (r_{D-1} - r_1).             */
+/* ------------------------------------------------------------------------- */
+ORACLE_EXPORT double oracle_degen(const uint16_t *hidden, int32_t L, int32_t H, double *adj_cos)
+{
+    if (L < 2) return 0.0;
+    double sum = 0.0, first = 0.0, last = 0.0;
+    for (int d = 0; d + 1 < L; ++d) {
+        const uint16_t *a = hidden + (size_t)d * (size_t)H;
+        const uint16_t *b = a + H;
+        double ab = 0.0, aa = 0.0, bb = 0.0;
+        for (int i = 0; i < H; ++i) {
+            double x = bf16_value(a[i]), y = bf16_value(b[i]);
+            ab += x * y;
+            aa += x * x;
+            bb += y * y;
+        }
+        double r = (aa > 0.0 && bb > 0.0) ? ab / sqrt(aa * bb) : 0.0;
+        if (adj_cos) adj_cos[d] = r;
+        if (d == 0) first = r;
+        last = r;
+        sum += r;
+    }
+    return sum / (double)(L - 1) + (last - first);
+}
+
+/* ------------------------------------------------------------------------- */
 /* O5: SABA.  B_t = argmax_B U(B),  U = G / C                                 */
 /*   G(B) = 1 - exp(-B / tau)        (eq. saba-gain, tau = phi^T s_t)         */
 /*   C(B) = c0 + c1 B + c2 B prefix  (eq. saba-cost)                          */
 /* The grid is scanned in ascending order; a later budget replaces the        */
 /* current best only when its utility is strictly larger.                     */
 /* ------------------------------------------------------------------------- */
-ORACLE_EXPORT int32_t oracle_saba(const oracle_params *P, double conf, double ent,
+ORACLE_EXPORT int32_t oracle_saba(const oracle_params *P, double conf, double degen,
                                   double hist, int32_t prefix, double *tau_out,
                                   double *relgap_out, double *util_out)
 {
-    double tau = P->phi[0] + P->phi[1] * conf + P->phi[2] * ent + P->phi[3] * hist;
+    /* s = [1, conf, degen, hist]; callers without hidden states pass ent */
+    double tau = P->phi[0] + P->phi[1] * conf + P->phi[2] * degen + P->phi[3] * hist;
     if (tau < P->tau_min) tau = P->tau_min;
     int32_t best = -1;
     double ubest = -INFINITY, usecond = -INFINITY;
@@ -457,10 +497,17 @@ ORACLE_EXPORT int oracle_build_sequence(const oracle_params *P, const oracle_seq
     ent /= (double)L;
     o->conf = conf;
     o->ent = ent;
+    /* the state's second feature: degen from the hidden states, else ent */
+    double feat = ent;
+    o->degen = 0.0;
+    if (in->hidden) {
+        o->degen = oracle_degen(in->hidden, L, in->hidden_dim, o->adj_cos);
+        feat = o->degen;
+    }
     int rc = oracle_edge_scores(P, o->topk_ids, o->topk_logq, in->root_token, o->edge, NULL);
     if (rc) return rc;
     if (P->use_saba) {
-        o->budget = oracle_saba(P, conf, ent, in->hist, in->prefix_len, &o->tau,
+        o->budget = oracle_saba(P, conf, feat, in->hist, in->prefix_len, &o->tau,
                                 &o->saba_relgap, NULL);
     } else {
         o->budget = in->fixed_budget;

@@ -33,7 +33,7 @@ import numpy as np
 __all__ = [
     "Workload", "WORKLOADS", "workload", "bf16_from_f32", "f32_from_bf16",
     "gen_sequence_logits", "gen_round", "gen_scorer", "saba_params",
-    "hist_ring_init", "node_targets", "splitmix64", "NODE_TARGET_P_NUM",
+    "hist_ring_init", "node_targets", "splitmix64", "NODE_TARGET_P_NUM", "gen_hidden",
 ]
 
 HIST_WINDOW = 4
@@ -206,6 +206,30 @@ def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = Tru
         out["fixed_budget"] = np.full(B, w.fixed_budget, dtype=np.int32)
     if w.targets == "depth":
         out["target_depth"] = tdepth
+    return out
+
+
+def gen_hidden(w: Workload, rnd: int = 0, hidden_dim: int = 4096, attempts=None,
+               seqs=None) -> np.ndarray:
+    """Drafter hidden states [batch, L, H] as bf16 bits, one per drafted position.
+
+    h_d = a_d c + n_d with a shared direction c ~ N(0, I_H) and independent
+    n_d ~ N(0, I_H): the share a_d = s (0.5 + 2.5 d / (L - 1)) of the common
+    direction grows with the depth d = 0..L-1, so adjacent states grow more
+    alike at later positions (the trend the degeneration signal measures);
+    s ~ U(0.3, 1.5) per sequence spreads the signal over the batch.
+    """
+    B, L, H = w.batch, w.L, int(hidden_dim)
+    attempts = np.zeros(B, dtype=np.int64) if attempts is None else np.asarray(attempts)
+    seqs = range(B) if seqs is None else seqs
+    out = np.zeros((B, L, H), dtype=np.uint16)
+    ramp = 0.5 + 2.5 * np.arange(L, dtype=np.float32) / max(L - 1, 1)
+    for b in seqs:
+        g = _rng(w, rnd, b, int(attempts[b]), 4)
+        c = g.standard_normal(H, dtype=np.float32)
+        n = g.standard_normal((L, H), dtype=np.float32)
+        s_b = np.float32(g.uniform(0.3, 1.5))
+        out[b] = bf16_from_f32((s_b * ramp)[:, None] * c[None, :] + n)
     return out
 
 

@@ -243,6 +243,86 @@ def test_saba_limits_and_ties():
 
 
 # ---------------------------------------------------------------------------
+# O5a: representation degeneration (SABA decoding state)
+# ---------------------------------------------------------------------------
+
+def _hidden_with_cosines(H=16):
+    """Hidden states built so that the adjacent cosines are known by
+    construction (small integers, exact in bf16):
+      h1 = 3 e0            h2 = 3 e0 + 4 e1   (3-4-5 triangle: cos = 3/5)
+      h3 = 6 e0 + 8 e1     (a multiple of h2: cos = 1)
+      h4 = 5 e2            (disjoint support: cos = 0)
+      h5 = -10 e2          (opposite direction: cos = -1)"""
+    h = np.zeros((5, H), np.float32)
+    h[0, 0] = 3
+    h[1, 0], h[1, 1] = 3, 4
+    h[2, 0], h[2, 1] = 6, 8
+    h[3, 2] = 5
+    h[4, 2] = -10
+    return h, [0.6, 1.0, 0.0, -1.0]
+
+
+def test_degen_worked_example():
+    h, r = _hidden_with_cosines()
+    d, got = oracle.degen(bf16(h))
+    assert np.allclose(got, r, atol=1e-15)
+    # the paper's degen: mean adjacent similarity plus its late-minus-early rise
+    # (r_4 - r_1 = -1.6 here), with the cosines above: 0.15 - 1.6
+    assert d == pytest.approx(0.15 - 1.6, abs=1e-15)
+
+
+def test_degen_special_cases_and_invariants():
+    g = np.random.default_rng(7)
+    # L = 1: no adjacent pair; L = 2: mean and rise collapse to r_1
+    assert oracle.degen(bf16(g.standard_normal((1, 32))))[0] == 0.0
+    h2 = bf16(g.standard_normal((2, 32)))
+    d2, r2 = oracle.degen(h2)
+    assert d2 == r2[0]
+    # identical states: every r = 1, degen = 1; a zero state gives cosine 0
+    same = bf16(np.tile(g.standard_normal(24), (6, 1)))
+    assert oracle.degen(same)[0] == pytest.approx(1.0, abs=1e-14)
+    z = np.asarray(S.f32_from_bf16(same)).copy()
+    z[2] = 0
+    dz, rz = oracle.degen(bf16(z))
+    assert rz[1] == 0.0 and rz[2] == 0.0
+    # scaling each state by a power of two (exact in bf16) changes nothing
+    x = g.standard_normal((8, 64)).astype(np.float32)
+    scale = (2.0 ** g.integers(-3, 4, size=8)).astype(np.float32)[:, None]
+    d, r = oracle.degen(bf16(x))
+    ds, rs = oracle.degen(bf16(x * scale))
+    assert ds == pytest.approx(d, abs=1e-14) and np.allclose(rs, r, atol=1e-14)
+    # cosines against numpy's normalised dot products of the bf16 values
+    xv = S.f32_from_bf16(bf16(x)).astype(np.float64)
+    u = xv / np.linalg.norm(xv, axis=1, keepdims=True)
+    assert np.allclose(r, np.einsum("ij,ij->i", u[:-1], u[1:]), atol=1e-14)
+    # reversing the depth order keeps the mean and negates the rise:
+    # degen(h) + degen(reversed h) = 2 * mean(r)
+    dr, _ = oracle.degen(bf16(x[::-1].copy()))
+    assert d + dr == pytest.approx(2 * r.mean(), abs=1e-14)
+
+
+def test_degen_drives_the_saba_state():
+    """With hidden states the budget follows tau = phi . [1, conf, degen, hist]
+    instead of the entropy stand-in."""
+    w = S.workload(2, batch=2, V=4096)
+    inp = S.gen_round(w, with_targets=False)
+    sc = S.gen_scorer(w)
+    sp = S.saba_params(w)
+    h = S.gen_hidden(w, hidden_dim=64)
+    P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
+    b = 0
+    res_h = oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b], inp["base_pos"][b],
+                                  inp["prefix_len"][b], 0, float(inp["hist"][b]), h[b])
+    d, r = oracle.degen(h[b])
+    assert res_h["degen"] == d and np.array_equal(res_h["adj_cos"], r)
+    bud, tau, _, _ = oracle.saba(P, res_h["conf"], d, float(inp["hist"][b]), inp["prefix_len"][b])
+    assert res_h["budget"] == bud and res_h["tau"] == tau
+    phi = [float(v) for v in sp["phi"]]
+    expect = phi[0] + phi[1] * res_h["conf"] + phi[2] * d + phi[3] * float(inp["hist"][b])
+    assert tau == pytest.approx(max(expect, sp["tau_min"]), rel=1e-12)
+
+
+# ---------------------------------------------------------------------------
 # O6/O7: selection and emission against brute-force enumeration
 # ---------------------------------------------------------------------------
 
