@@ -214,6 +214,43 @@ __device__ __noinline__ Compacted flush_ool(uint64_t *buf, int count, float thr,
   return {w.count, w.thr};
 }
 
+// The last flush of a wave's ring, inlined so that every access stays an LDS
+// access.  It first takes the largest threshold any wave of the block has
+// published (each is a lower bound of the block's K-th value), then the K-th
+// largest group maximum of the ring, and offers what survives both.
+template <int CAP>
+__device__ __forceinline__ void wave_flush_last(WaveBuf<CAP> &w, int K, const float *s_thr) {
+  const int lane = lane_id();
+  float o = w.thr;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i)
+    o = fmaxf(o, __hip_atomic_load(&s_thr[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+  w.thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(o)));
+  const bool have = lane < w.rcount;
+  uint4 r = make_uint4(0, 0, 0, 0);
+  uint32_t id0 = 0;
+  if (have) {
+    r = w.rq[lane];
+    id0 = w.rid[lane];
+  }
+  float v[8];
+  unpack8(r, v);
+  float gm = fmaxf(fmaxf(fmaxf(v[0], v[1]), v[2]), v[3]);
+  gm = fmaxf(fmaxf(fmaxf(gm, v[4]), v[5]), fmaxf(v[6], v[7]));
+  if (K <= kWave && w.rcount >= K) {
+    uint32_t key[1] = {have ? ordered_f32(gm) : 0u};
+    wave_sort_desc_u32<1>(key);
+    const float tau = unordered_f32(__builtin_amdgcn_readlane(key[0], K - 1));
+    if (tau > w.thr) w.thr = tau;
+  }
+  const bool live = have && gm >= w.thr;
+  if (__ballot(live) != 0ull) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) wave_offer<CAP>(w, K, v[e], id0 + e, live);
+  }
+  w.rcount = 0;
+}
+
 // Empties the wave's ring of deferred groups into its candidate buffer.
 template <int CAP>
 __device__ __forceinline__ void wave_flush(WaveBuf<CAP> &w, int K) {
@@ -454,6 +491,83 @@ __device__ __forceinline__ void write_row(const RowOut &o, int64_t row, int K, d
   }
 }
 
+// Sorts the first n <= 64*E keys of buf (LDS) and writes the best K back to
+// the front.
+template <int E>
+__device__ __forceinline__ void sort_front(uint64_t *buf, int n, int K) {
+  const int lane = lane_id();
+  uint64_t k[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kWave + lane;
+    k[e] = i < n ? buf[i] : 0ull;
+  }
+  wave_sort_desc<E>(k);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kWave + lane;
+    if (i < K) buf[i] = k[e];
+  }
+}
+template <int E>
+__device__ __noinline__ void sort_front_ool(uint64_t *buf, int n, int K) {
+  sort_front<E>(buf, n, K);
+}
+
+// Moves the keys of buf[from, n) that are larger than `above` to buf[to, ...)
+// in order (to <= from: nothing is overwritten before it is read) and returns
+// the new end.
+__device__ __forceinline__ int keep_above(uint64_t *buf, int from, int n, int to,
+                                          uint64_t above) {
+  const int lane = lane_id();
+  for (int j0 = from; j0 < n; j0 += kWave) {
+    const int j = j0 + lane;
+    const uint64_t key = j < n ? buf[j] : 0ull;
+    const bool keep = j < n && key > above;
+    const uint64_t b = __ballot(keep);
+    if (keep) buf[to + lanes_below(b)] = key;
+    to += __popcll(b);
+  }
+  return to;
+}
+
+// Top K of the block (wave 0).  Each wave's buffer holds keys at or above that
+// wave's threshold, and the largest threshold is a lower bound of the block's
+// K-th value: keys below it are dropped while the buffers are packed to the
+// front of buf (a key never moves past an entry not yet read).  More than 256
+// survivors are cut down by sorting the first 256 and keeping only keys above
+// the K-th of those, which removes at least 256 - K keys per pass.  On return
+// buf[0..K) holds the block's top K in descending key order, 0 past the last
+// candidate.
+template <int CAP>
+__device__ __forceinline__ void block_merge(uint64_t *buf, const int *cnt, const float *thr,
+                                            int K) {
+  const int lane = lane_id();
+  float th = thr[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) th = fmaxf(th, thr[i]);
+  int m = 0;
+  for (int wv = 0; wv < kWaves; ++wv) {
+    const int c = cnt[wv];
+    for (int j0 = 0; j0 < c; j0 += kWave) {
+      const int j = j0 + lane;
+      const uint64_t key = j < c ? buf[wv * CAP + j] : 0ull;
+      const bool keep = key != 0ull && cand_value(key) >= th;
+      const uint64_t b = __ballot(keep);
+      if (keep) buf[m + lanes_below(b)] = key;
+      m += __popcll(b);
+    }
+  }
+  while (m > 4 * kWave) {
+    sort_front_ool<4>(buf, 4 * kWave, K);
+    m = keep_above(buf, 4 * kWave, m, K, buf[K - 1]);
+  }
+  if (m <= kWave) sort_front<1>(buf, m, K);
+  else if (m <= 2 * kWave) sort_front<2>(buf, m, K);
+  else sort_front_ool<4>(buf, m, K);
+  for (int i = m + lane; i < K; i += kWave) buf[i] = 0ull;
+}
+
 template <int CAP>
 __global__ void __launch_bounds__(kThreads, 4)
 logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, int K,
@@ -598,49 +712,26 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
     }
   }
 
-  if (w.rcount > 0) wave_flush<CAP>(w, K);
-  wave_compact<CAP>(w, K);
+  // Every wave's buffer stays unsorted: after one barrier wave 0 selects the
+  // block's top K from all four at once.
+  if (w.rcount > 0) wave_flush_last<CAP>(w, K, s_thr);
   stats_wave_reduce(st);
+  __shared__ int s_cnt[kWaves];
   if (lane == 0) {
     s_stats[wave][0] = static_cast<double>(st.mL);
     s_stats[wave][1] = st.S;
     s_stats[wave][2] = st.T2;
+    s_cnt[wave] = w.count;
+    __hip_atomic_store(&s_thr[wave], w.thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
-  // clear the unused tail of each wave's top-K list
-  for (int i = w.count + lane; i < K; i += kWave) s_buf[wave][i] = 0ull;
   __syncthreads();
 
   if (wave != 0) return;
 
-  // Block merge in wave 0: statistics and the 4 waves' top-K lists.
+  // Block merge in wave 0: statistics and the candidates of the four waves.
   double mL = s_stats[0][0], S = s_stats[0][1], T2 = s_stats[0][2];
   for (int i = 1; i < kWaves; ++i) stats_merge(mL, S, T2, s_stats[i][0], s_stats[i][1], s_stats[i][2]);
-  // key i = wave * K + rank of the waves' lists (no division: at most 3 steps)
-  auto merged_key = [&](int i) -> uint64_t {
-    if (i >= kWaves * K) return 0ull;
-    int wv = 0, r = i;
-    while (r >= K) {
-      r -= K;
-      ++wv;
-    }
-    return s_buf[wv][r];
-  };
-  if (kWaves * K <= kWave) {
-    uint64_t k[1] = {merged_key(lane)};
-    wave_sort_desc<1>(k);
-    if (lane < K) s_buf[0][lane] = k[0];
-  } else {
-    constexpr int E = CAP / kWave;
-    uint64_t k[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) k[e] = merged_key(e * kWave + lane);
-    wave_sort_desc<E>(k);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int i = e * kWave + lane;
-      if (i < K) s_buf[0][i] = k[e];
-    }
-  }
+  block_merge<CAP>(&s_buf[0][0], s_cnt, s_thr, K);
 
   if (splits == 1) {
     write_row<CAP>(out, row, K, mL, S, T2, s_buf[0]);
