@@ -110,12 +110,15 @@ typedef struct {
 } graft_scorer_desc;
 
 /* SABA, eqs. saba-objective/gain/cost (host memory; copied into the context):
- *   tau = max(phi[0] + phi[1] conf + phi[2] ent + phi[3] hist, tau_min)
+ *   tau = max(phi[0] + phi[1] conf + phi[2] feat + phi[3] hist, tau_min)
  *   U(B) = (1 - exp(-B / tau)) / (c0 + c1 B + c2 B prefix)
  *   B_t = the smallest budget of the grid with the largest U.
- * conf = mean over depths of the top-1 probability, ent = mean per-depth
- * entropy (standing in for the representation-degeneration signal, which
- * needs drafter hidden states), hist = mean accepted length over the window. */
+ * conf = mean over depths of the top-1 probability; hist = mean accepted
+ * length over the window.  feat is the representation-degeneration signal of
+ * the decoding state when the round passes the drafter's hidden states,
+ *   degen = (1/(L-1)) sum_{d=1..L-1} r_d + (r_{L-1} - r_1),
+ *   r_d = cos(h_d, h_{d+1}) (0 if either state is zero; degen = 0 if L = 1),
+ * and otherwise the mean per-depth entropy of q, which stands in for it. */
 typedef struct {
     const int32_t *budgets;  /* (host) strictly ascending, each in 1..max_nodes */
     int32_t n_budgets;       /* 1..64 */
@@ -134,6 +137,10 @@ typedef struct {
     const int32_t *prefix_len;   /* [batch] prefix_t of eq. saba-cost, or NULL (0) */
     const float *hist;           /* [batch] hist_t, or NULL: mean of the context's ring */
     const int32_t *fixed_budget; /* [batch] fixed budgets (DDTree-style), or NULL: SABA */
+    const uint16_t *hidden;      /* [batch, L, hidden_dim] bf16 bit patterns of the drafter's
+                                    hidden state at each draft position, contiguous, 16-byte
+                                    aligned base; or NULL (SABA then uses the mean entropy) */
+    int32_t hidden_dim;          /* H: a multiple of 8, 8..1048576 (ignored without hidden) */
 } graft_round_in;
 
 /* Per-round outputs, caller-allocated.  Required: budget, n_nodes, tokens,
@@ -153,7 +160,10 @@ typedef struct {
     float *edge_scores;     /* [batch, L, K, K] [depth-1][parent rank][child rank];
                                depth 1 uses parent row 0 only (others 0) */
     double *node_scores;    /* [batch, max_nodes] path score of each node, 0 padded */
-    float *saba_state;      /* [batch, 4] conf, ent, hist, tau (tau = 0 for fixed budgets) */
+    float *saba_state;      /* [batch, 4] conf, feat (degen with hidden states, else the
+                               mean entropy), hist, tau (tau = 0 for fixed budgets) */
+    float *adj_cos;         /* [batch, L - 1] cosines r_d of adjacent hidden states; written
+                               only when the round passes hidden states */
 } graft_tree_out;
 
 /* Targets of the acceptance walk: exactly one of target_node / target_depth.

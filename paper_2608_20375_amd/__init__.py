@@ -52,7 +52,7 @@ class SabaDesc(C.Structure):
 class RoundIn(C.Structure):
     _fields_ = [("batch", C.c_int32), ("logits", C.c_void_p), ("root_token", C.c_void_p),
                 ("base_pos", C.c_void_p), ("prefix_len", C.c_void_p), ("hist", C.c_void_p),
-                ("fixed_budget", C.c_void_p)]
+                ("fixed_budget", C.c_void_p), ("hidden", C.c_void_p), ("hidden_dim", C.c_int32)]
 
 
 class TreeOut(C.Structure):
@@ -61,7 +61,7 @@ class TreeOut(C.Structure):
                 ("topk_ids", C.c_void_p), ("topk_logq", C.c_void_p), ("row_lse", C.c_void_p),
                 ("row_maxprob", C.c_void_p), ("row_entropy", C.c_void_p),
                 ("edge_scores", C.c_void_p), ("node_scores", C.c_void_p),
-                ("saba_state", C.c_void_p)]
+                ("saba_state", C.c_void_p), ("adj_cos", C.c_void_p)]
 
 
 class Targets(C.Structure):
@@ -131,7 +131,7 @@ class TreeBuffers:
     """Preallocated outputs of one build_tree call (torch tensors on the device)."""
 
     def __init__(self, ctx: "Context", batch: int, mask=True, topk=True, stats=True, edges=False,
-                 node_scores=True, saba_state=True, device=None):
+                 node_scores=True, saba_state=True, adj_cos=False, device=None):
         d = ctx.dims
         dev = device or torch.device("cuda", torch.cuda.current_device())
         L, K, N = d.num_pos, d.top_k, d.max_nodes
@@ -155,6 +155,8 @@ class TreeBuffers:
         self.node_scores = (torch.empty(batch, N, dtype=torch.float64, device=dev)
                             if node_scores else None)
         self.saba_state = torch.empty(batch, 4, **f32) if saba_state else None
+        # cosines of adjacent hidden states (written only when build_tree gets them)
+        self.adj_cos = torch.zeros(batch, max(L - 1, 1), **f32) if adj_cos else None
         t = TreeOut()
         for name, _ in TreeOut._fields_:
             setattr(t, name, _ptr(getattr(self, name), name=name))
@@ -206,16 +208,22 @@ class Context:
                                        _stream()), "graft_set_history")
 
     def build_tree(self, logits, root_token, base_pos, prefix_len=None, hist=None,
-                   fixed_budget=None, out: TreeBuffers | None = None, **want) -> TreeBuffers:
+                   fixed_budget=None, hidden=None, out: TreeBuffers | None = None,
+                   **want) -> TreeBuffers:
+        """hidden: optional [batch, L, H] bf16 bit patterns of the drafter's hidden
+        states; with them the SABA state uses the degeneration signal."""
         batch = logits.shape[0]
         if out is None:
             out = TreeBuffers(self, batch, **want)
+        if logits.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+            raise TypeError("logits must hold bf16 bit patterns")
+        if hidden is not None and hidden.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+            raise TypeError("hidden must hold bf16 bit patterns")
         r = RoundIn(batch, _ptr(logits, None, "logits"), _ptr(root_token, torch.int32, "root_token"),
                     _ptr(base_pos, torch.int32, "base_pos"),
                     _ptr(prefix_len, torch.int32, "prefix_len"), _ptr(hist, torch.float32, "hist"),
-                    _ptr(fixed_budget, torch.int32, "fixed_budget"))
-        if logits.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
-            raise TypeError("logits must hold bf16 bit patterns")
+                    _ptr(fixed_budget, torch.int32, "fixed_budget"), _ptr(hidden, None, "hidden"),
+                    0 if hidden is None else int(hidden.shape[-1]))
         _check(lib().graft_build_tree(self._h, C.byref(r), C.byref(out._struct), _stream()),
                "graft_build_tree")
         return out

@@ -55,6 +55,7 @@ void free_ctx(graft_ctx *c) {
   (void)hipFree(c->sorted_child);
   (void)hipFree(c->id_rank);
   (void)hipFree(c->positive);
+  (void)hipFree(c->adj_cos);
   (void)hipFree(c->proj_parent);
   (void)hipFree(c->proj_child);
   (void)hipFree(c->depth_emb);
@@ -122,6 +123,7 @@ int graft_create(const graft_dims *dims, graft_ctx **out) {
   GRAFT_ALLOC(c->sorted_child, B * L * K * K);
   GRAFT_ALLOC(c->id_rank, B * L * K);
   GRAFT_ALLOC(c->positive, B * L);
+  GRAFT_ALLOC(c->adj_cos, B * (L > 1 ? L - 1 : 1));
   GRAFT_ALLOC(c->hist_ring, B * d.hist_window);
   GRAFT_ALLOC(c->hist_pos, B);
   GRAFT_ALLOC(c->error_flag, 1);
@@ -250,6 +252,14 @@ int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_
   if (!in->fixed_budget && !ctx->has_saba)
     return fail(GRAFT_ERR_INVALID_ARG,
                 "graft_build_tree: no fixed budgets and no SABA parameters (graft_set_saba)");
+  if (in->hidden) {
+    if (in->hidden_dim < 8 || in->hidden_dim > (1 << 20) || (in->hidden_dim & 7) != 0)
+      return fail(GRAFT_ERR_INVALID_ARG,
+                  "graft_build_tree: hidden_dim %d must be a multiple of 8 in 8..1048576",
+                  in->hidden_dim);
+    if ((reinterpret_cast<uintptr_t>(in->hidden) & 15u) != 0)
+      return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: hidden must be 16-byte aligned");
+  }
   if (!in->hist && !in->fixed_budget && !ctx->has_history)
     return fail(GRAFT_ERR_INVALID_ARG,
                 "graft_build_tree: no hist input and no history ring (graft_set_history)");
@@ -260,6 +270,10 @@ int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_
   hipError_t e = graft::launch_logits_pass(ctx, in->batch, in->logits, out, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: logits pass");
   if (ev) (void)hipEventRecord(ev[1], s);
+  if (in->hidden) {
+    e = graft::launch_degen(ctx, in->batch, in->hidden, in->hidden_dim, out->adj_cos, s);
+    if (e != hipSuccess) return hip_fail(e, "graft_build_tree: hidden-state cosines");
+  }
   e = graft::launch_edge_scores(ctx, in, out, s);
   if (e != hipSuccess) return hip_fail(e, "graft_build_tree: edge scores and budget");
   if (ev) (void)hipEventRecord(ev[2], s);

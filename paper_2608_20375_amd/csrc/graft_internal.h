@@ -229,6 +229,7 @@ struct graft_ctx {
   uint8_t *sorted_child;   // [max_batch, L, K, K]
   uint8_t *id_rank;        // [max_batch, L, K] rank of each candidate's token id in its depth
   uint8_t *positive;       // [max_batch, L] 1 if some edge score of that depth is > 0
+  float *adj_cos;          // [max_batch, max(L - 1, 1)] adjacent hidden-state cosines
   // scorer
   float *proj_parent;      // [V, m]
   float *proj_child;       // [V, m]
@@ -255,6 +256,8 @@ namespace graft {
 hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
                               const graft_tree_out *out, hipStream_t stream);
 hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStream_t stream);
+hipError_t launch_degen(graft_ctx *ctx, int batch, const uint16_t *hidden, int hidden_dim,
+                        float *adj_cos_out, hipStream_t stream);
 hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
                               hipStream_t stream);
 hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,

@@ -68,22 +68,27 @@ struct SabaArgs {
   const int32_t *hist_ring;     // [B, window]
   const int32_t *prefix_len;    // [B] or nullptr (0)
   const int32_t *fixed_budget;  // [B]: budgets given by the caller, or nullptr: SABA
+  const float *adj_cos;         // [B, L - 1] adjacent hidden-state cosines, or nullptr
   int window;
   int32_t *budget;              // [B] out
-  float *saba_state;            // [B, 4] out (conf, ent, hist, tau) or nullptr
+  float *saba_state;            // [B, 4] out (conf, ent or degen, hist, tau) or nullptr
 };
 
-// B_t of sequence b by one wave: conf and ent are the means of the rows'
-// top-1 probability and entropy, hist the caller's value or the ring's mean;
-// tau = max(phi . [1, conf, ent, hist], tau_min); U(B) = (1 - exp(-B/tau)) /
-// (c0 + c1 B + c2 B prefix) (eqs. saba-gain, saba-cost) for every grid budget,
-// one lane each in fp64; B_t = the smallest budget with the largest U
-// (eq. saba-objective).
+// B_t of sequence b by one wave: conf is the mean of the rows' top-1
+// probability; the second feature is degen = mean_d r_d + (r_{L-1} - r_1)
+// over the adjacent hidden-state cosines when they are given, else the mean
+// row entropy standing in for it; hist is the caller's value or the ring's
+// mean; tau = max(phi . [1, conf, feature, hist], tau_min); U(B) = (1 -
+// exp(-B/tau)) / (c0 + c1 B + c2 B prefix) (eqs. saba-gain, saba-cost) for
+// every grid budget, one lane each in fp64; B_t = the smallest budget with the
+// largest U (eq. saba-objective).
 __device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int L) {
   const int lane = lane_id();
   // every global load first
   const float *rs = a.row_stats + (static_cast<int64_t>(b) * L + (lane < L ? lane : 0)) * 3;
   const float f_conf = rs[1], f_ent = rs[2];
+  const int np = L - 1;
+  const float f_r = (a.adj_cos && lane < np) ? a.adj_cos[static_cast<int64_t>(b) * np + lane] : 0.f;
   const float f_hist = a.hist ? a.hist[b] : 0.f;
   const int32_t ring =
       (!a.hist && lane < a.window) ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
@@ -109,6 +114,15 @@ __device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int 
   }
   conf /= static_cast<double>(L);
   ent /= static_cast<double>(L);
+  if (a.adj_cos) {
+    // degen from the cosines r_1 .. r_{L-1} (lanes 0 .. L-2); 0 without a pair
+    double r = lane < np ? static_cast<double>(f_r) : 0.0;
+    const double r_first = static_cast<double>(__shfl(f_r, 0));
+    const double r_last = static_cast<double>(__shfl(f_r, np > 0 ? np - 1 : 0));
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) r += xor_lane_f64(r, o);
+    ent = np > 0 ? r / static_cast<double>(np) + (r_last - r_first) : 0.0;
+  }
   double tau = 0.0;
   int budget;
   if (!a.fixed_budget) {
@@ -351,6 +365,7 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const gr
   sa.hist_ring = ctx->hist_ring;
   sa.prefix_len = in->prefix_len;
   sa.fixed_budget = in->fixed_budget;
+  sa.adj_cos = in->hidden ? ctx->adj_cos : nullptr;
   sa.window = d.hist_window;
   sa.budget = out->budget;
   sa.saba_state = out->saba_state;

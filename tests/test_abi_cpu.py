@@ -67,7 +67,8 @@ int main(void) {
   P(graft_scorer_desc, scale); P(graft_scorer_desc, center);
   P(graft_saba_desc, phi); P(graft_saba_desc, c2);
   P(graft_round_in, logits); P(graft_round_in, fixed_budget);
-  P(graft_tree_out, mask); P(graft_tree_out, saba_state);
+  P(graft_round_in, hidden); P(graft_round_in, hidden_dim);
+  P(graft_tree_out, mask); P(graft_tree_out, saba_state); P(graft_tree_out, adj_cos);
   P(graft_targets, target_depth);
   return 0;
 }

@@ -33,15 +33,23 @@ def saba_inputs(w):
     return sp
 
 
-def audited_round(w, rnd=0, mode="literal", seqs=None, with_targets=True):
+def audited_round(w, rnd=0, mode="literal", seqs=None, with_targets=True, hidden_dim=None,
+                  phi=None):
     """Inputs for the whole batch; sequences in `seqs` (default: all) are
     audited with the oracle and re-drawn until their decisions are robust.
+    With hidden_dim, drafter hidden states [batch, L, hidden_dim] are drawn too
+    and the SABA state uses their degeneration signal.  phi overrides the SABA
+    state weights.
     Returns (inputs, scorer, saba, {b: oracle result})."""
     sc = scorer_inputs(w, mode)
     sp = saba_inputs(w)
+    if phi is not None and sp is not None:
+        sp["phi"] = np.asarray(phi, np.float32)
     seqs = list(range(w.batch)) if seqs is None else list(seqs)
     attempts = np.zeros(w.batch, np.int64)
     inp = S.gen_round(w, rnd, attempts, with_targets=with_targets)
+    if hidden_dim:
+        inp["hidden"] = S.gen_hidden(w, rnd, hidden_dim, attempts)
     P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
     results = {}
     for b in seqs:
@@ -52,10 +60,13 @@ def audited_round(w, rnd=0, mode="literal", seqs=None, with_targets=True):
                 for k, v in one.items():
                     if isinstance(v, np.ndarray) and v.shape and v.shape[0] == w.batch:
                         inp[k][b] = v[b]
+                if hidden_dim:
+                    inp["hidden"][b] = S.gen_hidden(w, rnd, hidden_dim, attempts, seqs=[b])[b]
             r = oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b],
                                       inp["base_pos"][b], inp["prefix_len"][b],
                                       inp["fixed_budget"][b] if "fixed_budget" in inp else 0,
-                                      float(inp["hist"][b]))
+                                      float(inp["hist"][b]),
+                                      inp["hidden"][b] if hidden_dim else None)
             if oracle.sequence_ok(r, w.L):
                 break
         else:
@@ -85,7 +96,8 @@ def gpu_round(ctx, w, inp, torch, dev="cuda", use_ring=False, edges=True):
                          prefix_len=T(inp["prefix_len"]),
                          hist=None if use_ring else T(inp["hist"]),
                          fixed_budget=T(inp["fixed_budget"]) if "fixed_budget" in inp else None,
-                         edges=edges)
+                         hidden=T(inp["hidden"].view(np.int16)) if "hidden" in inp else None,
+                         edges=edges, adj_cos="hidden" in inp)
     torch.cuda.synchronize()
     res = {k: v.cpu().numpy() for k, v in out.as_dict().items()}
     res["_out"] = out
