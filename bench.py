@@ -11,9 +11,11 @@ cannot serve a round's reads from the previous round.
 
 Prints one JSON line: rounds/s and us/round of K rounds timed back to back;
 the logits pass against the HBM roofline, its duration from HIP events
-recorded around every stage while the same K rounds run a second time (the
-events themselves add a few microseconds per round, so they stay out of the
-headline figure); and the CPU oracle timed on a bounded sample on this host.
+recorded around every stage while the same K rounds run a second time (each
+event adds the same few microseconds of stream time: that cost, measured as
+the difference between the two passes per event, is subtracted from every
+stage, and the events stay out of the headline figure); and the CPU oracle
+timed on a bounded sample on this host.
 """
 from __future__ import annotations
 
@@ -96,6 +98,9 @@ def main():
     ap.add_argument("--rotate", type=int, default=0, help="logit buffers (0: >= 1 GiB total)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hidden-dim", type=int, default=0,
+                    help="also pass drafter hidden states of this width (SABA uses their "
+                         "degeneration signal); 0: the mean-entropy state of the workload")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
     args = ap.parse_args()
@@ -141,6 +146,9 @@ def main():
     if node_mode:
         ctx.set_history(T(inp["hist_ring"]))
     tdepth = T(inp["target_depth"]) if not node_mode else None
+    hidden = None
+    if args.hidden_dim:
+        hidden = T(S.gen_hidden(w, 0, args.hidden_dim).view(np.int16))
     tb = G.TreeBuffers(ctx, w.batch)
     acc_len = torch.empty(w.batch, dtype=torch.int32, device=dev)
     acc_nodes = torch.empty(w.batch, w.L, dtype=torch.int32, device=dev)
@@ -151,7 +159,7 @@ def main():
 
     def one_round(i):
         ctx.build_tree(bufs[i % R], root, base_pos, prefix_len=prefix, hist=hist,
-                       fixed_budget=fixed, out=tb)
+                       fixed_budget=fixed, hidden=hidden, out=tb)
         if node_mode:
             ctx.synth_node_targets(w.seed + i, root, tb.n_nodes, tb.tokens, tb.parents,
                                    tb.topk_ids, troot, tnode)
@@ -195,7 +203,16 @@ def main():
     log("with stage events: %.4f ms/round; stages ms %s" %
         (ms_events, ["%.4f" % x for x in stage_avg]))
 
-    k1_s = stage_avg[0] * 1e-3
+    # Every recorded event adds the same stream time (a marker packet), and a
+    # stage's interval holds exactly one of them: take that per-event cost from
+    # the two timed passes (with and without events; 4 events per
+    # graft_build_tree, 2 per graft_accept) and subtract it from every stage.
+    events_per_round = 6
+    event_ms = max(0.0, (ms_events - ms_per_step) / events_per_round)
+    stage_net = [max(0.0, x - event_ms) for x in stage_avg]
+    log("per-event stream cost %.4f ms; stages net of it %s" %
+        (event_ms, ["%.4f" % x for x in stage_net]))
+    k1_s = stage_net[0] * 1e-3
     achieved = logit_bytes / k1_s / 1e9 if k1_s > 0 else 0.0
     traffic = stored_traffic(args.workload)
 
@@ -239,10 +256,13 @@ def main():
                             if w.budget_mode == "saba" else "fixed budget %d" % w.fixed_budget,
                             w.n_max, w.emb_dim, w.rank, "per-node" if node_mode else "per-depth", R),
             "global_batch": w.batch,
+            "hidden_dim": args.hidden_dim,
             "mean_budget": budgets,
             "mean_nodes": nodes,
-            "stage_us": {"logits_pass": 1e3 * stage_avg[0], "edge_scores_and_saba": 1e3 * stage_avg[1],
-                         "select_emit_mask": 1e3 * stage_avg[2], "accept": 1e3 * stage_avg[3]},
+            "stage_us": {"logits_pass": 1e3 * stage_net[0], "edge_scores_and_saba": 1e3 * stage_net[1],
+                         "select_emit_mask": 1e3 * stage_net[2], "accept": 1e3 * stage_net[3]},
+            "stage_us_raw_events": [1e3 * x for x in stage_avg],
+            "event_overhead_us": 1e3 * event_ms,
         },
         "roofline": {
             "bound": "hbm",

@@ -231,9 +231,10 @@ GRAFT_API int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t s
 
 /* Stage timing for benchmarks.  graft_profile_begin arms timing of the next
  * max_calls calls of graft_build_tree and of graft_accept (each counted
- * separately): HIP events are recorded on the call's stream around every
- * stage, 0 = logits pass, 1 = edge scoring and the SABA budget, 2 = selection,
- * emission and mask, 3 = acceptance.  graft_profile_end synchronizes the events, writes
+ * separately): timing-only HIP events (no system-scope fence) are recorded on
+ * the call's stream around every stage, 0 = logits pass, 1 = hidden-state
+ * cosines, edge scoring and the SABA budget, 2 = selection, emission and mask,
+ * 3 = acceptance.  graft_profile_end synchronizes the events, writes
  * the summed milliseconds stage_ms[4] and the number of timed launches
  * stage_calls[4] (host arrays), and disarms.  Not for concurrent use. */
 GRAFT_API int graft_profile_begin(graft_ctx *ctx, int32_t max_calls);

@@ -343,8 +343,12 @@ int graft_profile_begin(graft_ctx *ctx, int32_t max_calls) {
   ctx->prof_cap = 0;
   for (int i = 0; i < max_calls; ++i) {
     hipError_t e = hipSuccess;
-    for (int j = 0; j < 4 && e == hipSuccess; ++j) e = hipEventCreate(&ctx->prof_build[4 * i + j]);
-    for (int j = 0; j < 2 && e == hipSuccess; ++j) e = hipEventCreate(&ctx->prof_acc[2 * i + j]);
+    // timing-only events: no system-scope fence (cache writeback and
+    // invalidation) when they are recorded, which would add to the stages
+    for (int j = 0; j < 4 && e == hipSuccess; ++j)
+      e = hipEventCreateWithFlags(&ctx->prof_build[4 * i + j], hipEventDisableSystemFence);
+    for (int j = 0; j < 2 && e == hipSuccess; ++j)
+      e = hipEventCreateWithFlags(&ctx->prof_acc[2 * i + j], hipEventDisableSystemFence);
     if (e != hipSuccess) {
       prof_release(ctx);
       return hip_fail(e, "graft_profile_begin: hipEventCreate");
