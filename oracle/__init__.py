@@ -97,6 +97,12 @@ def lib():
             L.oracle_accept.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
             L.oracle_accept.restype = C.c_int32
+            L.oracle_mask_to_bias.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_int32,
+                                              C.c_void_p]
+            L.oracle_mask_to_bias.restype = None
+            L.oracle_gather_rows.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_int64,
+                                             C.c_void_p, C.c_int64, C.c_int64]
+            L.oracle_gather_rows.restype = C.c_int
             _lib = L
     return _lib
 
@@ -264,6 +270,31 @@ def accept(n_nodes: int, tokens, parents, L: int, target_root: int = -1, target_
     a = lib().oracle_accept(int(n_nodes), _p(tokens), _p(parents), int(L), int(target_root),
                             _p(tn), _p(td), _p(acc), _p(bonus))
     return int(a), acc[:L].copy(), int(bonus[0])
+
+
+def mask_to_bias(n_nodes: int, mask: np.ndarray) -> np.ndarray:
+    """V1: [n_max, n_max] additive bias (0 / -inf, fp64) from mask [n_max, words]."""
+    mask = _c(mask, np.uint64)
+    n_max, words = mask.shape
+    out = np.empty((n_max, n_max), np.float64)
+    lib().oracle_mask_to_bias(int(n_nodes), int(n_max), _p(mask), int(words), _p(out))
+    return out
+
+
+def gather_rows(acc_len: int, acc_nodes, src: np.ndarray, dst: np.ndarray) -> np.ndarray:
+    """V2: dst[i] = src[acc_nodes[i]] for i < acc_len (rows of bytes); dst is
+    modified in place and returned.  src may be dst."""
+    nodes = _c(acc_nodes, np.int32)
+    assert src.flags.c_contiguous and dst.flags.c_contiguous and src.dtype == dst.dtype
+    row_bytes = src.strides[0]
+    assert dst.strides[0] == row_bytes
+    if acc_len > 0:
+        assert nodes.max(initial=-1) < src.shape[0] and acc_len <= dst.shape[0]
+    rc = lib().oracle_gather_rows(int(acc_len), _p(nodes), src.ctypes.data, row_bytes,
+                                  dst.ctypes.data, row_bytes, row_bytes)
+    if rc:
+        raise MemoryError("oracle_gather_rows")
+    return dst
 
 
 # ---------------------------------------------------------------------------

@@ -25,6 +25,11 @@
  *       ancestor tree-attention mask (Preliminaries, tree-based speculative
  *       decoding)
  *   O8  greedy acceptance: longest accepted root path (same paragraph)
+ *   V1  the verifier's additive attention bias of the draft block, expanded
+ *       from the ancestor mask (Preliminaries, tree attention)
+ *   V2  commit of the accepted path in the verifier's key/value rows: the
+ *       rows of the accepted nodes moved to consecutive positions (same
+ *       paragraph: the longest accepted path is committed)
  *
  * Readings where the paper is silent (all mirrored by the HIP library):
  *   - the budget counts draft nodes only; the root (last committed token) is
@@ -558,4 +563,45 @@ ORACLE_EXPORT int32_t oracle_accept(int32_t n_nodes, const int32_t *tokens,
         ++depth;
     }
     return a;
+}
+
+/* ------------------------------------------------------------------------- */
+/* V1: additive attention bias of the draft block.  Node i may attend to node */
+/* j iff j is i or an ancestor of i (bit j of mask row i): bias 0, else -inf. */
+/* Entries of padding rows or columns (i or j >= n) are -inf.  bias is        */
+/* [n_max, n_max] doubles, row-major.                                          */
+/* ------------------------------------------------------------------------- */
+ORACLE_EXPORT void oracle_mask_to_bias(int32_t n, int32_t n_max, const uint64_t *mask,
+                                       int32_t words, double *bias)
+{
+    for (int32_t i = 0; i < n_max; ++i)
+        for (int32_t j = 0; j < n_max; ++j) {
+            int visible = 0;
+            if (i < n && j < n)
+                visible = (int)((mask[(size_t)i * (size_t)words + (size_t)(j / 64)] >> (j % 64)) & 1u);
+            bias[(size_t)i * (size_t)n_max + (size_t)j] = visible ? 0.0 : -INFINITY;
+        }
+}
+
+/* ------------------------------------------------------------------------- */
+/* V2: the accepted path's rows.  Destination row i (i < acc_len) receives    */
+/* the row_bytes bytes of source row acc_nodes[i]; other rows are untouched.  */
+/* Rows are read before any is written, so src and dst may be the same       */
+/* buffer with the same stride (the accepted nodes then move down in place).  */
+/* ------------------------------------------------------------------------- */
+ORACLE_EXPORT int oracle_gather_rows(int32_t acc_len, const int32_t *acc_nodes,
+                                     const uint8_t *src, int64_t src_row_stride, uint8_t *dst,
+                                     int64_t dst_row_stride, int64_t row_bytes)
+{
+    if (acc_len <= 0) return 0;
+    uint8_t *tmp = (uint8_t *)malloc((size_t)acc_len * (size_t)row_bytes);
+    if (!tmp) return 1;
+    for (int32_t i = 0; i < acc_len; ++i)
+        memcpy(tmp + (size_t)i * (size_t)row_bytes,
+               src + (size_t)acc_nodes[i] * (size_t)src_row_stride, (size_t)row_bytes);
+    for (int32_t i = 0; i < acc_len; ++i)
+        memcpy(dst + (size_t)i * (size_t)dst_row_stride, tmp + (size_t)i * (size_t)row_bytes,
+               (size_t)row_bytes);
+    free(tmp);
+    return 0;
 }
