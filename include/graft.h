@@ -210,6 +210,45 @@ GRAFT_API int graft_accept(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes
                  int32_t *acc_len, int32_t *acc_nodes, int32_t *bonus,
                  int32_t update_history, graft_stream_t stream);
 
+/* Verifier-side consumers of a round: the draft tree goes to the target model
+ * under a tree-attention mask, and the longest accepted path is committed
+ * (the paper's Preliminaries, tree-based speculative decoding). */
+
+/* Expands the ancestor masks written by graft_build_tree into the additive
+ * attention bias of the draft block: entry (i, j) of sequence b is 0 when i and
+ * j are below n_nodes[b] and node j is node i or an ancestor of it, and -inf
+ * otherwise (padding rows and columns included).  Entry (b, i, j), j <
+ * max_nodes, is bias[b * batch_stride + i * ld + j]; dtype 0 writes fp32, 1 bf16
+ * bit patterns.  bias is 16-byte aligned; ld >= max_nodes and batch_stride >=
+ * max_nodes * ld are multiples of 4 (fp32) or 8 (bf16) elements.  Passing a
+ * column offset into a wider [batch, max_nodes, prefix + max_nodes] bias, with
+ * its full row stride as ld, fills that slice only.
+ *   n_nodes [batch]; mask [batch, max_nodes, ceil(max_nodes/64)]. */
+GRAFT_API int graft_mask_to_bias(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes,
+                                 const uint64_t *mask, void *bias, int32_t dtype, int64_t ld,
+                                 int64_t batch_stride, graft_stream_t stream);
+
+/* Commits the accepted path in the verifier's key/value rows: for i <
+ * acc_len[b], destination row i of sequence b receives the row_bytes bytes of
+ * row acc_nodes[b, i] (acc_len and acc_nodes [batch, L] as written by
+ * graft_accept; acc_len is clamped to 0..L); other rows are untouched.
+ * Row r of sequence b in plane p (p < n_planes, e.g. layer x {key, value}) is
+ * at byte offset p * plane_stride + b * batch_stride + r * row_stride from the
+ * source or destination base.  row_bytes, every stride and both bases are
+ * multiples of 16.  Within a plane and sequence every source row is read
+ * before a destination row that could alias it is written, so dst may be src
+ * with the same strides (compaction in place) when the node indices increase
+ * along the path and acc_nodes[b, i] >= i, which graft_accept guarantees;
+ * other overlaps are not supported.  Node indices outside [0, max_nodes) are
+ * skipped and reported by graft_get_device_status. */
+GRAFT_API int graft_commit_accepted(graft_ctx *ctx, int32_t batch, const int32_t *acc_len,
+                                    const int32_t *acc_nodes, const void *src, void *dst,
+                                    int64_t row_bytes, int32_t n_planes,
+                                    int64_t src_plane_stride, int64_t src_batch_stride,
+                                    int64_t src_row_stride, int64_t dst_plane_stride,
+                                    int64_t dst_batch_stride, int64_t dst_row_stride,
+                                    graft_stream_t stream);
+
 /* Synchronizes `stream` and reports data errors the kernels detected since
  * the last call (token ids outside [0, V), for example): GRAFT_OK or
  * GRAFT_ERR_DEVICE_DATA; the flag is then cleared. */

@@ -22,6 +22,7 @@ EXPORTED_SYMBOLS = (
     "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
     "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
     "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
+    "graft_mask_to_bias", "graft_commit_accepted",
 )
 
 
@@ -92,6 +93,10 @@ def lib():
         L.graft_accept.argtypes = [vp, i32, vp, vp, vp, C.POINTER(Targets), vp, vp, vp, i32, vp]
         L.graft_get_device_status.argtypes = [vp, vp]
         L.graft_synth_node_targets.argtypes = [vp, i32, C.c_uint64, vp, vp, vp, vp, vp, vp, vp, vp]
+        i64 = C.c_int64
+        L.graft_mask_to_bias.argtypes = [vp, i32, vp, vp, vp, i32, i64, i64, vp]
+        L.graft_commit_accepted.argtypes = [vp, i32, vp, vp, vp, vp, i64, i32, i64, i64, i64,
+                                            i64, i64, i64, vp]
         L.graft_profile_begin.argtypes = [vp, i32]
         L.graft_profile_end.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
         L.graft_status_string.argtypes = [C.c_int]
@@ -100,7 +105,8 @@ def lib():
         L.graft_last_error.restype = C.c_char_p
         for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
                   "graft_build_tree", "graft_accept", "graft_get_device_status",
-                  "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end"):
+                  "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
+                  "graft_mask_to_bias", "graft_commit_accepted"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -263,6 +269,50 @@ class Context:
             _ptr(topk_ids, torch.int32, "topk_ids"), _ptr(target_root, torch.int32, "target_root"),
             _ptr(target_node, torch.int32, "target_node"), _stream()), "graft_synth_node_targets")
         return target_root, target_node
+
+    def mask_to_bias(self, n_nodes, mask, bias=None, dtype=torch.bfloat16):
+        """Additive attention bias of the draft block (0 / -inf) from the ancestor
+        masks.  bias: [batch, max_nodes, >= max_nodes] tensor or strided view with
+        unit stride along the last dimension (e.g. the tree columns of a wider
+        bias); allocated as [batch, max_nodes, max_nodes] when None."""
+        batch = n_nodes.shape[0]
+        N = self.dims.max_nodes
+        if bias is None:
+            bias = torch.empty(batch, N, N, dtype=dtype, device=n_nodes.device)
+        if bias.dtype not in (torch.float32, torch.bfloat16):
+            raise TypeError("bias must be float32 or bfloat16")
+        if bias.dim() != 3 or bias.shape[0] < batch or bias.shape[1] < N or bias.shape[2] < N:
+            raise ValueError("bias must be at least [batch, max_nodes, max_nodes]")
+        if bias.stride(2) != 1:
+            raise ValueError("bias must have unit stride along its last dimension")
+        _check(lib().graft_mask_to_bias(self._h, batch, _ptr(n_nodes, torch.int32, "n_nodes"),
+                                        _ptr(mask, torch.int64, "mask"), bias.data_ptr(),
+                                        1 if bias.dtype == torch.bfloat16 else 0,
+                                        bias.stride(1), bias.stride(0), _stream()),
+               "graft_mask_to_bias")
+        return bias
+
+    def commit_accepted(self, acc_len, acc_nodes, src, dst=None):
+        """Moves the accepted nodes' rows to rows 0..acc_len-1: src and dst are
+        [planes, batch, rows, width] tensors (any dtype, unit stride along width);
+        dst defaults to src (compaction in place)."""
+        dst = src if dst is None else dst
+        for name, t in (("src", src), ("dst", dst)):
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dim() != 4:
+                raise TypeError("%s must be a 4-d CUDA tensor [planes, batch, rows, width]" % name)
+            if t.stride(3) != 1:
+                raise ValueError("%s must have unit stride along its last dimension" % name)
+        if src.dtype != dst.dtype or src.shape[0] != dst.shape[0] or src.shape[3] != dst.shape[3]:
+            raise ValueError("src and dst must agree in dtype, planes and width")
+        es = src.element_size()
+        batch = acc_len.shape[0]
+        _check(lib().graft_commit_accepted(
+            self._h, batch, _ptr(acc_len, torch.int32, "acc_len"),
+            _ptr(acc_nodes, torch.int32, "acc_nodes"), src.data_ptr(), dst.data_ptr(),
+            src.shape[3] * es, src.shape[0], src.stride(0) * es, src.stride(1) * es,
+            src.stride(2) * es, dst.stride(0) * es, dst.stride(1) * es, dst.stride(2) * es,
+            _stream()), "graft_commit_accepted")
+        return dst
 
     def profile_begin(self, max_calls: int):
         _check(lib().graft_profile_begin(self._h, int(max_calls)), "graft_profile_begin")

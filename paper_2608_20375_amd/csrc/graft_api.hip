@@ -312,6 +312,62 @@ int graft_accept(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes, const in
   return GRAFT_OK;
 }
 
+int graft_mask_to_bias(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes,
+                       const uint64_t *mask, void *bias, int32_t dtype, int64_t ld,
+                       int64_t batch_stride, graft_stream_t stream) {
+  if (!ctx || !n_nodes || !mask || !bias)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_mask_to_bias: NULL argument");
+  if (batch < 1 || batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_mask_to_bias: batch %d outside 1..%d", batch,
+                ctx->dims.max_batch);
+  if (dtype != 0 && dtype != 1)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_mask_to_bias: dtype %d is neither 0 (fp32) nor 1 (bf16)",
+                dtype);
+  const int64_t n_max = ctx->dims.max_nodes, per = dtype == 1 ? 8 : 4;
+  if (ld < n_max || (batch > 1 && batch_stride < n_max * ld))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_mask_to_bias: ld or batch_stride too small");
+  if ((reinterpret_cast<uintptr_t>(bias) & 15u) != 0 || ld % per != 0 || batch_stride % per != 0)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "graft_mask_to_bias: bias must be 16-byte aligned with ld and batch_stride "
+                "multiples of %d elements", static_cast<int>(per));
+  hipError_t e = graft::launch_mask_to_bias(ctx, batch, n_nodes, mask, bias, dtype, ld,
+                                            batch_stride, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graft_mask_to_bias");
+  return GRAFT_OK;
+}
+
+int graft_commit_accepted(graft_ctx *ctx, int32_t batch, const int32_t *acc_len,
+                          const int32_t *acc_nodes, const void *src, void *dst, int64_t row_bytes,
+                          int32_t n_planes, int64_t src_plane_stride, int64_t src_batch_stride,
+                          int64_t src_row_stride, int64_t dst_plane_stride,
+                          int64_t dst_batch_stride, int64_t dst_row_stride,
+                          graft_stream_t stream) {
+  if (!ctx || !acc_len || !acc_nodes || !src || !dst)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_commit_accepted: NULL argument");
+  if (batch < 1 || batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_commit_accepted: batch %d outside 1..%d", batch,
+                ctx->dims.max_batch);
+  if (n_planes < 1 || row_bytes < 16)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_commit_accepted: need n_planes >= 1, row_bytes >= 16");
+  const int64_t v[7] = {row_bytes, src_plane_stride, src_batch_stride, src_row_stride,
+                        dst_plane_stride, dst_batch_stride, dst_row_stride};
+  for (int i = 0; i < 7; ++i)
+    if (v[i] < 0 || v[i] % 16 != 0)
+      return fail(GRAFT_ERR_INVALID_ARG,
+                  "graft_commit_accepted: row_bytes and strides must be non-negative multiples of 16");
+  if (((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15u) != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_commit_accepted: src and dst must be 16-byte aligned");
+  const int64_t chunks = (row_bytes + 4095) / 4096;
+  if (static_cast<int64_t>(n_planes) * batch * chunks >= (int64_t{1} << 31))
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_commit_accepted: too many rows to move in one call");
+  hipError_t e = graft::launch_commit(ctx, batch, acc_len, acc_nodes, src, dst, row_bytes,
+                                      n_planes, src_plane_stride, src_batch_stride,
+                                      src_row_stride, dst_plane_stride, dst_batch_stride,
+                                      dst_row_stride, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graft_commit_accepted");
+  return GRAFT_OK;
+}
+
 int graft_get_device_status(graft_ctx *ctx, graft_stream_t stream) {
   if (!ctx) return fail(GRAFT_ERR_INVALID_ARG, "graft_get_device_status: NULL context");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);

@@ -268,6 +268,13 @@ hipError_t launch_accept(graft_ctx *ctx, int batch, const int32_t *n_nodes,
                          int32_t *bonus, int update_history, hipStream_t stream);
 hipError_t launch_set_history(graft_ctx *ctx, int batch, const int32_t *init,
                               hipStream_t stream);
+hipError_t launch_mask_to_bias(graft_ctx *ctx, int batch, const int32_t *n_nodes,
+                               const uint64_t *mask, void *bias, int dtype, int64_t ld,
+                               int64_t batch_stride, hipStream_t stream);
+hipError_t launch_commit(graft_ctx *ctx, int batch, const int32_t *acc_len,
+                         const int32_t *acc_nodes, const void *src, void *dst, int64_t row_bytes,
+                         int n_planes, int64_t sp, int64_t sb, int64_t sr, int64_t dp,
+                         int64_t db, int64_t dr, hipStream_t stream);
 hipError_t launch_synth_targets(graft_ctx *ctx, int batch, uint64_t seed,
                                 const int32_t *root_token, const int32_t *n_nodes,
                                 const int32_t *tokens, const int32_t *parents,
