@@ -89,6 +89,46 @@ def cpu_baseline(w, inp, sc, sp, seconds: float):
             "seconds": el}
 
 
+def time_verifier(ctx, w, tb, acc_len, acc_nodes, steps, torch, dev):
+    """Per-call time of the verifier-side consumers on the last round's tree
+    and acceptance: the bf16 additive bias of the draft block (written once
+    per call: batch * N_max^2 * 2 bytes, plus the mask read) and the commit of
+    the accepted rows of a key/value cache of 72 planes (36 layers x key and
+    value) of 2 KiB rows (8 heads x 128 dims, bf16): 2 * 72 * sum(acc_len) *
+    2 KiB bytes read and written."""
+    planes, row = 72, 2048
+    kv = torch.empty(planes, w.batch, w.n_max, row, dtype=torch.uint8, device=dev)
+    bias = torch.empty(w.batch, w.n_max, w.n_max, dtype=torch.bfloat16, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        ctx.mask_to_bias(tb.n_nodes, tb.mask, bias=bias)
+        ctx.commit_accepted(acc_len, acc_nodes, kv)
+    torch.cuda.synchronize()
+
+    def timed(call):
+        # a sleep kernel ahead of the batch lets the host enqueue every call
+        # before the GPU reaches them: the events then time GPU work only
+        torch.cuda._sleep(100_000_000)
+        e0.record()
+        for _ in range(steps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        return 1e3 * e0.elapsed_time(e1) / steps
+
+    bias_us = timed(lambda: ctx.mask_to_bias(tb.n_nodes, tb.mask, bias=bias))
+    commit_us = timed(lambda: ctx.commit_accepted(acc_len, acc_nodes, kv))
+    words = (w.n_max + 63) // 64
+    bias_bytes = w.batch * w.n_max * (w.n_max * 2 + words * 8)
+    moved = int(acc_len.sum().item())
+    commit_bytes = 2 * planes * moved * row
+    return {"mask_to_bias_us": bias_us, "bias_bytes": bias_bytes,
+            "bias_gbs": bias_bytes / bias_us / 1e3,
+            "commit_us": commit_us, "commit_bytes": commit_bytes,
+            "commit_gbs": commit_bytes / commit_us / 1e3, "accepted_rows": moved,
+            "kv": "%d planes x batch %d x %d rows x %d bytes" % (planes, w.batch, w.n_max, row)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +141,10 @@ def main():
     ap.add_argument("--hidden-dim", type=int, default=0,
                     help="also pass drafter hidden states of this width (SABA uses their "
                          "degeneration signal); 0: the mean-entropy state of the workload")
+    ap.add_argument("--verifier", action="store_true",
+                    help="also time the verifier-side consumers after the headline: the bf16 "
+                         "attention bias of the draft block and the commit of the accepted "
+                         "rows in a key/value cache of 72 planes of 2 KiB rows")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
     args = ap.parse_args()
@@ -225,6 +269,11 @@ def main():
         torch.cuda.synchronize()
         log("copy calibration: 3 copies of %d bytes" % n)
 
+    verifier = None
+    if args.verifier:
+        verifier = time_verifier(ctx, w, tb, acc_len, acc_nodes, args.steps, torch, dev)
+        log("verifier consumers: %s" % verifier)
+
     nodes = tb.n_nodes.float().mean().item()
     budgets = tb.budget.float().mean().item()
     cpu = None
@@ -276,6 +325,8 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if verifier is not None:
+        result["verifier"] = verifier
     print(json.dumps(result), flush=True)
     ctx.close()
 
