@@ -51,8 +51,7 @@ void free_ctx(graft_ctx *c) {
   (void)hipFree(c->topk_ids);
   (void)hipFree(c->topk_logq);
   (void)hipFree(c->row_stats);
-  (void)hipFree(c->sorted_score);
-  (void)hipFree(c->sorted_child);
+  (void)hipFree(c->edge_rows);
   (void)hipFree(c->id_rank);
   (void)hipFree(c->positive);
   (void)hipFree(c->adj_cos);
@@ -119,8 +118,7 @@ int graft_create(const graft_dims *dims, graft_ctx **out) {
   GRAFT_ALLOC(c->topk_ids, B * L * K);
   GRAFT_ALLOC(c->topk_logq, B * L * K);
   GRAFT_ALLOC(c->row_stats, B * L * 3);
-  GRAFT_ALLOC(c->sorted_score, B * L * K * K);
-  GRAFT_ALLOC(c->sorted_child, B * L * K * K);
+  GRAFT_ALLOC(c->edge_rows, B * L * K * K);
   GRAFT_ALLOC(c->id_rank, B * L * K);
   GRAFT_ALLOC(c->positive, B * L);
   GRAFT_ALLOC(c->adj_cos, B * (L > 1 ? L - 1 : 1));

@@ -225,8 +225,7 @@ struct graft_ctx {
   int32_t *topk_ids;       // [max_batch, L, K]
   float *topk_logq;        // [max_batch, L, K]
   float *row_stats;        // [max_batch, L, 3]: lse, maxprob, entropy
-  float *sorted_score;     // [max_batch, L, K, K] children of each parent by rank
-  uint8_t *sorted_child;   // [max_batch, L, K, K]
+  float *edge_rows;        // [max_batch, L, K, K] edge scores: [depth][parent slot][child slot]
   uint8_t *id_rank;        // [max_batch, L, K] rank of each candidate's token id in its depth
   uint8_t *positive;       // [max_batch, L] 1 if some edge score of that depth is > 0
   float *adj_cos;          // [max_batch, max(L - 1, 1)] adjacent hidden-state cosines

@@ -7,12 +7,15 @@
 //   children and of the parents (the root token at depth 1, else the K
 //   candidates of the previous depth) into LDS, forms every parent-child dot
 //   product (eq. tdes-bitower), centers over the children of each parent when
-//   asked (eq. tdes-center) and adds log q of the child (eq. tdes-score).  It
-//   then ranks the children of every parent by (score desc, token id asc) so
-//   that selection can expand a parent's children lazily in order.
+//   asked (eq. tdes-center) and adds log q of the child (eq. tdes-score).
+//   Row (depth, parent) of the output holds the scores of the K children in
+//   candidate-slot order; selection filters a row against its threshold and
+//   needs no ranking.
 // The K x m x K contraction is at most 64 x 64 x 64 per (sequence, depth):
-// VALU work on LDS-staged rows; there is no dense tile to feed MFMA.  The
-// depth-1 block of each sequence also computes its SABA budget.
+// VALU work, each lane keeping one child's projection in registers and
+// reading the parents' rows from LDS as broadcasts; there is no dense tile to
+// feed MFMA.  The depth-1 block of each sequence also computes its SABA
+// budget.
 #include "graft_internal.h"
 
 namespace graft {
@@ -163,24 +166,6 @@ __device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int 
   }
 }
 
-// Bitonic sort, descending, of the keys of each run of SEG consecutive lanes.
-template <int SEG>
-__device__ __forceinline__ uint64_t seg_sort_desc(uint64_t k) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int size = 2; size <= SEG; size <<= 1) {
-#pragma unroll
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      const uint64_t o = xor_lane_u64(k, stride);
-      const bool lower = (lane & stride) == 0;
-      const bool desc = size == SEG || (lane & size) == 0;
-      const uint64_t mx = k > o ? k : o, mn = k > o ? o : k;
-      k = (lower == desc) ? mx : mn;
-    }
-  }
-  return k;
-}
-
 // Sum over each run of SEG consecutive lanes, in every lane of the run.
 template <int SEG>
 __device__ __forceinline__ float seg_sum(float v) {
@@ -195,16 +180,18 @@ __device__ __forceinline__ float seg_sum(float v) {
 // aligned rows that start on different banks), depth embedding [m], log q [K],
 // token ids [K], their ranks by id [K], clamped child and parent ids [K].
 // The (parent, child) pairs are processed SEG lanes per parent (SEG = K
-// rounded up to a power of two): dot product, centering over the parent's
-// children, score, then a segmented sort ranks the children of the parent.
+// rounded up to a power of two), kRows = 64 / SEG parents at a time: lane c of
+// a run keeps child c's row in registers, reads the parent's row from LDS (one
+// address for the whole run), and forms the dot product, the centering over
+// the parent's children and the score.
 template <int SEG>
 __global__ void __launch_bounds__(kEdgeThreads)
 edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__restrict__ topk_ids,
             const float *__restrict__ topk_logq, const int32_t *__restrict__ root_token,
             const float *__restrict__ P, const float *__restrict__ Q,
             const float *__restrict__ depth_emb, ScorerParams sp,
-            float *__restrict__ sorted_score, uint8_t *__restrict__ sorted_child,
-            uint8_t *__restrict__ id_rank, uint8_t *__restrict__ positive,
+            float *__restrict__ edge_rows, uint8_t *__restrict__ id_rank,
+            uint8_t *__restrict__ positive,
             float *__restrict__ edge_out, uint32_t *__restrict__ error_flag, SabaArgs sa,
             SabaParams sp_saba) {
   extern __shared__ float smem[];
@@ -295,43 +282,51 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   const float fscale = sp.scale / sqrtf(static_cast<float>(m));
   constexpr int kRows = kEdgeThreads / SEG;
   const int c = lane & (SEG - 1);
+  const int cc = c < K ? c : 0;
   const int64_t base = row * K * K;
   bool pos = false;
+  const int m4 = m >> 2;
+  // the child's row, 16 bytes a register group (m % 4 == 0) or a float each
+  float4 cr[kMaxScoreDim / 4];
+  if ((m & 3) == 0) {
+    const float4 *c4 = reinterpret_cast<const float4 *>(s_chd + cc * mp);
+#pragma unroll
+    for (int q = 0; q < kMaxScoreDim / 4; ++q)
+      if (q < m4) cr[q] = c4[q];
+  }
+  const float lq = s_lq[cc];
   for (int p0 = 0; p0 < n_par; p0 += kRows) {
     const int p = p0 + lane / SEG;
     const bool valid = p < n_par && c < K;
-    const int pp = p < n_par ? p : 0, cc = c < K ? c : 0;
-    const float *pv = s_par + pp * mp, *cv = s_chd + cc * mp;
+    const int pp = p < n_par ? p : 0;
+    const float *pv = s_par + pp * mp;
     float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
     if ((m & 3) == 0) {
       const float4 *p4 = reinterpret_cast<const float4 *>(pv);
-      const float4 *c4 = reinterpret_cast<const float4 *>(cv);
-#pragma unroll 4
-      for (int q = 0; q < (m >> 2); ++q) {
-        const float4 x = p4[q], y = c4[q];
-        a0 = __builtin_fmaf(x.x, y.x, a0);
-        a1 = __builtin_fmaf(x.y, y.y, a1);
-        a2 = __builtin_fmaf(x.z, y.z, a2);
-        a3 = __builtin_fmaf(x.w, y.w, a3);
+#pragma unroll
+      for (int q = 0; q < kMaxScoreDim / 4; ++q) {
+        if (q < m4) {
+          const float4 x = p4[q], y = cr[q];
+          a0 = __builtin_fmaf(x.x, y.x, a0);
+          a1 = __builtin_fmaf(x.y, y.y, a1);
+          a2 = __builtin_fmaf(x.z, y.z, a2);
+          a3 = __builtin_fmaf(x.w, y.w, a3);
+        }
       }
     } else {
+      const float *cv = s_chd + cc * mp;
 #pragma unroll 4
       for (int j = 0; j < m; ++j) a0 = __builtin_fmaf(pv[j], cv[j], a0);
     }
     const float f = fscale * ((a0 + a1) + (a2 + a3));
     float mean = 0.f;
     if (sp.center) mean = seg_sum<SEG>(valid ? f : 0.f) / static_cast<float>(K);
-    const float S = (s_lq[cc] + sp.beta * (f - mean)) + 0.0f;   // -0 -> +0 for the key
-    if (valid && edge_out) edge_out[base + p * K + c] = S;
-    pos |= valid && S > 0.f;
-    // key: score, then smaller token id, then the child slot
-    const uint32_t lo = (static_cast<uint32_t>(63 - s_idr[cc]) << 6) | static_cast<uint32_t>(cc);
-    const uint64_t key = valid ? (static_cast<uint64_t>(ordered_f32(S)) << 32) | lo : 0ull;
-    const uint64_t sorted = seg_sort_desc<SEG>(key);
-    if (valid) {   // lane c of the run now holds the child ranked c
-      sorted_score[base + p * K + c] = unordered_f32(static_cast<uint32_t>(sorted >> 32));
-      sorted_child[base + p * K + c] = static_cast<uint8_t>(sorted & 63u);
+    const float S = (lq + sp.beta * (f - mean)) + 0.0f;   // -0 -> +0
+    if (valid) {
+      edge_rows[base + p * K + c] = S;
+      if (edge_out) edge_out[base + p * K + c] = S;
     }
+    pos |= valid && S > 0.f;
   }
   if (edge_out && l == 0)
     for (int i = K + lane; i < K * K; i += kEdgeThreads) edge_out[base + i] = 0.f;
@@ -379,7 +374,7 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const gr
   hipLaunchKernelGGL(edge_kernel<SEG>, grid, block, lds, stream, d.num_pos, K, m,            \
                      static_cast<int64_t>(d.vocab), mdiv4, ctx->topk_ids, ctx->topk_logq,     \
                      root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
-                     ctx->scorer, ctx->sorted_score, ctx->sorted_child, ctx->id_rank,         \
+                     ctx->scorer, ctx->edge_rows, ctx->id_rank,                               \
                      ctx->positive, edge_out, ctx->error_flag, sa, ctx->saba)
   if (K <= 1) GRAFT_EDGE(1);
   else if (K <= 2) GRAFT_EDGE(2);

@@ -15,7 +15,8 @@
 //           histogram of the scores locates the boundary bin, whose few
 //           members are ranked with the full order); let theta be the N-th;
 //           expand every kept prefix not yet expanded, adding only children
-//           whose score reaches theta (a prefix of each parent's ranked row);
+//           whose score reaches theta (a parent's edge row is filtered in
+//           child-slot order; no ranking of the row is needed);
 //           stop when an expansion adds nothing.
 //   A prefix outside the kept set can only gain better competitors, and a
 //   skipped child is worse than theta, which only rises, so the result is the
@@ -23,7 +24,8 @@
 //   append-only: dropped prefixes are marked dead and stay in place (so the
 //   children of a prefix always form one contiguous run), and it is compacted
 //   only when an expansion would not fit.
-//   Otherwise (some positive edge score) one thread runs the heap directly.
+//   Otherwise (some positive edge score) one thread runs the heap directly,
+//   finding a parent's next child in rank order by a scan of its row.
 //
 // Emission: canonical numbering (depth ascending, token path ascending), token
 //   ids, parent indices, position ids base_pos + depth, path scores, and the
@@ -42,8 +44,7 @@ constexpr int kStageRows = 4096;   // L * K * K edges staged in LDS up to this s
 
 struct SelectArgs {
   int L, K, n_max, words;
-  const float *sorted_score;    // [B, L, K, K]
-  const uint8_t *sorted_child;  // [B, L, K, K]
+  const float *edge_rows;       // [B, L, K, K] edge scores, [depth][parent slot][child slot]
   const int32_t *topk_ids;      // [B, L, K]
   const uint8_t *id_rank;       // [B, L, K] rank of each candidate's token id in its depth
   const uint8_t *positive;      // [B, L] some edge score of that depth is > 0
@@ -86,9 +87,8 @@ struct SelMem {
   } u;
   int32_t cand[kMaxL * kMaxK];
   uint8_t idr[kMaxL * kMaxK];
-  // ranked rows of the sequence, staged when they fit
+  // edge rows of the sequence, staged when they fit
   alignas(16) float rows[kStageRows];
-  alignas(16) uint8_t rowc[kStageRows];
   // reductions and scalars
   int32_t dcnt[kMaxL];   // nodes per depth
   int32_t doff[kMaxL];   // first canonical index of each depth
@@ -267,20 +267,22 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
   return kept;
 }
 
-// Ranked-row helpers for K % 4 == 0 with kv = K / 4 groups of four, KV the
-// next power of two >= kv.  Every load is issued unconditionally (clamped to
-// the row) before any use, so one memory round trip covers the row.
+// Edge-row helpers for K % 4 == 0 with kv = K / 4 groups of four, KV the
+// next power of two >= kv.  A row holds the K children's edge scores in
+// child-slot order.  Every load is issued unconditionally (clamped to the
+// row) before any use, so one memory round trip covers the row.
 
-// Number of children r < K with ps + row[r] >= theta (fp64 sums).
+// Number of children r < K with ps + row[r] >= theta (fp64 sums), and the
+// row's smallest edge score.
 template <int KV>
 __device__ __forceinline__ int count_reach(const float *row, int kv, double ps, double theta,
-                                           float &last) {
+                                           float &rmin) {
   const float4 *r4 = reinterpret_cast<const float4 *>(row);
   float4 v[KV];
 #pragma unroll
   for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
-  last = v[KV - 1].w;   // group kv - 1 (clamped), element K - 1
   int c = 0;
+  float mn = v[0].x;
 #pragma unroll
   for (int q = 0; q < KV; ++q) {
     const int g = (ps + static_cast<double>(v[q].x) >= theta) +
@@ -288,13 +290,16 @@ __device__ __forceinline__ int count_reach(const float *row, int kv, double ps, 
                   (ps + static_cast<double>(v[q].z) >= theta) +
                   (ps + static_cast<double>(v[q].w) >= theta);
     c += q < kv ? g : 0;
+    mn = fminf(mn, fminf(fminf(v[q].x, v[q].y), fminf(v[q].z, v[q].w)));   // clamped groups repeat
   }
+  rmin = mn;
   return c;
 }
 
-// Adds the first cnt children of a row (scores ps + row[r]) to the histogram.
+// Adds the children of a row that reach theta (scores ps + row[r]) to the
+// histogram.
 template <int KV>
-__device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv, int cnt,
+__device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv, double theta,
                                              double ps, double hi, double scale) {
   const float4 *r4 = reinterpret_cast<const float4 *>(row);
   float4 v[KV];
@@ -302,48 +307,44 @@ __device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv
   for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
 #pragma unroll
   for (int q = 0; q < KV; ++q) {
-    if (q * 4 >= cnt) break;
     const float f[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (q * 4 + k < cnt)
-        atomicAdd(&s.u.b.hist[hslot(score_bin(ps + static_cast<double>(f[k]), hi, scale))], 1);
+    for (int k = 0; k < 4; ++k) {
+      const double sc = ps + static_cast<double>(f[k]);
+      if (q < kv && sc >= theta) atomicAdd(&s.u.b.hist[hslot(score_bin(sc, hi, scale))], 1);
+    }
   }
 }
 
-// Appends the first cnt children of a row at dst (scores ps + row[r], info
-// with parent x at depth d + 1).
+// Appends the children of a row that reach theta at dst, dst + 1, ... in
+// child-slot order (scores ps + row[r], info with parent x at depth d + 1) and
+// returns the smallest appended score.
 template <int KV>
-__device__ __forceinline__ void append_children(SelMem &s, const float *row, const uint8_t *rowc,
-                                                int kv, int cnt, int dst, int x, int d,
-                                                double ps, const uint8_t *idr) {
+__device__ __forceinline__ double append_children(SelMem &s, const float *row, int kv,
+                                                  double theta, int dst, int x, int d, double ps,
+                                                  const uint8_t *idr) {
   const float4 *r4 = reinterpret_cast<const float4 *>(row);
-  const uint32_t *c4 = reinterpret_cast<const uint32_t *>(rowc);
   float4 v[KV];
-  uint32_t w[KV];
+#pragma unroll
+  for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
+  double vmin = INFINITY;
 #pragma unroll
   for (int q = 0; q < KV; ++q) {
-    v[q] = r4[q < kv ? q : kv - 1];
-    w[q] = c4[q < kv ? q : kv - 1];
-  }
-#pragma unroll
-  for (int q = 0; q < KV; ++q) {
-    if (q * 4 >= cnt) break;
     const float f[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
-    int slot[4], rk[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) slot[k] = static_cast<int>((w[q] >> (8 * k)) & 0xFF);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) rk[k] = idr[slot[k]];   // every slot of the row is < K
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int r = q * 4 + k;
-      if (r < cnt) {
-        s.p_score[dst + r] = ps + static_cast<double>(f[k]);
-        s.p_info[dst + r] = pinfo(x, d + 1, slot[k], rk[k]);
+      const double sc = ps + static_cast<double>(f[k]);
+      const bool take = q < kv && sc >= theta;
+      if (take) {
+        const int slot = q * 4 + k;
+        s.p_score[dst] = sc;
+        s.p_info[dst] = pinfo(x, d + 1, slot, idr[slot]);
+        vmin = sc < vmin ? sc : vmin;
       }
+      dst += take ? 1 : 0;
     }
   }
+  return vmin;
 }
 
 // Children of pool entry x (alive, depth < L) that reach theta, and the
@@ -358,28 +359,31 @@ __device__ __forceinline__ Counted entry_count(const SelMem &s, const float *rs,
   const double ps = s.p_score[x];
   if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
   const float *row = rs + (pi_depth(info) * K + pi_slot(info)) * K;
-  float last = 0.f;
+  float rmin = 0.f;
   int c = 0;
-  if (KVP == 1) c = count_reach<1>(row, kv, ps, theta, last);
-  else if (KVP == 2) c = count_reach<2>(row, kv, ps, theta, last);
-  else if (KVP == 4) c = count_reach<4>(row, kv, ps, theta, last);
-  else if (KVP == 8) c = count_reach<8>(row, kv, ps, theta, last);
-  else if (KVP == 16) c = count_reach<16>(row, kv, ps, theta, last);
+  if (KVP == 1) c = count_reach<1>(row, kv, ps, theta, rmin);
+  else if (KVP == 2) c = count_reach<2>(row, kv, ps, theta, rmin);
+  else if (KVP == 4) c = count_reach<4>(row, kv, ps, theta, rmin);
+  else if (KVP == 8) c = count_reach<8>(row, kv, ps, theta, rmin);
+  else if (KVP == 16) c = count_reach<16>(row, kv, ps, theta, rmin);
   else {
-    for (int r = 0; r < K; ++r) c += ps + static_cast<double>(row[r]) >= theta;
-    last = row[K - 1];
+    rmin = row[0];
+    for (int r = 0; r < K; ++r) {
+      c += ps + static_cast<double>(row[r]) >= theta;
+      rmin = fminf(rmin, row[r]);
+    }
   }
-  return {c, ps + static_cast<double>(last)};
+  return {c, ps + static_cast<double>(rmin)};
 }
 
 // A lower bound of the N-th best score, from a histogram over the alive pool
-// entries and the counted children (aux[i] of them) of every entry of
+// entries and the children reaching theta (aux[i] of them) of every entry of
 // [x_lo, n): these are all distinct prefixes, so the score at the start of the
 // bin that holds the N-th of them bounds the final N-th score from below.
 // All the scores lie in [lo, hi]; hist[] is cleared before and after.
 template <bool kLds>
 __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K, int kv, int KVP, int n, int x_lo,
-                              int i0, int per, int n_keep, double lo, double hi) {
+                              int i0, int per, int n_keep, double theta, double lo, double hi) {
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const float *rs = kLds ? s.rows : gs;
   const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
@@ -398,14 +402,16 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
     const uint32_t info = s.p_info[x];
     const float *row = rs + (pi_depth(info) * K + pi_slot(info)) * K;
     const double ps = s.p_score[x];
-    if (KVP == 1) bin_children<1>(s, row, kv, c, ps, hi, scale);
-    else if (KVP == 2) bin_children<2>(s, row, kv, c, ps, hi, scale);
-    else if (KVP == 4) bin_children<4>(s, row, kv, c, ps, hi, scale);
-    else if (KVP == 8) bin_children<8>(s, row, kv, c, ps, hi, scale);
-    else if (KVP == 16) bin_children<16>(s, row, kv, c, ps, hi, scale);
+    if (KVP == 1) bin_children<1>(s, row, kv, theta, ps, hi, scale);
+    else if (KVP == 2) bin_children<2>(s, row, kv, theta, ps, hi, scale);
+    else if (KVP == 4) bin_children<4>(s, row, kv, theta, ps, hi, scale);
+    else if (KVP == 8) bin_children<8>(s, row, kv, theta, ps, hi, scale);
+    else if (KVP == 16) bin_children<16>(s, row, kv, theta, ps, hi, scale);
     else
-      for (int r = 0; r < c; ++r)
-        atomicAdd(&s.u.b.hist[hslot(score_bin(ps + static_cast<double>(row[r]), hi, scale))], 1);
+      for (int r = 0; r < K; ++r) {
+        const double sc = ps + static_cast<double>(row[r]);
+        if (sc >= theta) atomicAdd(&s.u.b.hist[hslot(score_bin(sc, hi, scale))], 1);
+      }
   }
   __syncthreads();
   if (wave == 0) {
@@ -433,53 +439,62 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
   return edge - 1e-9 * (fabs(edge) + fabs(hi) + 1.0);
 }
 
-// Appends the first cnt children of pool entry x at dst and lowers s.lomin
-// to the last (smallest) of them.
-__device__ __forceinline__ void entry_append(SelMem &s, const float *rs, const uint8_t *rc, int x,
-                                             int K, int kv, int KVP, int cnt, int dst) {
+// Appends the children of pool entry x that reach theta at dst (the caller
+// counted them) and returns the smallest appended score.
+__device__ __forceinline__ double entry_append(SelMem &s, const float *rs, int x, int K, int kv,
+                                               int KVP, double theta, int dst) {
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
   const int row = (d * K + pi_slot(info)) * K;
   const double ps = s.p_score[x];
   const uint8_t *idr = s.idr + d * K;
-  if (KVP == 1) append_children<1>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
-  else if (KVP == 2) append_children<2>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
-  else if (KVP == 4) append_children<4>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
-  else if (KVP == 8) append_children<8>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
-  else if (KVP == 16) append_children<16>(s, rs + row, rc + row, kv, cnt, dst, x, d, ps, idr);
-  else
-    for (int r = 0; r < cnt; ++r) {
-      const int slot = rc[row + r];
-      s.p_score[dst + r] = ps + static_cast<double>(rs[row + r]);
-      s.p_info[dst + r] = pinfo(x, d + 1, slot, idr[slot]);
+  if (KVP == 1) return append_children<1>(s, rs + row, kv, theta, dst, x, d, ps, idr);
+  if (KVP == 2) return append_children<2>(s, rs + row, kv, theta, dst, x, d, ps, idr);
+  if (KVP == 4) return append_children<4>(s, rs + row, kv, theta, dst, x, d, ps, idr);
+  if (KVP == 8) return append_children<8>(s, rs + row, kv, theta, dst, x, d, ps, idr);
+  if (KVP == 16) return append_children<16>(s, rs + row, kv, theta, dst, x, d, ps, idr);
+  double vmin = INFINITY;
+  for (int r = 0; r < K; ++r) {
+    const double sc = ps + static_cast<double>(rs[row + r]);
+    if (sc >= theta) {
+      s.p_score[dst] = sc;
+      s.p_info[dst] = pinfo(x, d + 1, r, idr[r]);
+      ++dst;
+      vmin = sc < vmin ? sc : vmin;
     }
-  atomicMin(&s.lomin, ordered_f64(ps + static_cast<double>(rs[row + cnt - 1])));
+  }
+  return vmin;
 }
 
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
-// alive unexpanded entry lies in [x_lo, n).  kLds: the ranked rows are staged
-// in LDS (s.rows / s.rowc), else read from gs / gc.
+// alive unexpanded entry lies in [x_lo, n).  kLds: the edge rows are staged in
+// LDS (s.rows), else read from gs.
 template <bool kLds>
 __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, const float *gs,
-                               const uint8_t *gc, int n_target) {
+                               int n_target) {
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int L = a.L, K = a.K;
   const float *rs = kLds ? s.rows : gs;
-  const uint8_t *rc = kLds ? s.rowc : gc;
   // vector path: K % 4 == 0, kv = K / 4 groups, KVP = next power of two
   const int kv = K / 4;
   const int KVP = (K & 3) ? 0 : kv <= 1 ? 1 : kv <= 2 ? 2 : kv <= 4 ? 4 : kv <= 8 ? 8 : 16;
   for (int r = tid; r < K; r += kSelThreads) {
-    const int slot = rc[r];
     s.p_score[r] = static_cast<double>(rs[r]);
-    s.p_info[r] = pinfo(-1, 1, slot, s.idr[slot]);
+    s.p_info[r] = pinfo(-1, 1, r, s.idr[r]);
   }
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
-  if (tid == 0) s.lomin = ordered_f64(static_cast<double>(rs[K - 1]));
+  // the depth-1 row's largest and smallest scores, in every wave (K <= 64)
+  float r_hi = lane < K ? rs[lane] : -INFINITY, r_lo = lane < K ? rs[lane] : INFINITY;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    r_hi = fmaxf(r_hi, __uint_as_float(xor_lane(__float_as_uint(r_hi), o)));
+    r_lo = fminf(r_lo, __uint_as_float(xor_lane(__float_as_uint(r_lo), o)));
+  }
+  if (tid == 0) s.lomin = ordered_f64(static_cast<double>(r_lo));
   __syncthreads();
   // every prefix scores at most its depth-1 ancestor, so at most the best
   // depth-1 prefix, which is never dropped
-  const double hi = static_cast<double>(rs[0]);
+  const double hi = static_cast<double>(r_hi);
   double theta = -INFINITY;
   bool pruned = false;
   int n = K, n_alive = K, x_lo = 0;
@@ -527,7 +542,8 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       // many children: bound the N-th score by a histogram over the pool and
       // the children, then count again against the tighter bound
       const double lo = theta > -INFINITY ? theta : unordered_f64(s.lomin);
-      const double bound = prune_bound<kLds>(s, gs, K, kv, KVP, n, x_lo, i0, per, n_target, lo, hi);
+      const double bound =
+          prune_bound<kLds>(s, gs, K, kv, KVP, n, x_lo, i0, per, n_target, theta, lo, hi);
       pruned = true;
       if (bound > theta) {
         theta = bound;
@@ -563,13 +579,24 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       if (tid == 0) atomicOr(a.error_flag, 2u);
       break;
     }
+    double amin = INFINITY;
     for (int k = 0; k < per; ++k) {
       const int i = i0 + k;
       if (i >= lim) break;
       const int c = fit ? s.aux[i] : s.aux[i + 1] - s.aux[i];
-      if (c > 0) entry_append(s, rs, rc, x_lo + i, K, kv, KVP, c, dst);
+      if (c > 0) {
+        const double v = entry_append(s, rs, x_lo + i, K, kv, KVP, theta, dst);
+        amin = v < amin ? v : amin;
+      }
       dst += c;
     }
+    // the smallest appended score: one LDS atomic per wave
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const double ov = xor_lane_f64(amin, o);
+      amin = ov < amin ? ov : amin;
+    }
+    if (lane == 0 && amin < INFINITY) atomicMin(&s.lomin, ordered_f64(amin));
     __syncthreads();
     n += grown;
     n_alive += grown;
@@ -674,15 +701,15 @@ __device__ void canon_preorder(SelMem &s, int L, int K, int n, int n_sel) {
 
 // ---------------------------------------------------------------------------
 // Serial fallback (positive edge scores): lazy best-first with a binary heap.
-// Heap entries point at a (parent, rank) stream; popped nodes are written to
-// the pool arrays in pop order (parents before children).
+// A heap entry is a (parent, child slot) candidate; popping it pushes the
+// parent's next child in rank order and the popped node's best child.  Popped
+// nodes are written to the pool arrays in pop order (parents before children).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t hinfo(int parent, int rank, int slot, int depth) {
-  return (static_cast<uint32_t>(parent + 1) << 18) | (static_cast<uint32_t>(rank) << 12) |
-         (static_cast<uint32_t>(slot) << 6) | static_cast<uint32_t>(depth - 1);
+__device__ __forceinline__ uint32_t hinfo(int parent, int slot, int depth) {
+  return (static_cast<uint32_t>(parent + 1) << 18) | (static_cast<uint32_t>(slot) << 6) |
+         static_cast<uint32_t>(depth - 1);
 }
 __device__ __forceinline__ int hi_parent(uint32_t v) { return static_cast<int>(v >> 18) - 1; }
-__device__ __forceinline__ int hi_rank(uint32_t v) { return static_cast<int>((v >> 12) & 63); }
 __device__ __forceinline__ int hi_slot(uint32_t v) { return static_cast<int>((v >> 6) & 63); }
 __device__ __forceinline__ int hi_depth(uint32_t v) { return static_cast<int>(v & 63) + 1; }
 
@@ -741,28 +768,55 @@ __device__ void heap_pop_root(SelMem &s, int K, int &n) {
   }
 }
 
-__device__ void select_serial(SelMem &s, const SelectArgs &a, const float *rs, const uint8_t *rc,
-                              int n_target) {
+// Rank key of child slot c of a row: larger = earlier in (edge score desc,
+// token id asc).  idr is the depth's rank of each candidate's token id.
+__device__ __forceinline__ uint64_t child_key(const float *row, const uint8_t *idr, int c) {
+  return (static_cast<uint64_t>(ordered_f32(row[c] + 0.0f)) << 32) |
+         (static_cast<uint64_t>(63 - idr[c]) << 6) | static_cast<uint64_t>(c);
+}
+
+// The child of a row that follows key `after` in rank order (~0 for the
+// first), by a scan of the row; -1 when none is left.
+__device__ __forceinline__ int next_child(const float *row, const uint8_t *idr, int K, uint64_t after) {
+  uint64_t best = 0ull;
+  int slot = -1;
+  for (int c = 0; c < K; ++c) {
+    const uint64_t k = child_key(row, idr, c);
+    if (k < after && k > best) {
+      best = k;
+      slot = c;
+    }
+  }
+  return slot;
+}
+
+__device__ void select_serial(SelMem &s, const SelectArgs &a, const float *rs, int n_target) {
   const int L = a.L, K = a.K;
   int hn = 0, n_sel = 0;
-  if (n_target > 0) heap_push(s, K, hn, static_cast<double>(rs[0]), hinfo(-1, 0, rc[0], 1));
+  if (n_target > 0) {
+    const int c0 = next_child(rs, s.idr, K, ~0ull);
+    heap_push(s, K, hn, static_cast<double>(rs[c0]), hinfo(-1, c0, 1));
+  }
   while (n_sel < n_target && hn > 0) {
     const double score = s.u.heap.score[0];
     const uint32_t info = s.u.heap.info[0];
     heap_pop_root(s, K, hn);
-    const int p = hi_parent(info), r = hi_rank(info), slot = hi_slot(info), d = hi_depth(info);
+    const int p = hi_parent(info), slot = hi_slot(info), d = hi_depth(info);
     const int i = n_sel++;
     s.p_score[i] = score;
     s.p_info[i] = pinfo(p, d, slot, s.idr[(d - 1) * K + slot]);
-    if (r + 1 < K) {   // next sibling under the same parent
+    {   // next sibling under the same parent, in rank order
       const int pslot = p < 0 ? 0 : pi_slot(s.p_info[p]);
       const double pscore = p < 0 ? 0.0 : s.p_score[p];
-      const int off = ((d - 1) * K + pslot) * K + (r + 1);
-      heap_push(s, K, hn, pscore + static_cast<double>(rs[off]), hinfo(p, r + 1, rc[off], d));
+      const float *row = rs + ((d - 1) * K + pslot) * K;
+      const uint8_t *idr = s.idr + (d - 1) * K;
+      const int nx = next_child(row, idr, K, child_key(row, idr, slot));
+      if (nx >= 0) heap_push(s, K, hn, pscore + static_cast<double>(row[nx]), hinfo(p, nx, d));
     }
     if (d < L) {       // best child of the new node
-      const int off = (d * K + slot) * K;
-      heap_push(s, K, hn, score + static_cast<double>(rs[off]), hinfo(i, 0, rc[off], d + 1));
+      const float *row = rs + (d * K + slot) * K;
+      const int c0 = next_child(row, s.idr + d * K, K, ~0ull);
+      heap_push(s, K, hn, score + static_cast<double>(row[c0]), hinfo(i, c0, d + 1));
     }
   }
   s.sc[kNPool] = n_sel;
@@ -822,8 +876,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int L = a.L, K = a.K;
-  const float *ss = a.sorted_score + static_cast<int64_t>(b) * L * K * K;
-  const uint8_t *sc = a.sorted_child + static_cast<int64_t>(b) * L * K * K;
+  const float *ss = a.edge_rows + static_cast<int64_t>(b) * L * K * K;
 
   // wave 0: the budget (computed by the edge stage) and the sign flags
   int budget0 = 0;
@@ -837,41 +890,27 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
     s.cand[i] = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
     s.idr[i] = a.id_rank[static_cast<int64_t>(b) * L * K + i];
   }
-  // waves 1.. stage the ranked rows (16-byte loads, all issued before the
+  // waves 1.. stage the edge rows (16-byte loads, all issued before the
   // stores) while wave 0 computes the budget
   const bool staged = L * K * K <= kStageRows;
   constexpr int kStageThreads = kSelThreads - kWave;
-  if (staged && tid >= kWave && (L * K * K) % 16 != 0) {
-    for (int i = tid - kWave; i < L * K * K; i += kStageThreads) {
-      s.rows[i] = ss[i];
-      s.rowc[i] = sc[i];
-    }
+  if (staged && tid >= kWave && (L * K * K) % 4 != 0) {
+    for (int i = tid - kWave; i < L * K * K; i += kStageThreads) s.rows[i] = ss[i];
   } else if (staged && tid >= kWave) {
-    // L*K*K is a multiple of 16 here, so both sequences' bases are 16-byte aligned
+    // L*K*K is a multiple of 4 here, so the sequence's base is 16-byte aligned
     constexpr int kF4 = (kStageRows / 4 + kStageThreads - 1) / kStageThreads;
-    constexpr int kB16 = (kStageRows / 16 + kStageThreads - 1) / kStageThreads;
     const int t = tid - kWave;
-    const int nf4 = L * K * K / 4, nb16 = L * K * K / 16;
+    const int nf4 = L * K * K / 4;
     const float4 *src_f = reinterpret_cast<const float4 *>(ss);
-    const uint4 *src_b = reinterpret_cast<const uint4 *>(sc);
     float4 vf[kF4];
-    uint4 vb[kB16];
 #pragma unroll
     for (int k = 0; k < kF4; ++k) {
       const int i = t + k * kStageThreads;
       vf[k] = src_f[i < nf4 ? i : nf4 - 1];
     }
 #pragma unroll
-    for (int k = 0; k < kB16; ++k) {
-      const int i = t + k * kStageThreads;
-      vb[k] = src_b[i < nb16 ? i : nb16 - 1];
-    }
-#pragma unroll
     for (int k = 0; k < kF4; ++k)
       if (t + k * kStageThreads < nf4) reinterpret_cast<float4 *>(s.rows)[t + k * kStageThreads] = vf[k];
-#pragma unroll
-    for (int k = 0; k < kB16; ++k)
-      if (t + k * kStageThreads < nb16) reinterpret_cast<uint4 *>(s.rowc)[t + k * kStageThreads] = vb[k];
   }
 
   // ---------------- budget and sign flags ----------------
@@ -890,16 +929,16 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   const bool mono = s.sc[kMono] != 0;
   if (mono) {
     if (n_target > 0) {
-      const int n_pool = staged ? select_parallel<true>(s, a, ss, sc, n_target)
-                                : select_parallel<false>(s, a, ss, sc, n_target);
+      const int n_pool = staged ? select_parallel<true>(s, a, ss, n_target)
+                                : select_parallel<false>(s, a, ss, n_target);
       if (tid == 0) s.sc[kNPool] = n_pool;
     } else if (tid == 0) {
       s.sc[kNPool] = 0;
       s.sc[kNSel] = 0;
     }
   } else if (tid == 0) {
-    if (staged) select_serial(s, a, s.rows, s.rowc, n_target);
-    else select_serial(s, a, ss, sc, n_target);
+    if (staged) select_serial(s, a, s.rows, n_target);
+    else select_serial(s, a, ss, n_target);
   }
   __syncthreads();
   const int n = s.sc[kNPool];       // pool entries, dead ones included
@@ -992,8 +1031,7 @@ hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_t
   a.K = d.top_k;
   a.n_max = d.max_nodes;
   a.words = (d.max_nodes + 63) / 64;
-  a.sorted_score = ctx->sorted_score;
-  a.sorted_child = ctx->sorted_child;
+  a.edge_rows = ctx->edge_rows;
   a.topk_ids = ctx->topk_ids;
   a.id_rank = ctx->id_rank;
   a.positive = ctx->positive;
