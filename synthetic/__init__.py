@@ -34,6 +34,7 @@ __all__ = [
     "Workload", "WORKLOADS", "workload", "bf16_from_f32", "f32_from_bf16",
     "gen_sequence_logits", "gen_round", "gen_scorer", "saba_params",
     "hist_ring_init", "node_targets", "splitmix64", "NODE_TARGET_P_NUM", "gen_hidden",
+    "gen_traces",
 ]
 
 HIST_WINDOW = 4
@@ -322,3 +323,76 @@ def node_targets(seed: int, b, depth, parent_tok, tok, topk_ids_seq, V: int, L: 
     from_cand = topk[nd, r]
     use = pick & (depth < L)
     return np.where(use, from_cand, hashed).astype(np.int32)
+
+
+def gen_traces(w: Workload, n_groups: int, n_pairs: int, step: int = 0) -> dict:
+    """A batch of synthetic target-model traces for TDES training, shaped like
+    the workload's rounds (its vocabulary, L and K).
+
+    groups: parent tokens Zipf(1.1)-distributed over a fixed random permutation
+      of the vocabulary; depth d in 1..L with P(d) proportional to 0.8^(d-1);
+      K distinct children (Zipf draws, topped up uniformly); logq strictly
+      descending, logq_k = -0.2 - 0.7 * (E_1 + ... + E_k), E_i ~ Exp(1);
+      target logits z = 2 logq + N(0, 1); target token = the child with the
+      largest z with probability 0.8, else a token outside the children.
+    pairs: v+ = (parent, target, d) of a group whose target is a child; v- keeps
+      the child under a uniformly drawn wrong parent, or (with probability 0.5)
+      a competing child under the right parent.
+    Integer arrays are int32, real ones float32.
+    """
+    g = np.random.default_rng([w.seed, w.wid, 91, step, n_groups, n_pairs])
+    V, L, K = w.V, w.L, w.K
+    perm = np.random.default_rng([w.seed, w.wid, 92]).permutation(V)
+
+    def zipf_tokens(n):
+        r = g.zipf(1.1, size=n) - 1
+        r = np.where(r < V, r, g.integers(0, V, size=n))
+        return perm[r]
+
+    G = n_groups
+    parent = zipf_tokens(G).astype(np.int32)
+    pd = 0.8 ** np.arange(L)
+    depth = (g.choice(L, size=G, p=pd / pd.sum()) + 1).astype(np.int32)
+    child = np.empty((G, K), np.int32)
+    for i in range(G):
+        c = np.unique(zipf_tokens(2 * K))
+        g.shuffle(c)
+        c = list(c[:K])
+        seen = set(int(x) for x in c)
+        while len(c) < K:
+            t = int(g.integers(0, V))
+            if t not in seen:
+                seen.add(t)
+                c.append(t)
+        child[i] = c
+    logq = (-0.2 - 0.7 * np.cumsum(g.exponential(1.0, size=(G, K)), axis=1)).astype(np.float32)
+    z = (2.0 * logq + g.standard_normal((G, K))).astype(np.float32)
+    hit = g.random(G) < 0.8
+    target = np.empty(G, np.int32)
+    for i in range(G):
+        if hit[i]:
+            target[i] = child[i, int(np.argmax(z[i]))]
+        else:
+            t = int(g.integers(0, V))
+            while t in set(child[i].tolist()):
+                t = int(g.integers(0, V))
+            target[i] = t
+    pairs = np.empty((n_pairs, 6), np.int32)
+    pos = np.flatnonzero(hit) if hit.any() else np.arange(max(G, 1))
+    for i in range(n_pairs):
+        if G == 0:
+            p, c, q = (int(x) for x in g.integers(0, V, size=3))
+            pairs[i] = (p, c, 1, q, c, 1)
+            continue
+        k = int(pos[int(g.integers(0, len(pos)))])
+        p, c, d = int(parent[k]), int(target[k]), int(depth[k])
+        if g.random() < 0.5 and K > 1:
+            alt = [int(x) for x in child[k] if int(x) != c]
+            pairs[i] = (p, c, d, p, alt[int(g.integers(0, len(alt)))], d)
+        else:
+            q = int(g.integers(0, V))
+            while q == p:
+                q = int(g.integers(0, V))
+            pairs[i] = (p, c, d, q, c, d)
+    return dict(parent=parent, depth=depth, child=child, logq=logq, z=z, target=target,
+                pairs=pairs)
