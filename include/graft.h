@@ -279,6 +279,91 @@ GRAFT_API int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t s
 GRAFT_API int graft_profile_begin(graft_ctx *ctx, int32_t max_calls);
 GRAFT_API int graft_profile_end(graft_ctx *ctx, double *stage_ms, int32_t *stage_calls);
 
+/* ------------------------------------------------------------------------ */
+/* TDES training (the paper's Target-Distilled Edge Scoring section: the       */
+/* objectives KL, pairwise margin and class-balanced BCE, summed by eq.         */
+/* tdes-training, and AdamW as in its training setup).                          */
+/* ------------------------------------------------------------------------ */
+
+typedef struct graft_tdes graft_tdes;
+
+/* Sizes fixed for the life of a trainer.  Supported: emb_dim E in {32, 64,
+ * 128}; score_dim m in 1..64 with E * M <= 4096 and num_pos * M <= 1024, where
+ * M = m rounded up to a multiple of 16; top_k 1..64. */
+typedef struct {
+    int32_t vocab;       /* V, rows of the frozen embedding table */
+    int32_t emb_dim;     /* E */
+    int32_t score_dim;   /* m */
+    int32_t num_pos;     /* L: depths 1..L */
+    int32_t top_k;       /* K: children per group */
+    int32_t max_groups;  /* >= 0 */
+    int32_t max_pairs;   /* >= 0 */
+} graft_tdes_dims;
+
+/* One batch of target-model traces (device arrays, int32 / fp32).
+ *   Groups g < n_groups (each an accepted parent and its candidate children
+ *   C_{p,d}): parent[g], depth[g] in 1..L, child[g, K], logq[g, K] (drafter
+ *   log-probabilities of the children), z_target[g, K] (target-model logits of
+ *   the children), target[g] (the target's next token under the parent, -1 if
+ *   none).  Every child is a verified edge of the BCE objective, labelled 1
+ *   where it equals target[g].
+ *   Pairs i < n_pairs: pairs[i, 0..5] = (p+, c+, d+, p-, c-, d-), a
+ *   target-compatible edge and an incompatible alternative.
+ * Token ids outside [0, V) or depths outside 1..L drop their group or pair
+ * tile and are reported by graft_tdes_device_status. */
+typedef struct {
+    int32_t n_groups;
+    const int32_t *parent;
+    const int32_t *depth;
+    const int32_t *child;
+    const float *logq;
+    const float *z_target;
+    const int32_t *target;
+    int32_t n_pairs;
+    const int32_t *pairs;
+} graft_tdes_batch;
+
+/* L = lambda_kl * mean_groups KL(softmax(z) || softmax(logq + f))
+ *   + lambda_pair * mean_pairs softplus(gamma - f(v+) + f(v-))
+ *   - lambda_bce * mean_edges [w1 y log sigmoid(f) + (1 - y) log(1 - sigmoid(f))]
+ * (an empty mean is 0).  The paper trains with lambda = (1, 1, 0.25), AdamW at
+ * lr 2e-3 and weight decay 1e-4; beta1 = 0.9, beta2 = 0.999, eps = 1e-8 are
+ * the usual AdamW defaults. */
+typedef struct {
+    float lambda_kl, lambda_pair, lambda_bce;
+    float gamma;          /* margin of the pairwise objective */
+    float w1;             /* weight of the positive edges in the BCE */
+    float lr, weight_decay, beta1, beta2, eps;
+} graft_tdes_hyper;
+
+/* Creates a trainer and its workspace (block partial gradients; synchronous). */
+GRAFT_API int graft_tdes_create(const graft_tdes_dims *dims /* host */, graft_tdes **out /* host */);
+GRAFT_API void graft_tdes_destroy(graft_tdes *t);
+
+/* Number of trainable parameters: 2 E m + L m + 1, laid out as
+ *   g_parent [E, m] row-major | g_child [E, m] | depth_emb [L, m] (u_d at row
+ *   d - 1) | scale s,
+ * the arrays graft_scorer_desc takes (its scale is the last element). */
+GRAFT_API int64_t graft_tdes_param_count(const graft_tdes_dims *dims /* host */);
+
+/* One training step on `stream`: the objective and its gradient at theta for
+ * the batch, then AdamW (decoupled weight decay on every parameter, bias
+ * corrections for step `step` >= 1) updating theta, adam_m and adam_v in place
+ * (device [param_count] fp32; the moments start at zero).  emb [V, E] fp32,
+ * 16-byte aligned, frozen.  loss (device, 4 doubles: L, L_KL, L_pair, L_BCE at
+ * theta before the update) and grad (device [param_count] fp32: dL/dtheta) may
+ * be NULL.  The step is deterministic: partial gradients are summed in a
+ * fixed order. */
+GRAFT_API int graft_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *batch /* host */,
+                              const graft_tdes_hyper *hyper /* host */, int32_t step, float *theta,
+                              float *adam_m, float *adam_v, double *loss, float *grad,
+                              graft_stream_t stream);
+
+/* Synchronizes `stream`; GRAFT_OK, or GRAFT_ERR_DEVICE_DATA if a step since the
+ * last call dropped a group or pair tile for invalid ids (the flag is then
+ * cleared). */
+GRAFT_API int graft_tdes_device_status(graft_tdes *t, graft_stream_t stream);
+
 GRAFT_API const char *graft_status_string(int status);
 GRAFT_API const char *graft_last_error(void);
 

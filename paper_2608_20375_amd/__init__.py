@@ -12,7 +12,8 @@ import os
 
 import torch
 
-__all__ = ["Context", "TreeBuffers", "lib", "library_path", "GraftError", "EXPORTED_SYMBOLS"]
+__all__ = ["Context", "TreeBuffers", "TdesTrainer", "TdesHyper", "lib", "library_path",
+           "GraftError", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libgraft.so")
@@ -22,7 +23,8 @@ EXPORTED_SYMBOLS = (
     "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
     "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
     "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
-    "graft_mask_to_bias", "graft_commit_accepted",
+    "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create", "graft_tdes_destroy",
+    "graft_tdes_param_count", "graft_tdes_step", "graft_tdes_device_status",
 )
 
 
@@ -65,6 +67,31 @@ class TreeOut(C.Structure):
                 ("saba_state", C.c_void_p), ("adj_cos", C.c_void_p)]
 
 
+class TdesDims(C.Structure):
+    _fields_ = [("vocab", C.c_int32), ("emb_dim", C.c_int32), ("score_dim", C.c_int32),
+                ("num_pos", C.c_int32), ("top_k", C.c_int32), ("max_groups", C.c_int32),
+                ("max_pairs", C.c_int32)]
+
+
+class TdesBatch(C.Structure):
+    _fields_ = [("n_groups", C.c_int32), ("parent", C.c_void_p), ("depth", C.c_void_p),
+                ("child", C.c_void_p), ("logq", C.c_void_p), ("z_target", C.c_void_p),
+                ("target", C.c_void_p), ("n_pairs", C.c_int32), ("pairs", C.c_void_p)]
+
+
+class TdesHyper(C.Structure):
+    """Loss weights, margin, positive weight and AdamW settings; the defaults
+    are the paper's training setup (lambda 1 / 1 / 0.25, lr 2e-3, weight decay
+    1e-4) with the usual AdamW betas and eps, margin 1 and w1 = 1."""
+    _fields_ = [(n, C.c_float) for n in ("lambda_kl", "lambda_pair", "lambda_bce", "gamma", "w1",
+                                         "lr", "weight_decay", "beta1", "beta2", "eps")]
+
+    def __init__(self, lambda_kl=1.0, lambda_pair=1.0, lambda_bce=0.25, gamma=1.0, w1=1.0,
+                 lr=2e-3, weight_decay=1e-4, beta1=0.9, beta2=0.999, eps=1e-8):
+        super().__init__(lambda_kl, lambda_pair, lambda_bce, gamma, w1, lr, weight_decay, beta1,
+                         beta2, eps)
+
+
 class Targets(C.Structure):
     _fields_ = [("target_root", C.c_void_p), ("target_node", C.c_void_p),
                 ("target_depth", C.c_void_p)]
@@ -99,6 +126,14 @@ def lib():
                                             i64, i64, i64, vp]
         L.graft_profile_begin.argtypes = [vp, i32]
         L.graft_profile_end.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
+        L.graft_tdes_create.argtypes = [C.POINTER(TdesDims), C.POINTER(vp)]
+        L.graft_tdes_destroy.argtypes = [vp]
+        L.graft_tdes_destroy.restype = None
+        L.graft_tdes_param_count.argtypes = [C.POINTER(TdesDims)]
+        L.graft_tdes_param_count.restype = C.c_int64
+        L.graft_tdes_step.argtypes = [vp, vp, C.POINTER(TdesBatch), C.POINTER(TdesHyper), i32, vp,
+                                      vp, vp, vp, vp, vp]
+        L.graft_tdes_device_status.argtypes = [vp, vp]
         L.graft_status_string.argtypes = [C.c_int]
         L.graft_status_string.restype = C.c_char_p
         L.graft_last_error.argtypes = []
@@ -106,7 +141,8 @@ def lib():
         for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
                   "graft_build_tree", "graft_accept", "graft_get_device_status",
                   "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
-                  "graft_mask_to_bias", "graft_commit_accepted"):
+                  "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create",
+                  "graft_tdes_step", "graft_tdes_device_status"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -326,3 +362,83 @@ class Context:
 
     def device_status(self) -> int:
         return lib().graft_get_device_status(self._h, _stream())
+
+
+class TdesTrainer:
+    """A graft_tdes: one TDES training step per call (objectives of eq.
+    tdes-training and AdamW), on tensors the caller owns.  theta, adam_m and
+    adam_v are fp32 [param_count] vectors laid out as g_parent [E, m] |
+    g_child [E, m] | depth_emb [L, m] | scale."""
+
+    def __init__(self, vocab: int, emb_dim: int, score_dim: int, num_pos: int, top_k: int,
+                 max_groups: int, max_pairs: int):
+        L = lib()
+        self.dims = TdesDims(vocab, emb_dim, score_dim, num_pos, top_k, max_groups, max_pairs)
+        h = C.c_void_p()
+        _check(L.graft_tdes_create(C.byref(self.dims), C.byref(h)), "graft_tdes_create")
+        self._h = h
+        self.param_count = int(L.graft_tdes_param_count(C.byref(self.dims)))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().graft_tdes_destroy(self._h)
+            self._h = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def split(self, theta):
+        """Views (g_parent, g_child, depth_emb, scale) of a parameter vector."""
+        d = self.dims
+        n = d.emb_dim * d.score_dim
+        return (theta[:n].view(d.emb_dim, d.score_dim), theta[n:2 * n].view(d.emb_dim, d.score_dim),
+                theta[2 * n:2 * n + d.num_pos * d.score_dim].view(d.num_pos, d.score_dim),
+                theta[-1:])
+
+    def step(self, emb, batch: dict, theta, adam_m, adam_v, step: int, hyper: TdesHyper = None,
+             loss=None, grad=None):
+        """One step on `batch` (CUDA tensors: parent, depth, target int32 [G]; child
+        int32 [G, K]; logq, z float32 [G, K]; pairs int32 [P, 6]).  Updates theta,
+        adam_m, adam_v in place; writes loss (float64 [4]) and grad when given."""
+        d = self.dims
+        G = int(batch["child"].shape[0]) if "child" in batch else 0
+        P = int(batch["pairs"].shape[0]) if "pairs" in batch else 0
+        if G and tuple(batch["child"].shape) != (G, d.top_k):
+            raise ValueError("child must be [G, %d]" % d.top_k)
+        i32, f32 = torch.int32, torch.float32
+        b = TdesBatch(G, _ptr(batch["parent"], i32, "parent") if G else None,
+                      _ptr(batch["depth"], i32, "depth") if G else None,
+                      _ptr(batch["child"], i32, "child") if G else None,
+                      _ptr(batch["logq"], f32, "logq") if G else None,
+                      _ptr(batch["z"], f32, "z") if G else None,
+                      _ptr(batch["target"], i32, "target") if G else None,
+                      P, _ptr(batch["pairs"], i32, "pairs") if P else None)
+        if G:
+            for k in ("parent", "depth", "target"):
+                if batch[k].numel() != G:
+                    raise ValueError("%s must have %d entries" % (k, G))
+            for k in ("logq", "z"):
+                if tuple(batch[k].shape) != (G, d.top_k):
+                    raise ValueError("%s must be [G, K]" % k)
+        if P and tuple(batch["pairs"].shape) != (P, 6):
+            raise ValueError("pairs must be [P, 6]")
+        for name, t in (("theta", theta), ("adam_m", adam_m), ("adam_v", adam_v), ("grad", grad)):
+            if t is not None and t.numel() != self.param_count:
+                raise ValueError("%s must have %d entries" % (name, self.param_count))
+        if tuple(emb.shape) != (d.vocab, d.emb_dim):
+            raise ValueError("emb must be [%d, %d]" % (d.vocab, d.emb_dim))
+        if loss is not None and (loss.dtype != torch.float64 or loss.numel() < 4):
+            raise ValueError("loss must be float64 with 4 entries")
+        h = hyper if hyper is not None else TdesHyper()
+        _check(lib().graft_tdes_step(self._h, _ptr(emb, f32, "emb"), C.byref(b), C.byref(h),
+                                     int(step), _ptr(theta, f32, "theta"),
+                                     _ptr(adam_m, f32, "adam_m"), _ptr(adam_v, f32, "adam_v"),
+                                     _ptr(loss, torch.float64, "loss"), _ptr(grad, f32, "grad"),
+                                     _stream()), "graft_tdes_step")
+
+    def device_status(self) -> int:
+        return lib().graft_tdes_device_status(self._h, _stream())
+

@@ -463,4 +463,104 @@ int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t seed,
   return GRAFT_OK;
 }
 
+int64_t graft_tdes_param_count(const graft_tdes_dims *d) {
+  if (!d || d->emb_dim < 1 || d->score_dim < 1 || d->num_pos < 1) return -1;
+  return 2 * static_cast<int64_t>(d->emb_dim) * d->score_dim +
+         static_cast<int64_t>(d->num_pos) * d->score_dim + 1;
+}
+
+int graft_tdes_create(const graft_tdes_dims *dims, graft_tdes **out) {
+  if (!dims || !out) return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_create: NULL argument");
+  *out = nullptr;
+  const graft_tdes_dims d = *dims;
+  if (d.vocab < 1 || d.emb_dim < 1 || d.score_dim < 1 || d.num_pos < 1 || d.top_k < 1 ||
+      d.max_groups < 0 || d.max_pairs < 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_create: sizes must be positive");
+  if (d.top_k > d.vocab)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_create: top_k %d > vocab %d", d.top_k, d.vocab);
+  if (!graft::tdes_shape_supported(d.emb_dim, d.score_dim, d.num_pos, d.top_k))
+    return fail(GRAFT_ERR_UNSUPPORTED,
+                "graft_tdes_create: unsupported shape E=%d m=%d L=%d K=%d (E in {32, 64, 128}, "
+                "E*M <= 4096, L*M <= 1024 for M = m rounded up to 16, K <= 64)",
+                d.emb_dim, d.score_dim, d.num_pos, d.top_k);
+  if (static_cast<int64_t>(d.max_groups) * d.top_k > (int64_t{1} << 31) - 1)
+    return fail(GRAFT_ERR_UNSUPPORTED, "graft_tdes_create: max_groups * top_k too large");
+  graft_tdes *t = new (std::nothrow) graft_tdes();
+  if (!t) return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_tdes_create: host allocation failed");
+  t->dims = d;
+  const size_t n_g = 2 * static_cast<size_t>(d.emb_dim) * d.score_dim +
+                     static_cast<size_t>(d.num_pos) * d.score_dim;
+  hipError_t e = dalloc(&t->part_g, n_g * graft::kTdesMaxBlocks);
+  if (e == hipSuccess) e = dalloc(&t->part_d, 4 * static_cast<size_t>(graft::kTdesMaxBlocks));
+  if (e == hipSuccess) e = dalloc(&t->error_flag, 1);
+  if (e == hipSuccess) e = hipMemset(t->error_flag, 0, sizeof(uint32_t));
+  if (e != hipSuccess) {
+    graft_tdes_destroy(t);
+    return e == hipErrorOutOfMemory ? fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_tdes_create: %s",
+                                           hipGetErrorString(e))
+                                    : hip_fail(e, "graft_tdes_create");
+  }
+  *out = t;
+  return GRAFT_OK;
+}
+
+void graft_tdes_destroy(graft_tdes *t) {
+  if (!t) return;
+  (void)hipDeviceSynchronize();
+  (void)hipFree(t->part_g);
+  (void)hipFree(t->part_d);
+  (void)hipFree(t->error_flag);
+  delete t;
+}
+
+int graft_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *b,
+                    const graft_tdes_hyper *h, int32_t step, float *theta, float *adam_m,
+                    float *adam_v, double *loss, float *grad, graft_stream_t stream) {
+  if (!t || !emb || !b || !h || !theta || !adam_m || !adam_v)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: NULL argument");
+  const graft_tdes_dims &d = t->dims;
+  if (b->n_groups < 0 || b->n_groups > d.max_groups)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: n_groups %d outside 0..%d", b->n_groups,
+                d.max_groups);
+  if (b->n_pairs < 0 || b->n_pairs > d.max_pairs)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: n_pairs %d outside 0..%d", b->n_pairs,
+                d.max_pairs);
+  if (b->n_groups > 0 &&
+      (!b->parent || !b->depth || !b->child || !b->logq || !b->z_target || !b->target))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: a group array is NULL");
+  if (b->n_pairs > 0 && !b->pairs)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: pairs is NULL");
+  if (reinterpret_cast<uintptr_t>(emb) % 16 != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: emb must be 16-byte aligned");
+  if (step < 1) return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: step must be >= 1");
+  const float hv[10] = {h->lambda_kl, h->lambda_pair, h->lambda_bce, h->gamma, h->w1,
+                        h->lr, h->weight_decay, h->beta1, h->beta2, h->eps};
+  for (float v : hv)
+    if (!std::isfinite(v)) return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: non-finite hyper-parameter");
+  if (h->lr < 0.0f || h->weight_decay < 0.0f || h->eps <= 0.0f || h->beta1 < 0.0f ||
+      h->beta1 >= 1.0f || h->beta2 < 0.0f || h->beta2 >= 1.0f)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: AdamW settings out of range");
+  hipError_t e = graft::launch_tdes_step(t, emb, b, h, step, theta, adam_m, adam_v, loss, grad,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graft_tdes_step");
+  return GRAFT_OK;
+}
+
+int graft_tdes_device_status(graft_tdes *t, graft_stream_t stream) {
+  if (!t) return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_device_status: NULL trainer");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint32_t flag = 0;
+  hipError_t e = hipMemcpyAsync(&flag, t->error_flag, sizeof flag, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "graft_tdes_device_status");
+  if (flag) {
+    e = hipMemsetAsync(t->error_flag, 0, sizeof flag, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "graft_tdes_device_status: clear");
+    return fail(GRAFT_ERR_DEVICE_DATA, "training step dropped items with invalid ids (flags 0x%x)",
+                flag);
+  }
+  return GRAFT_OK;
+}
+
 }  // extern "C"

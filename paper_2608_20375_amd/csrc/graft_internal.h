@@ -14,6 +14,7 @@ constexpr int kMaxK = 64;
 constexpr int kMaxNodes = 1024;
 constexpr int kMaxGrid = 64;
 constexpr int kMaxScoreDim = 64;
+constexpr int kTdesMaxBlocks = 256;
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -249,6 +250,13 @@ struct graft_ctx {
   int32_t prof_cap, prof_nbuild, prof_nacc;
 };
 
+struct graft_tdes {
+  graft_tdes_dims dims;
+  float *part_g;           // [kTdesMaxBlocks, 2 E m + L m] block partial gradients
+  double *part_d;          // [kTdesMaxBlocks, 4] scale gradient and loss sums
+  uint32_t *error_flag;
+};
+
 namespace graft {
 
 // Launchers (stream-ordered, no synchronization).  They return hipError_t.
@@ -279,6 +287,14 @@ hipError_t launch_synth_targets(graft_ctx *ctx, int batch, uint64_t seed,
                                 const int32_t *tokens, const int32_t *parents,
                                 const int32_t *topk_ids, int32_t *target_root,
                                 int32_t *target_node, hipStream_t stream);
+
+// TDES training step: block count for a batch, the instantiated shapes, and
+// the two launches (train_kernel, update_kernel).
+int tdes_blocks(int G, int P);
+bool tdes_shape_supported(int E, int m, int L, int K);
+hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *b,
+                            const graft_tdes_hyper *h, int32_t step, float *theta, float *m1,
+                            float *m2, double *loss, float *grad, hipStream_t stream);
 
 // Number of splits per row used by the logits pass for a given row count.
 int logits_splits(const graft_dims &d, int rows);
