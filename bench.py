@@ -129,6 +129,69 @@ def time_verifier(ctx, w, tb, acc_len, acc_nodes, steps, torch, dev):
             "kv": "%d planes x batch %d x %d rows x %d bytes" % (planes, w.batch, w.n_max, row)}
 
 
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+
+def time_training(w, steps, torch, dev, G=4096, P=4096, cpu=True):
+    """One TDES training step per call (objectives of eq. tdes-training, their
+    gradient and AdamW) on a batch of synthetic target-model traces shaped like
+    the workload (its vocabulary, L, K and scorer: E = emb_dim, m = rank): G
+    groups of K children and P pairs.  GPU time per step from events around
+    `steps` calls queued behind a sleep kernel; algorithmic work per step:
+      flops = 2 E m (2 (G (K + 1) + 4 P) + G)   (projection of every parent,
+              child and pair row, its weight-gradient contraction, and the
+              parent-side matrix-vector product of each group),
+      bytes = 4 E (G (K + 1) + 4 P) gathered embedding rows + the traces.
+    The oracle's CPU time for the same step is reported beside it."""
+    import synthetic as S
+    import paper_2608_20375_amd as GR
+    sc = S.gen_scorer(w, "paper")
+    tr = S.gen_traces(w, G, P)
+    E, m, L, K = w.emb_dim, w.rank, w.L, w.K
+    theta0 = np.concatenate([sc["g_parent"].ravel(), sc["g_child"].ravel(),
+                             sc["depth_emb"].ravel(), [np.float32(sc["scale"])]]).astype(np.float32)
+    Tt = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    batch = {k: Tt(v) for k, v in tr.items()}
+    emb = Tt(sc["emb"])
+    tt = GR.TdesTrainer(w.V, E, m, L, K, G, P)
+    theta, m1, m2 = Tt(theta0), torch.zeros(theta0.size, device=dev), torch.zeros(theta0.size, device=dev)
+    loss = torch.zeros(4, dtype=torch.float64, device=dev)
+    hyper = GR.TdesHyper(w1=float(K - 1))
+    for i in range(3):
+        tt.step(emb, batch, theta, m1, m2, i + 1, hyper, loss=loss)
+    torch.cuda.synchronize()
+    first_loss = loss.cpu().numpy().tolist()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(100_000_000)
+    e0.record()
+    for i in range(steps):
+        tt.step(emb, batch, theta, m1, m2, i + 4, hyper)
+    e1.record()
+    torch.cuda.synchronize()
+    if tt.device_status() != 0:
+        raise RuntimeError("training step reported invalid ids")
+    us = 1e3 * e0.elapsed_time(e1) / steps
+    rows = G * (K + 1) + 4 * P
+    flops = 2 * E * m * (2 * rows + G)
+    nbytes = 4 * E * rows + G * (12 + 12 * K) + 24 * P
+    out = {"step_us": us, "steps_per_s": 1e6 / us, "groups": G, "pairs": P,
+           "edges_per_s": (G * K + 2 * P) * 1e6 / us,
+           "flops_per_step": flops, "tflops": flops / us / 1e6,
+           "mfma_f32_frac": flops / us / 1e6 / MFMA_F32_PEAK_TFLOPS,
+           "bytes_per_step": nbytes, "gbs": nbytes / us / 1e3,
+           "loss_after_3_steps": first_loss,
+           "shape": "E=%d m=%d L=%d K=%d V=%d" % (E, m, L, K, w.V)}
+    tt.close()
+    if cpu:
+        from oracle import tdes_train as OT
+        h = OT.Hyper(w1=float(K - 1))
+        z = np.zeros(theta0.size)
+        t0 = time.time()
+        OT.train_step(theta0.astype(np.float64), z, z, 1, sc["emb"], tr, h, E, m, L)
+        out["cpu_oracle_step_s"] = time.time() - t0
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,6 +208,9 @@ def main():
                     help="also time the verifier-side consumers after the headline: the bf16 "
                          "attention bias of the draft block and the commit of the accepted "
                          "rows in a key/value cache of 72 planes of 2 KiB rows")
+    ap.add_argument("--train", action="store_true",
+                    help="also time one TDES training step (4096 groups, 4096 pairs of synthetic "
+                         "traces with the workload's vocabulary, L, K and scorer sizes)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
     args = ap.parse_args()
@@ -274,6 +340,11 @@ def main():
         verifier = time_verifier(ctx, w, tb, acc_len, acc_nodes, args.steps, torch, dev)
         log("verifier consumers: %s" % verifier)
 
+    training = None
+    if args.train:
+        training = time_training(w, args.steps, torch, dev, cpu=not args.no_cpu_baseline)
+        log("tdes training step: %s" % training)
+
     nodes = tb.n_nodes.float().mean().item()
     budgets = tb.budget.float().mean().item()
     cpu = None
@@ -327,6 +398,8 @@ def main():
     }
     if verifier is not None:
         result["verifier"] = verifier
+    if training is not None:
+        result["tdes_training"] = training
     print(json.dumps(result), flush=True)
     ctx.close()
 

@@ -488,10 +488,12 @@ int graft_tdes_create(const graft_tdes_dims *dims, graft_tdes **out) {
   graft_tdes *t = new (std::nothrow) graft_tdes();
   if (!t) return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_tdes_create: host allocation failed");
   t->dims = d;
-  const size_t n_g = 2 * static_cast<size_t>(d.emb_dim) * d.score_dim +
-                     static_cast<size_t>(d.num_pos) * d.score_dim;
-  hipError_t e = dalloc(&t->part_g, n_g * graft::kTdesMaxBlocks);
-  if (e == hipSuccess) e = dalloc(&t->part_d, 4 * static_cast<size_t>(graft::kTdesMaxBlocks));
+  const graft::TdesWorkspace ws = graft::tdes_workspace(d);
+  hipError_t e = dalloc(&t->dyc, static_cast<size_t>(ws.dyc));
+  if (e == hipSuccess) e = dalloc(&t->dyp, static_cast<size_t>(ws.dyp));
+  if (e == hipSuccess) e = dalloc(&t->part_u, static_cast<size_t>(ws.part_u));
+  if (e == hipSuccess) e = dalloc(&t->part_d, static_cast<size_t>(ws.part_d));
+  if (e == hipSuccess) e = dalloc(&t->part_w, static_cast<size_t>(ws.part_w));
   if (e == hipSuccess) e = dalloc(&t->error_flag, 1);
   if (e == hipSuccess) e = hipMemset(t->error_flag, 0, sizeof(uint32_t));
   if (e != hipSuccess) {
@@ -507,8 +509,11 @@ int graft_tdes_create(const graft_tdes_dims *dims, graft_tdes **out) {
 void graft_tdes_destroy(graft_tdes *t) {
   if (!t) return;
   (void)hipDeviceSynchronize();
-  (void)hipFree(t->part_g);
+  (void)hipFree(t->dyc);
+  (void)hipFree(t->dyp);
+  (void)hipFree(t->part_u);
   (void)hipFree(t->part_d);
+  (void)hipFree(t->part_w);
   (void)hipFree(t->error_flag);
   delete t;
 }

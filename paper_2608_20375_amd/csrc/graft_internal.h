@@ -14,7 +14,7 @@ constexpr int kMaxK = 64;
 constexpr int kMaxNodes = 1024;
 constexpr int kMaxGrid = 64;
 constexpr int kMaxScoreDim = 64;
-constexpr int kTdesMaxBlocks = 256;
+constexpr int kTdesMaxLossBlocks = 512;
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -252,8 +252,11 @@ struct graft_ctx {
 
 struct graft_tdes {
   graft_tdes_dims dims;
-  float *part_g;           // [kTdesMaxBlocks, 2 E m + L m] block partial gradients
-  double *part_d;          // [kTdesMaxBlocks, 4] scale gradient and loss sums
+  float *dyc;              // [max_groups K + 2 max_pairs, M16] dL/db of the child-tower rows
+  float *dyp;              // [max_groups + 2 max_pairs, M16] dL/da of the parent-tower rows
+  float *part_u;           // depth-embedding gradient partials of the loss blocks
+  double *part_d;          // [kTdesMaxLossBlocks, 4] scale gradient and objective sums
+  float *part_w;           // projection gradient partials of the wgrad blocks
   uint32_t *error_flag;
 };
 
@@ -288,9 +291,16 @@ hipError_t launch_synth_targets(graft_ctx *ctx, int batch, uint64_t seed,
                                 const int32_t *topk_ids, int32_t *target_root,
                                 int32_t *target_node, hipStream_t stream);
 
-// TDES training step: block count for a batch, the instantiated shapes, and
-// the two launches (train_kernel, update_kernel).
-int tdes_blocks(int G, int P);
+// TDES training step: launch sizes for a batch, the instantiated shapes, and
+// the three launches (loss_kernel, wgrad_kernel, update_kernel).
+struct TdesPlan {
+  int loss_blocks, child_blocks, parent_blocks;
+};
+TdesPlan tdes_plan(const graft_tdes_dims &d, int G, int P);
+struct TdesWorkspace {   // element counts of the trainer's buffers
+  int64_t dyc, dyp, part_u, part_d, part_w;
+};
+TdesWorkspace tdes_workspace(const graft_tdes_dims &d);
 bool tdes_shape_supported(int E, int m, int L, int K);
 hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *b,
                             const graft_tdes_hyper *h, int32_t step, float *theta, float *m1,

@@ -3,24 +3,26 @@
 // KL, pairwise margin and class-balanced BCE, summed by eq. tdes-training;
 // AdamW as in the training setup of the experiments).
 //
-// train_kernel: every wave takes a contiguous share of the work items, weighted
-//   by cost (a group of K children costs 1, a tile of 8 pairs 2).  For a group
-//   it gathers the K child embedding rows with 16-byte loads, projects them
-//   through g_child with MFMA (v_mfma_f32_16x16x4_f32: 16 rows x 16 score
-//   dimensions per instruction, g_child staged in LDS), projects the parent
-//   row through g_parent on the VALU, then forms f, both softmaxes over the
-//   children, the KL and BCE terms and dL/df in registers.  The weight
-//   gradient e^T dY is one more MFMA contraction over the rows, accumulated
-//   in per-wave fp32 registers; its embedding operand is re-read (from L1/L2)
-//   in the transposed lane layout the contraction needs.  The rank-1 updates
-//   of four groups' parents share one contraction step.  A pair tile projects
-//   16 parent rows and 16 child rows the same way.  At the end the block sums
-//   its waves' accumulators in a fixed order and writes one partial gradient.
-// update_kernel: sums the block partials in fp64 in block order (so a step is
-//   deterministic), then applies AdamW to every parameter.
+// Rows.  Every edge of the batch contributes a parent-tower row and a
+// child-tower row: the K children and the parent of each group (the parent
+// row is shared by its K edges), and both edges of each pair.  With the
+// towers a = g_p(e_p) + u_d, b = g_c(e_c) + u_d and f = s a.b / sqrt(m), the
+// weight gradients are contractions over rows,
+//   dL/dg_parent = sum over parent rows of e (dL/da)^T,
+//   dL/dg_child  = sum over child rows of e (dL/db)^T.
 //
-// The projections are dense contractions (rows x E x m), so they run on the
-// matrix cores; fp32 MFMA has twice the fp32 VALU rate here.
+// loss_kernel (one wave per group or tile of 8 pairs): gathers the item's
+//   embedding rows (16-byte loads), projects them on MFMA
+//   (v_mfma_f32_16x16x4_f32, 16 rows x 16 score dimensions per instruction;
+//   g_parent and g_child staged in LDS), forms f, the objectives and dL/df,
+//   and writes dL/da, dL/db of every row (fp32, m padded to a multiple of 16)
+//   plus per-block sums of the depth-embedding and scale gradients and of the
+//   objectives.  Few registers per wave: many waves in flight hide the gathers.
+// wgrad_kernel: the two contractions on MFMA, 4 rows per instruction, over
+//   contiguous row chunks (the embedding rows come back from L2 / MALL, 16
+//   bytes per lane); per-block partial gradients.
+// update_kernel: sums every partial in fp64 in a fixed order (a step is
+//   deterministic), then applies AdamW to every parameter.
 #include <cmath>
 
 #include "graft_internal.h"
@@ -28,12 +30,14 @@
 namespace graft {
 namespace {
 
-constexpr int kTrainWaves = 8;
-constexpr int kTrainThreads = kTrainWaves * kWave;
-constexpr int kMaxEM = 4096;          // E * ceil(m / 16) * 16
-constexpr int kMaxLM = 1024;          // L * ceil(m / 16) * 16
-constexpr int kMaxSG = 68;            // LDS row stride of a staged projection
-constexpr int kMaxGs = 4608;          // max E * (M16 + 4) over supported shapes
+constexpr int kLossWaves = 4;
+constexpr int kLossThreads = kLossWaves * kWave;
+constexpr int kGradWaves = 8;
+constexpr int kGradThreads = kGradWaves * kWave;
+constexpr int kGradRowsPerWave = 32;
+constexpr int kGradRows = kGradWaves * kGradRowsPerWave;   // rows per wgrad block
+constexpr int kMaxEM = 4096;          // E * M16, M16 = m rounded up to 16
+constexpr int kMaxLM = 1024;          // L * M16
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
@@ -45,15 +49,18 @@ struct TrainArgs {
   const int32_t *parent, *depth, *child, *target, *pairs;
   const float *logq, *z;
   float c_kl, c_bce, c_pair, gamma, w1;
-  float *part_g;         // [blocks, 2*E*m + L*m]
-  double *part_d;        // [blocks, 4]: ds, sum KL, sum pair, sum BCE
+  float *dyc;            // [G*K + 2P, M16] dL/db of the child-tower rows
+  float *dyp;            // [G + 2P, M16] dL/da of the parent-tower rows
+  float *part_u;         // L*m per loss block (chunked)
+  double *part_d;        // [loss blocks, 4]: ds, sum KL, sum pair, sum BCE
+  float *part_w;         // E*m per child-side then parent-side wgrad block (chunked)
   uint32_t *error_flag;
 };
 
 __device__ __forceinline__ float xorf(float v, int m) {
   return __uint_as_float(xor_lane(__float_as_uint(v), m));
 }
-// sum over the 16 lanes of a row (lanes with equal lane / 16)
+// sum over the 16 lanes of a row of lanes (equal lane / 16)
 __device__ __forceinline__ float sum16(float v) {
   v += xorf(v, 1);
   v += xorf(v, 2);
@@ -61,7 +68,7 @@ __device__ __forceinline__ float sum16(float v) {
   v += xorf(v, 8);
   return v;
 }
-// sum / max over the 4 rows of 16 lanes (lanes with equal lane % 16)
+// sum / max over the 4 rows of lanes (equal lane % 16)
 __device__ __forceinline__ float sum_rows(float v) {
   v += xorf(v, 16);
   v += xorf(v, 32);
@@ -72,10 +79,13 @@ __device__ __forceinline__ float max_rows(float v) {
   v = fmaxf(v, xorf(v, 32));
   return v;
 }
-__device__ __forceinline__ double sum_rows_f64(double v) {
-  v += xor_lane_f64(v, 16);
-  v += xor_lane_f64(v, 32);
-  return v;
+__device__ __forceinline__ float wave_sum(float v) { return sum_rows(sum16(v)); }
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, xorf(v, 1));
+  v = fmaxf(v, xorf(v, 2));
+  v = fmaxf(v, xorf(v, 4));
+  v = fmaxf(v, xorf(v, 8));
+  return max_rows(v);
 }
 // log(1 + e^x) without overflow
 __device__ __forceinline__ float softplus(float x) {
@@ -94,299 +104,247 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
-
-struct alignas(16) WaveScratch {
-  float delta[kMaxK];      // dL/df of a group's rows
-  float f[kMaxK];          // f of a group's rows
-  float dot[kMaxK];        // (g_p + u).(g_c + u) / sqrt(m) of a group's rows
-  float xv[128];           // an E-vector
-  float pend[4][kMaxScoreDim];  // dA of up to four groups awaiting their parents' update
-  int32_t ptok[4];              // their parent tokens
-  int32_t tok[kMaxK];      // a group's child tokens; a pair tile's parent tokens
-  int32_t tok2[16];        // a pair tile's child tokens
-  int32_t dep[16];         // a pair tile's depths
-  float tile[16 * kMaxSG]; // dY of a pair tile, transposed through LDS
-};
-
-struct TrainLds {
-  float gs[2][kMaxGs];                    // g_parent, g_child [E][SG]; later the block sums
-  float us[kMaxLM];                       // u [L][M16]
-  float du[kTrainWaves][kMaxLM];          // per-wave depth-embedding gradients
-  WaveScratch ws[kTrainWaves];
-  double wd[kTrainWaves][4];
-};
-
-template <int NT, int EB>
-struct Acc {
-  v4f c[NT][EB];   // dG_child^T tiles: lane holds n = nt*16 + 4*(lane/16) + i, k = kb*16 + lane%16
-  v4f p[NT][EB];   // dG_parent^T tiles
-};
-
-// plain (cached) loads: the contraction re-reads the same rows right after
 __device__ __forceinline__ float4 ld4(const float *p) {
   return *reinterpret_cast<const float4 *>(p);
 }
 
-// The rank-1 updates e_p dA^T of up to four groups' parents as one
-// contraction step: row q of the step is pending group q (held in LDS).
-template <int NT, int EB>
-__device__ __forceinline__ void flush_parents(const TrainArgs &a, WaveScratch &ws,
-                                              Acc<NT, EB> &acc, int &np) {
-  if (np == 0) return;
-  const int lane = lane_id(), q = lane >> 4, c16 = lane & 15;
-  constexpr int E = EB * 16;
-  const bool live = q < np;
-  const int32_t tk = ws.ptok[q];
-  float av[NT];
+// Block partials are stored chunked, [n / kChunk][blocks][kChunk]: a block
+// writes kChunk consecutive values per chunk and the update reads each chunk
+// of all blocks as one contiguous run.
+constexpr int kChunk = 32;
+__host__ __device__ __forceinline__ int64_t chunked(int i, int blocks, int b) {
+  return (static_cast<int64_t>(i / kChunk) * blocks + b) * kChunk + i % kChunk;
+}
+__host__ __device__ __forceinline__ int64_t chunked_size(int n, int blocks) {
+  return static_cast<int64_t>((n + kChunk - 1) / kChunk) * blocks * kChunk;
+}
+
+// 16 rows of E fp32 embedding entries times a staged projection [E][SG]: lane
+// (q, c16) supplies entries kb*16 + 4q + j of its row (row c16 of the tile);
+// the result holds rows 4q + i, column nt*16 + c16 in component i.
+template <int EB>
+__device__ __forceinline__ void load16(const float *row, bool valid, float4 (&ev)[EB]) {
+  const int q = lane_id() >> 4;
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) av[nt] = live ? ws.pend[q][nt * 16 + c16] : 0.0f;
-  const float *er = a.emb + static_cast<int64_t>(live ? tk : 0) * E + c16;
+  for (int kb = 0; kb < EB; ++kb)
+    ev[kb] = valid ? ld4(row + kb * 16 + 4 * q) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+}
+template <int NT, int EB>
+__device__ __forceinline__ void mma16(const float4 (&ev)[EB], const float *gs, v4f (&y)[NT]) {
+  constexpr int SG = NT * 16 + 4;
+  const int lane = lane_id(), q = lane >> 4, c16 = lane & 15;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) y[nt] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int kb = 0; kb < EB; ++kb) {
-    const float b = live ? er[kb * 16] : 0.0f;
+    const float *gb = gs + (kb * 16 + 4 * q) * SG + c16;
+    const float e4[4] = {ev[kb].x, ev[kb].y, ev[kb].z, ev[kb].w};
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc.p[nt][kb] = mfma(av[nt], b, acc.p[nt][kb]);
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) y[nt] = mfma(e4[j], gb[j * SG + nt * 16], y[nt]);
+    __builtin_amdgcn_sched_barrier(0);   // bounds the LDS reads in flight (registers)
   }
-  np = 0;
 }
-
-// wave-wide (64-lane) reductions
-__device__ __forceinline__ float wave_sum(float v) {
-  v = sum16(v);
-  return sum_rows(v);
-}
-__device__ __forceinline__ float wave_max(float v) {
-  v = fmaxf(v, xorf(v, 1));
-  v = fmaxf(v, xorf(v, 2));
-  v = fmaxf(v, xorf(v, 4));
-  v = fmaxf(v, xorf(v, 8));
-  return max_rows(v);
-}
-
-// E-vector x (in LDS) times a staged projection [E][SG]: lane (q, c16) sums
-// k in [q E/4, (q+1) E/4) for column nt*16 + c16, then the 4 quarters add up.
 template <int NT, int EB>
-__device__ __forceinline__ void matvec(const float *x, const float *gs, float (&out)[NT]) {
-  constexpr int E = EB * 16, SG = NT * 16 + 4;
-  const int lane = lane_id(), q = lane >> 4, c16 = lane & 15;
+__device__ __forceinline__ void project16(const float *row, bool valid, const float *gs, v4f (&y)[NT]) {
   float4 ev[EB];
-#pragma unroll
-  for (int t = 0; t < EB; ++t) ev[t] = *reinterpret_cast<const float4 *>(x + q * (E / 4) + 4 * t);
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    float acc0 = 0.0f;
-    const float *gcol = gs + q * (E / 4) * SG + nt * 16 + c16;
-#pragma unroll
-    for (int t = 0; t < EB; ++t) {
-      acc0 = fmaf(ev[t].x, gcol[(4 * t + 0) * SG], acc0);
-      acc0 = fmaf(ev[t].y, gcol[(4 * t + 1) * SG], acc0);
-      acc0 = fmaf(ev[t].z, gcol[(4 * t + 2) * SG], acc0);
-      acc0 = fmaf(ev[t].w, gcol[(4 * t + 3) * SG], acc0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    out[nt] = sum_rows(acc0);
-  }
+  load16<EB>(row, valid, ev);
+  mma16<NT, EB>(ev, gs, y);
 }
 
-template <int NT, int EB>
-__device__ __forceinline__ void do_group(const TrainArgs &a, TrainLds &s, int wave, int g, float sk,
-                                         float inv_sqrt_m, Acc<NT, EB> &acc, int &np,
-                                         double (&tot)[4]) {
-  constexpr int E = EB * 16, M16 = NT * 16, SG = M16 + 4;
+// LDS of loss_kernel (dynamic): gs0, gs1 [E][SG] | us [L][M16] |
+// du [waves][L][M16] | per wave delta, f, dot [64 each] | wd [waves][4] (double)
+struct LossLds {
+  float *gs0, *gs1, *us, *du, *wsf;
+  double *wd;
+};
+
+__device__ __forceinline__ LossLds loss_lds(char *base, int E, int M16, int L) {
+  LossLds s;
+  const int SG = M16 + 4;
+  float *p = reinterpret_cast<float *>(base);
+  s.gs0 = p;
+  s.gs1 = p + E * SG;
+  s.us = s.gs1 + E * SG;
+  s.du = s.us + L * M16;
+  s.wsf = s.du + kLossWaves * L * M16;
+  s.wd = reinterpret_cast<double *>(s.wsf + kLossWaves * 3 * kMaxK);
+  return s;
+}
+
+template <int NT, int EB, int RT>
+__device__ __forceinline__ void group_item(const TrainArgs &a, const LossLds &s, int wave, int g,
+                                           float sk, float inv_sqrt_m, double (&tot)[4]) {
+  constexpr int E = EB * 16, M16 = NT * 16;
   const int lane = lane_id(), q = lane >> 4, c16 = lane & 15;
   const int K = a.K;
-  const int p = a.parent[g], d = a.depth[g];
   const int64_t gk = static_cast<int64_t>(g) * K;
-  // lane r < K owns child row r for the softmaxes
+  const int p = a.parent[g], d = a.depth[g];
+  // lane r < K owns child row r for the softmaxes; its inputs load early
   const bool own = lane < K;
   const int ctok = own ? a.child[gk + lane] : 0;
+  const float lq = own ? a.logq[gk + lane] : 0.0f;
+  const float zt = own ? a.z[gk + lane] : -INFINITY;
+  const int tgt = a.target[g];
+  float *dyc = a.dyc + gk * M16;
+  float *dyp = a.dyp + static_cast<int64_t>(g) * M16;
   const bool bad = p < 0 || p >= a.V || d < 1 || d > a.L || (own && (ctok < 0 || ctok >= a.V));
   if (__any(bad)) {
+    // dropped: zero rows keep the contractions exact for the rest
+    for (int i = lane; i < K * M16; i += kWave) dyc[i] = 0.0f;
+    if (lane < M16) dyp[lane] = 0.0f;
     if (lane == 0) atomicOr(a.error_flag, 1u);
     return;
   }
-  WaveScratch &ws = s.ws[wave];
+  float *delta = s.wsf + wave * 3 * kMaxK, *fs = delta + kMaxK, *dots = fs + kMaxK;
   const float *us = s.us + (d - 1) * M16;
-  ws.tok[lane] = ctok;
 
-  // parent tower on the VALU
+  // parent tower on the VALU (one row): lane (q, c16) sums entries
+  // kb*16 + 4q + j for column nt*16 + c16, then the 4 rows of lanes add up.
+  // Its loads go out with those of the first child tile.
+  float4 evc0[EB];
   float abar[NT];
-  matvec<NT, EB>(a.emb + static_cast<int64_t>(p) * E, s.gs[0], abar);
+  {
+    float4 evp[EB];
+    load16<EB>(a.emb + static_cast<int64_t>(p) * E, true, evp);
+    load16<EB>(a.emb + static_cast<int64_t>(__shfl(ctok, c16)) * E, c16 < K, evc0);
+    constexpr int SG = M16 + 4;
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) abar[nt] += us[nt * 16 + c16];
-  wave_lds_sync();
-
-  // child tower on MFMA, tiles of 16 rows; f and a.b / sqrt(m) go to LDS
-#pragma unroll 1
-  for (int r0 = 0; r0 < K; r0 += 16) {
-    const int row = r0 + c16;
-    const bool valid = row < K;
-    const float *er = a.emb + static_cast<int64_t>(valid ? ws.tok[row] : 0) * E + 4 * q;
-    float4 ev[EB];
+    for (int nt = 0; nt < NT; ++nt) {
+      float acc0 = 0.0f;
 #pragma unroll
-    for (int kb = 0; kb < EB; ++kb)
-      ev[kb] = valid ? ld4(er + kb * 16) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    v4f bb[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) bb[nt] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int kb = 0; kb < EB; ++kb) {
-      const float *gb = s.gs[1] + (kb * 16 + 4 * q) * SG + c16;
-      const float e4[4] = {ev[kb].x, ev[kb].y, ev[kb].z, ev[kb].w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) bb[nt] = mfma(e4[j], gb[j * SG + nt * 16], bb[nt]);
-      // keep the next block's LDS operands from being hoisted (register budget)
-      __builtin_amdgcn_sched_barrier(0);
+      for (int kb = 0; kb < EB; ++kb) {
+        const float *gcol = s.gs0 + (kb * 16 + 4 * q) * SG + nt * 16 + c16;
+        acc0 = fmaf(evp[kb].x, gcol[0], acc0);
+        acc0 = fmaf(evp[kb].y, gcol[SG], acc0);
+        acc0 = fmaf(evp[kb].z, gcol[2 * SG], acc0);
+        acc0 = fmaf(evp[kb].w, gcol[3 * SG], acc0);
+        __builtin_amdgcn_sched_barrier(0);   // bounds the LDS reads in flight (registers)
+      }
+      abar[nt] = sum_rows(acc0) + us[nt * 16 + c16];
     }
+  }
+
+  // child tower, RT tiles of 16 rows (kept for dL/da)
+  v4f bb[RT][NT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float part = 0.0f;
+  for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) part = fmaf(abar[nt], bb[nt][i] + us[nt * 16 + c16], part);
-      const float sum = sum16(part);
-      const int r = r0 + 4 * q + i;
-      if (c16 == 0 && r < K) {
-        ws.f[r] = sk * sum;
-        ws.dot[r] = sum * inv_sqrt_m;
+    for (int nt = 0; nt < NT; ++nt) bb[rt][nt] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    if (rt * 16 < K) {
+      const int row = rt * 16 + c16;
+      if (rt == 0) {
+        mma16<NT, EB>(evc0, s.gs1, bb[0]);
+      } else {
+        const int tok = __shfl(ctok, row);
+        project16<NT, EB>(a.emb + static_cast<int64_t>(tok) * E, row < K, s.gs1, bb[rt]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float part = 0.0f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          bb[rt][nt][i] += us[nt * 16 + c16];
+          part = fmaf(abar[nt], bb[rt][nt][i], part);
+        }
+        const float sum = sum16(part);
+        const int r = rt * 16 + 4 * q + i;
+        if (c16 == 0 && r < K) {
+          fs[r] = sk * sum;
+          dots[r] = sum * inv_sqrt_m;
+        }
       }
     }
   }
   wave_lds_sync();
 
   // softmaxes over the K children, one row per lane
-  const float f = own ? ws.f[lane] : 0.0f;
-  const float x = own ? a.logq[gk + lane] + f : -INFINITY;
-  const float zt = own ? a.z[gk + lane] : -INFINITY;
-  const float y = own && ctok == a.target[g] ? 1.0f : 0.0f;
-  const float lse_x = [&] {
-    const float mx = wave_max(x);
-    return mx + logf(wave_sum(expf(x - mx)));
-  }();
-  const float lse_z = [&] {
-    const float mz = wave_max(zt);
-    return mz + logf(wave_sum(expf(zt - mz)));
-  }();
-  float delta = 0.0f, kl = 0.0f, bce = 0.0f;
+  const float f = own ? fs[lane] : 0.0f;
+  const float x = own ? lq + f : -INFINITY;
+  const float y = own && ctok == tgt ? 1.0f : 0.0f;
+  const float mx = wave_max(x), mz = wave_max(zt);
+  const float lse_x = mx + logf(wave_sum(own ? expf(x - mx) : 0.0f));
+  const float lse_z = mz + logf(wave_sum(own ? expf(zt - mz) : 0.0f));
+  float dl = 0.0f, kl = 0.0f, bce = 0.0f;
   if (own) {
     const float lpt = zt - lse_z, lpth = x - lse_x;
     const float pt = expf(lpt), pth = expf(lpth);
     const float dbce = -a.w1 * y * sigmoid(-f) + (1.0f - y) * sigmoid(f);
-    delta = a.c_kl * (pth - pt) + a.c_bce * dbce;
+    dl = a.c_kl * (pth - pt) + a.c_bce * dbce;
     kl = pt * (lpt - lpth);
     bce = a.w1 * y * softplus(-f) + (1.0f - y) * softplus(f);
   }
-  ws.delta[lane] = delta;
-  const float sd = wave_sum(delta);
-  tot[0] += static_cast<double>(wave_sum(own ? delta * ws.dot[lane] : 0.0f));
+  delta[lane] = dl;
+  const float sd = wave_sum(dl);
+  tot[0] += static_cast<double>(wave_sum(own ? dl * dots[lane] : 0.0f));
   tot[1] += static_cast<double>(wave_sum(kl));
   tot[3] += static_cast<double>(wave_sum(bce));
   wave_lds_sync();
 
-  // dG_child^T += dB^T E_child, four rows per contraction step; the same rows
-  // also give sum_r delta_r e_r for the parent-side gradient
-  const float *eb = a.emb + c16;
-  float wsum[EB];
+  // dL/db_r = sk delta_r abar (lanes of row q of lanes take rows q, q + 4, ...)
+  for (int r = q; r < K; r += 4) {
+    const float c = sk * delta[r];
 #pragma unroll
-  for (int kb = 0; kb < EB; ++kb) wsum[kb] = 0.0f;
-#pragma unroll 2
-  for (int r0 = 0; r0 < K; r0 += 4) {
-    const int r = r0 + q;
-    const bool valid = r < K;
-    const float dr = valid ? ws.delta[r] : 0.0f;
-    const float *er = eb + static_cast<int64_t>(valid ? ws.tok[r] : 0) * E;
-    float av[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) av[nt] = sk * dr * abar[nt];
-#pragma unroll
-    for (int kb = 0; kb < EB; ++kb) {
-      const float b = valid ? er[kb * 16] : 0.0f;
-      wsum[kb] = fmaf(dr, b, wsum[kb]);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc.c[nt][kb] = mfma(av[nt], b, acc.c[nt][kb]);
-    }
+    for (int nt = 0; nt < NT; ++nt) dyc[r * M16 + nt * 16 + c16] = c * abar[nt];
   }
-  // dL/d(parent tower) = sk (g_child^T sum_r delta_r e_r + u sum_r delta_r)
-#pragma unroll
-  for (int kb = 0; kb < EB; ++kb) {
-    const float v = sum_rows(wsum[kb]);
-    if (q == 0) ws.xv[kb * 16 + c16] = v;
-  }
-  wave_lds_sync();
-  float dA[NT];
-  matvec<NT, EB>(ws.xv, s.gs[1], dA);
+  // dL/da = sk sum_r delta_r bbar_r; the depth embedding gets dL/da + sum_r dL/db_r
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const float un = us[nt * 16 + c16];
-    dA[nt] = sk * (dA[nt] + un * sd);
+    float part = 0.0f;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = rt * 16 + 4 * q + i;
+        part = fmaf(r < K ? delta[r] : 0.0f, bb[rt][nt][i], part);
+      }
+    const float dA = sk * sum_rows(part);
     if (q == 0) {
-      s.du[wave][(d - 1) * M16 + nt * 16 + c16] += dA[nt] + sk * abar[nt] * sd;
-      ws.pend[np][nt * 16 + c16] = dA[nt];   // the parent's rank-1 update waits
+      dyp[nt * 16 + c16] = dA;
+      s.du[(wave * a.L + d - 1) * M16 + nt * 16 + c16] += dA + sk * abar[nt] * sd;
     }
   }
-  if (lane == 0) ws.ptok[np] = p;
   wave_lds_sync();
-  if (++np == 4) flush_parents<NT, EB>(a, ws, acc, np);
 }
 
 template <int NT, int EB>
-__device__ __forceinline__ void do_pairs(const TrainArgs &a, TrainLds &s, int wave, int tile, float sk,
-                         float inv_sqrt_m, Acc<NT, EB> &acc, double (&tot)[4]) {
-  constexpr int E = EB * 16, M16 = NT * 16, SG = M16 + 4;
+__device__ __forceinline__ void pair_item(const TrainArgs &a, const LossLds &s, int wave, int tile,
+                                          float sk, float inv_sqrt_m, double (&tot)[4]) {
+  constexpr int E = EB * 16, M16 = NT * 16;
   const int lane = lane_id(), q = lane >> 4, c16 = lane & 15;
-  WaveScratch &ws = s.ws[wave];
-  // forward rows: edge r = c16 is pair tile*8 + r/2, v+ for even r, v- for odd
+  // edge r = c16 of the tile: pair tile*8 + r/2, v+ for even r, v- for odd
   const int pr = tile * 8 + (c16 >> 1);
-  const int32_t *pe = a.pairs + static_cast<int64_t>(pr < a.P ? pr : 0) * 6 + 3 * (c16 & 1);
   const bool exists = pr < a.P;
+  const int32_t *pe = a.pairs + static_cast<int64_t>(exists ? pr : 0) * 6 + 3 * (c16 & 1);
   const int ptk = exists ? pe[0] : 0, ctk = exists ? pe[1] : 0, dd = exists ? pe[2] : 1;
+  const int64_t pbase = a.G + static_cast<int64_t>(tile) * 16;   // dyp row of edge 0
+  const int64_t cbase = static_cast<int64_t>(a.G) * a.K + static_cast<int64_t>(tile) * 16;
   const bool bad_row = exists && (ptk < 0 || ptk >= a.V || ctk < 0 || ctk >= a.V || dd < 1 || dd > a.L);
   if (__any(bad_row)) {
+    for (int i = lane; i < 16 * M16; i += kWave) {
+      if (tile * 8 + (i / M16) / 2 < a.P) {
+        a.dyp[pbase * M16 + i] = 0.0f;
+        a.dyc[cbase * M16 + i] = 0.0f;
+      }
+    }
     if (lane == 0) atomicOr(a.error_flag, 1u);
     return;
   }
-  if (q == 0) {
-    ws.tok[c16] = ptk;
-    ws.tok2[c16] = ctk;
-    ws.dep[c16] = dd;
-  }
-  // both towers on MFMA: 16 parent rows through g_parent, 16 child rows through g_child
   v4f pa[NT], pb[NT];
-#pragma unroll
-  for (int side = 0; side < 2; ++side) {
-    const float *er = a.emb + static_cast<int64_t>(side == 0 ? ptk : ctk) * E + 4 * q;
-    float4 ev[EB];
-#pragma unroll
-    for (int kb = 0; kb < EB; ++kb)
-      ev[kb] = exists ? ld4(er + kb * 16) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    v4f t[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) t[nt] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int kb = 0; kb < EB; ++kb) {
-      const float e4[4] = {ev[kb].x, ev[kb].y, ev[kb].z, ev[kb].w};
-      const float *gb = s.gs[side] + (kb * 16 + 4 * q) * SG + c16;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) t[nt] = mfma(e4[j], gb[j * SG + nt * 16], t[nt]);
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      if (side == 0)
-        pa[nt] = t[nt];
-      else
-        pb[nt] = t[nt];
-    }
+  {
+    float4 evp[EB], evc[EB];
+    load16<EB>(a.emb + static_cast<int64_t>(ptk) * E, exists, evp);
+    load16<EB>(a.emb + static_cast<int64_t>(ctk) * E, exists, evc);
+    mma16<NT, EB>(evp, s.gs0, pa);
+    mma16<NT, EB>(evc, s.gs1, pb);
   }
-  wave_lds_sync();
-  // rows 4q + i of the output: pair tile*8 + 2q + i/2
-  float f[4], dot[4], delta[4];
+  // output rows 4q + i: pair tile*8 + 2q + i/2
+  float f[4], dot[4], dl[4];
   int drow[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    drow[i] = ws.dep[4 * q + i];
+    drow[i] = __shfl(dd, 4 * q + i);
     const float *u = s.us + (drow[i] - 1) * M16 + c16;
     float part = 0.0f;
 #pragma unroll
@@ -406,182 +364,188 @@ __device__ __forceinline__ void do_pairs(const TrainArgs &a, TrainLds &s, int wa
     const float xm = a.gamma - f[2 * h] + f[2 * h + 1];
     const float t = live ? a.c_pair * sigmoid(xm) : 0.0f;
     loss += live ? softplus(xm) : 0.0f;
-    delta[2 * h] = -t;
-    delta[2 * h + 1] = t;
+    dl[2 * h] = -t;
+    dl[2 * h + 1] = t;
     dsum += -t * dot[2 * h] + t * dot[2 * h + 1];
   }
-  // every lane of a row holds its row's values; summing the 4 rows gives the tile
+  // each lane holds its row of lanes' two pairs: the 4 rows of lanes sum to the tile
   tot[0] += static_cast<double>(sum_rows(dsum));
   tot[2] += static_cast<double>(sum_rows(loss));
-
-  // dY of both towers, depth-embedding gradient (LDS adds: rows of one
-  // instruction may share a depth)
-  float dA[NT][4], dB[NT][4];
+  // dL/da = sk delta bbar, dL/db = sk delta abar; the depth embedding gets both
+  // (LDS adds: rows of one instruction may share a depth)
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * q + i;
+    const bool live = tile * 8 + r / 2 < a.P;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      dA[nt][i] = sk * delta[i] * pb[nt][i];
-      dB[nt][i] = sk * delta[i] * pa[nt][i];
-      atomicAdd(&s.du[wave][(drow[i] - 1) * M16 + nt * 16 + c16], dA[nt][i] + dB[nt][i]);
-    }
-  // parent rows: dG_parent^T += dA^T E_parent, then the child rows
-#pragma unroll
-  for (int side = 0; side < 2; ++side) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        ws.tile[(4 * q + i) * SG + nt * 16 + c16] = side == 0 ? dA[nt][i] : dB[nt][i];
-    wave_lds_sync();
-#pragma unroll
-    for (int r0 = 0; r0 < 16; r0 += 4) {
-      const int r = r0 + q;
-      const int tk = side == 0 ? ws.tok[r] : ws.tok2[r];
-      const float *er = a.emb + static_cast<int64_t>(tk) * E + c16;
-      const bool live = tile * 8 + (r >> 1) < a.P;
-      float av[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) av[nt] = live ? ws.tile[r * SG + nt * 16 + c16] : 0.0f;
-#pragma unroll
-      for (int kb = 0; kb < EB; ++kb) {
-        const float b = live ? er[kb * 16] : 0.0f;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          if (side == 0)
-            acc.p[nt][kb] = mfma(av[nt], b, acc.p[nt][kb]);
-          else
-            acc.c[nt][kb] = mfma(av[nt], b, acc.c[nt][kb]);
-        }
+      const float dA = sk * dl[i] * pb[nt][i], dB = sk * dl[i] * pa[nt][i];
+      if (live) {
+        a.dyp[(pbase + r) * M16 + nt * 16 + c16] = dA;
+        a.dyc[(cbase + r) * M16 + nt * 16 + c16] = dB;
+        atomicAdd(&s.du[(wave * a.L + drow[i] - 1) * M16 + nt * 16 + c16], dA + dB);
       }
     }
-    wave_lds_sync();
   }
 }
 
-template <int NT, int EB>
-__global__ void __launch_bounds__(kTrainThreads)
-train_kernel(TrainArgs a) {
+template <int NT, int EB, int RT>
+__global__ void __launch_bounds__(kLossThreads)
+loss_kernel(TrainArgs a) {
   constexpr int E = EB * 16, M16 = NT * 16, SG = M16 + 4;
-  __shared__ TrainLds s;
+  extern __shared__ __align__(16) char lds_raw[];
+  const LossLds s = loss_lds(lds_raw, E, M16, a.L);
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  const int q = lane >> 4, c16 = lane & 15;
   const int m = a.m, L = a.L;
-  // stage g_parent, g_child (zero columns past m) and u
-  for (int i = tid; i < E * SG; i += kTrainThreads) {
+  for (int i = tid; i < E * SG; i += kLossThreads) {
     const int k = i / SG, n = i % SG;
     const bool in = n < m;
-    s.gs[0][i] = in ? a.theta[k * m + n] : 0.0f;
-    s.gs[1][i] = in ? a.theta[E * m + k * m + n] : 0.0f;
+    s.gs0[i] = in ? a.theta[k * m + n] : 0.0f;
+    s.gs1[i] = in ? a.theta[E * m + k * m + n] : 0.0f;
   }
-  for (int i = tid; i < L * M16; i += kTrainThreads) {
+  for (int i = tid; i < L * M16; i += kLossThreads) {
     const int l = i / M16, n = i % M16;
     s.us[i] = n < m ? a.theta[2 * E * m + l * m + n] : 0.0f;
   }
-  for (int i = tid; i < kTrainWaves * kMaxLM; i += kTrainThreads) (&s.du[0][0])[i] = 0.0f;
+  for (int i = tid; i < kLossWaves * L * M16; i += kLossThreads) s.du[i] = 0.0f;
   const float inv_sqrt_m = 1.0f / sqrtf(static_cast<float>(m));
   const float sk = a.theta[2 * E * m + L * m] * inv_sqrt_m;
   __syncthreads();
 
-  Acc<NT, EB> acc;
+  double tot[4] = {0.0, 0.0, 0.0, 0.0};
+  const int T = (a.P + 7) / 8;
+  const int items = a.G + T;
+  const int W = gridDim.x * kLossWaves;
+  for (int it = blockIdx.x * kLossWaves + wave; it < items; it += W) {
+    if (it < a.G)
+      group_item<NT, EB, RT>(a, s, wave, it, sk, inv_sqrt_m, tot);
+    else
+      pair_item<NT, EB>(a, s, wave, it - a.G, sk, inv_sqrt_m, tot);
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s.wd[wave * 4 + j] = tot[j];
+  }
+  __syncthreads();
+  for (int i = tid; i < L * m; i += kLossThreads) {
+    const int l = i / m, n = i % m;
+    float v = 0.0f;
+    for (int wv = 0; wv < kLossWaves; ++wv) v += s.du[(wv * L + l) * M16 + n];
+    a.part_u[chunked(i, gridDim.x, blockIdx.x)] = v;
+  }
+  if (tid < 4) {
+    double v = 0.0;
+    for (int wv = 0; wv < kLossWaves; ++wv) v += s.wd[wv * 4 + tid];
+    a.part_d[static_cast<int64_t>(blockIdx.x) * 4 + tid] = v;
+  }
+}
+
+// Token of row `row` of one side: child side = the children of the groups,
+// then the child of every pair edge; parent side = the parents of the groups,
+// then the parent of every pair edge (edge 2i is v+ of pair i, 2i + 1 its v-).
+__device__ __forceinline__ int row_token(const TrainArgs &a, int side, int64_t row) {
+  const int64_t first = side == 0 ? static_cast<int64_t>(a.G) * a.K : a.G;
+  if (row < first) return side == 0 ? a.child[row] : a.parent[row];
+  const int64_t e = row - first;
+  return a.pairs[(e >> 1) * 6 + 3 * (e & 1) + (side == 0 ? 1 : 0)];
+}
+
+// dL/dg = sum over the rows of one side of e_row (dL/dy_row)^T, 4 rows per
+// instruction.  Lane (q, c16) loads 16 bytes of embedding row 4s + q,
+// entries 64h + 4 c16 + j, so tile (nt, 4h + j) of the transposed gradient
+// holds n = nt*16 + 4q + i (component i), k = 64h + 4 c16 + j.
+template <int NT, int EB>
+__global__ void __launch_bounds__(kGradThreads)
+wgrad_kernel(TrainArgs a, int child_blocks) {
+  constexpr int E = EB * 16, M16 = NT * 16, KH = (E + 63) / 64;
+  __shared__ float red[kMaxEM];
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int q = lane >> 4, c16 = lane & 15;
+  const int side = blockIdx.x < child_blocks ? 0 : 1;
+  const int blk = side == 0 ? blockIdx.x : blockIdx.x - child_blocks;
+  const int64_t rows = side == 0 ? static_cast<int64_t>(a.G) * a.K + 2 * static_cast<int64_t>(a.P)
+                                 : static_cast<int64_t>(a.G) + 2 * static_cast<int64_t>(a.P);
+  const float *dy = side == 0 ? a.dyc : a.dyp;
+  v4f acc[NT][4 * KH];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int kb = 0; kb < EB; ++kb) acc.c[nt][kb] = acc.p[nt][kb] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-  int np = 0;
-  double tot[4] = {0.0, 0.0, 0.0, 0.0};
-
-  // cost-weighted contiguous share: groups cost 1, pair tiles 2
-  const int64_t T = (a.P + 7) / 8;
-  const int64_t C = static_cast<int64_t>(a.G) + 2 * T;
-  const int64_t W = static_cast<int64_t>(gridDim.x) * kTrainWaves;
-  const int64_t w = static_cast<int64_t>(blockIdx.x) * kTrainWaves + wave;
-  const int64_t lo = w * C / W, hi = (w + 1) * C / W;
-  for (int64_t g = lo; g < hi && g < a.G; ++g)
-    do_group<NT, EB>(a, s, wave, static_cast<int>(g), sk, inv_sqrt_m, acc, np, tot);
-  flush_parents<NT, EB>(a, s.ws[wave], acc, np);
-  const int64_t t0 = lo > a.G ? (lo - a.G + 1) / 2 : 0;
-  const int64_t t1 = hi > a.G ? (hi - a.G + 1) / 2 : 0;
-  for (int64_t t = t0; t < t1 && t < T; ++t)
-    do_pairs<NT, EB>(a, s, wave, static_cast<int>(t), sk, inv_sqrt_m, acc, tot);
-
-  if (lane == 0) {
+    for (int t = 0; t < 4 * KH; ++t) acc[nt][t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  const int64_t r0 = static_cast<int64_t>(blk) * kGradRows + wave * kGradRowsPerWave;
+  // the tokens of the wave's rows, one per lane, in one round trip
+  int mytok = -1;
+  if (lane < kGradRowsPerWave && r0 + lane < rows) mytok = row_token(a, side, r0 + lane);
+  const bool kin = 4 * c16 < E;   // E = 32 uses half the lanes of a 64-entry block
+#pragma unroll 4
+  for (int st = 0; st < kGradRowsPerWave; st += 4) {
+    const int64_t r = r0 + st + q;
+    const int tok = __shfl(mytok, st + q);
+    const bool live = r < rows && tok >= 0 && tok < a.V;
+    const float *er = a.emb + static_cast<int64_t>(live ? tok : 0) * E + 4 * c16;
+    const float *yr = dy + (live ? r : 0) * M16 + c16;
+    float av[NT];
+    float4 ev[KH];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) s.wd[wave][j] = tot[j];
+    for (int nt = 0; nt < NT; ++nt) av[nt] = live ? yr[nt * 16] : 0.0f;
+#pragma unroll
+    for (int h = 0; h < KH; ++h)
+      ev[h] = live && kin ? ld4(er + 64 * h) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int h = 0; h < KH; ++h) {
+        acc[nt][4 * h + 0] = mfma(av[nt], ev[h].x, acc[nt][4 * h + 0]);
+        acc[nt][4 * h + 1] = mfma(av[nt], ev[h].y, acc[nt][4 * h + 1]);
+        acc[nt][4 * h + 2] = mfma(av[nt], ev[h].z, acc[nt][4 * h + 2]);
+        acc[nt][4 * h + 3] = mfma(av[nt], ev[h].w, acc[nt][4 * h + 3]);
+      }
   }
-  __syncthreads();
-  // block sum of the waves' accumulators, in wave order: [child | parent] x [n][k]
-  float *red = &s.gs[0][0];
-  for (int wv = 0; wv < kTrainWaves; ++wv) {
-    if (wave == wv) {
+  // block sum in wave order into red[n][k] (one wave at a time measured faster
+  // than four LDS slots added pairwise)
+  for (int wv = 0; wv < kGradWaves; ++wv) {
+    if (wave == wv && kin) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
+        for (int t = 0; t < 4 * KH; ++t)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int idx = (nt * 16 + 4 * q + i) * E + kb * 16 + c16;
-            red[idx] = (wv ? red[idx] : 0.0f) + acc.c[nt][kb][i];
-            red[M16 * E + idx] = (wv ? red[M16 * E + idx] : 0.0f) + acc.p[nt][kb][i];
+            const int k = 64 * (t / 4) + 4 * c16 + (t % 4);
+            const int idx = (nt * 16 + 4 * q + i) * E + k;
+            if (k < E) red[idx] = (wv ? red[idx] : 0.0f) + acc[nt][t][i];
           }
     }
     __syncthreads();
   }
-  const int n_g = 2 * E * m + L * m;
-  float *out = a.part_g + static_cast<int64_t>(blockIdx.x) * n_g;
-  for (int i = tid; i < n_g; i += kTrainThreads) {
-    float v;
-    if (i < 2 * E * m) {
-      const int kind = i / (E * m), r = i % (E * m), k = r / m, n = r % m;
-      v = red[(kind == 0 ? M16 * E : 0) + n * E + k];
-    } else {
-      const int r = i - 2 * E * m, l = r / m, n = r % m;
-      v = 0.0f;
-      for (int wv = 0; wv < kTrainWaves; ++wv) v += s.du[wv][l * M16 + n];
-    }
-    out[i] = v;
-  }
-  if (tid < 4) {
-    double v = 0.0;
-    for (int wv = 0; wv < kTrainWaves; ++wv) v += s.wd[wv][tid];
-    a.part_d[static_cast<int64_t>(blockIdx.x) * 4 + tid] = v;
+  const int m = a.m, em = E * m;
+  const int nb = side == 0 ? child_blocks : gridDim.x - child_blocks;
+  float *out = a.part_w + (side == 0 ? 0 : chunked_size(em, child_blocks));
+  for (int i = tid; i < em; i += kGradThreads) {
+    const int idx = (i % m) * E + i / m;
+    const float v = red[idx];
+    out[chunked(i, nb, blk)] = v;
   }
 }
 
 struct UpdateArgs {
   float *theta, *m1, *m2, *grad_out;
-  const float *part_g;
+  const float *part_u, *part_w;
   const double *part_d;
   double *loss;
-  int n_params, n_g, blocks, G, P, K;
+  int E, m, L, n_params, loss_blocks, child_blocks, parent_blocks, G, P, K;
   double lr, wd, beta1, beta2, eps, bc1, bc2;
   double lambda_kl, lambda_pair, lambda_bce;
 };
 
-__global__ void __launch_bounds__(256) update_kernel(UpdateArgs u) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i == 0 && u.loss) {
-    double kl = 0.0, pr = 0.0, bce = 0.0;
-    for (int b = 0; b < u.blocks; ++b) {
-      kl += u.part_d[b * 4 + 1];
-      pr += u.part_d[b * 4 + 2];
-      bce += u.part_d[b * 4 + 3];
-    }
-    kl = u.G ? kl / u.G : 0.0;
-    pr = u.P ? pr / u.P : 0.0;
-    bce = u.G ? bce / (static_cast<double>(u.G) * u.K) : 0.0;
-    u.loss[0] = u.lambda_kl * kl + u.lambda_pair * pr + u.lambda_bce * bce;
-    u.loss[1] = kl;
-    u.loss[2] = pr;
-    u.loss[3] = bce;
-  }
-  if (i >= u.n_params) return;
-  double g = 0.0;
-  if (i < u.n_g) {
-    for (int b = 0; b < u.blocks; ++b) g += static_cast<double>(u.part_g[static_cast<int64_t>(b) * u.n_g + i]);
-  } else {
-    for (int b = 0; b < u.blocks; ++b) g += u.part_d[b * 4];
-  }
+// Block r < 2 cw + cu (cw, cu: chunks of E*m and L*m) updates the kChunk
+// parameters of one chunk of g_parent, g_child or u: thread (slice, o) sums
+// blocks slice, slice + kUpdSlices, ... of parameter o, then the slices add
+// in order.  The last block does the scale and the objectives with fixed-order
+// tree sums.  Every sum is fp64 and deterministic.
+constexpr int kUpdSlices = 32;
+constexpr int kUpdThreads = kChunk * kUpdSlices;
+
+__device__ __forceinline__ void adamw(const UpdateArgs &u, int i, double g) {
   if (u.grad_out) u.grad_out[i] = static_cast<float>(g);
   double th = static_cast<double>(u.theta[i]) * (1.0 - u.lr * u.wd);
   const double m1 = u.beta1 * static_cast<double>(u.m1[i]) + (1.0 - u.beta1) * g;
@@ -592,42 +556,127 @@ __global__ void __launch_bounds__(256) update_kernel(UpdateArgs u) {
   u.m2[i] = static_cast<float>(m2);
 }
 
+__global__ void __launch_bounds__(kUpdThreads) update_kernel(UpdateArgs u) {
+  __shared__ double red[kUpdSlices][kChunk];
+  __shared__ double tree[4][kTdesMaxLossBlocks];
+  const int tid = threadIdx.x;
+  const int em = u.E * u.m, lm = u.L * u.m;
+  const int cw = (em + kChunk - 1) / kChunk, cu = (lm + kChunk - 1) / kChunk;
+  const int r = blockIdx.x;
+  if (r < 2 * cw + cu) {
+    const int o = tid % kChunk, sl = tid / kChunk;
+    const float *src;
+    int nb, c, base, n;
+    if (r < cw) {            // g_parent: parent-side wgrad blocks
+      src = u.part_w + chunked_size(em, u.child_blocks);
+      nb = u.parent_blocks, c = r, base = 0, n = em;
+    } else if (r < 2 * cw) { // g_child: child-side wgrad blocks
+      src = u.part_w;
+      nb = u.child_blocks, c = r - cw, base = em, n = em;
+    } else {                 // depth embedding: loss blocks
+      src = u.part_u;
+      nb = u.loss_blocks, c = r - 2 * cw, base = 2 * em, n = lm;
+    }
+    const float *run = src + static_cast<int64_t>(c) * nb * kChunk + o;
+    double g = 0.0;
+#pragma unroll 8
+    for (int b = sl; b < nb; b += kUpdSlices) g += static_cast<double>(run[static_cast<int64_t>(b) * kChunk]);
+    red[sl][o] = g;
+    __syncthreads();
+    const int i = c * kChunk + o;
+    if (sl != 0 || i >= n) return;
+    g = 0.0;
+    for (int k = 0; k < kUpdSlices; ++k) g += red[k][o];
+    adamw(u, base + i, g);
+    return;
+  }
+  // scale gradient and objective sums: loss block t in thread t, pairwise tree
+  for (int c = 0; c < 4; ++c)
+    for (int t = tid; t < kTdesMaxLossBlocks; t += kUpdThreads)
+      tree[c][t] = t < u.loss_blocks ? u.part_d[t * 4 + c] : 0.0;
+  __syncthreads();
+  for (int half = kTdesMaxLossBlocks / 2; half > 0; half >>= 1) {
+    for (int t = tid; t < 4 * half; t += kUpdThreads) tree[t / half][t % half] += tree[t / half][t % half + half];
+    __syncthreads();
+  }
+  if (tid != 0) return;
+  adamw(u, u.n_params - 1, tree[0][0]);
+  if (u.loss) {
+    const double kl = u.G ? tree[1][0] / u.G : 0.0;
+    const double pr = u.P ? tree[2][0] / u.P : 0.0;
+    const double bce = u.G ? tree[3][0] / (static_cast<double>(u.G) * u.K) : 0.0;
+    u.loss[0] = u.lambda_kl * kl + u.lambda_pair * pr + u.lambda_bce * bce;
+    u.loss[1] = kl;
+    u.loss[2] = pr;
+    u.loss[3] = bce;
+  }
+}
+
+size_t loss_lds_bytes(int E, int M16, int L) {
+  return sizeof(float) * (2 * static_cast<size_t>(E) * (M16 + 4) + static_cast<size_t>(L) * M16 +
+                          static_cast<size_t>(kLossWaves) * L * M16 + kLossWaves * 3 * kMaxK) +
+         sizeof(double) * kLossWaves * 4;
+}
+
 template <int NT, int EB>
-bool launch_train_t(const TrainArgs &a, int nt, int eb, int blocks, hipStream_t stream) {
+bool launch_t(const TrainArgs &a, int nt, int eb, int loss_blocks, int child_blocks,
+              int grad_blocks, hipStream_t stream) {
   if (nt != NT || eb != EB) return false;
-  hipLaunchKernelGGL((train_kernel<NT, EB>), dim3(blocks), dim3(kTrainThreads), 0, stream, a);
+  const size_t lds = loss_lds_bytes(EB * 16, NT * 16, a.L);
+  // child tiles of 16 rows per group: K <= 16, 32 or 64
+  if (a.K <= 16)
+    hipLaunchKernelGGL((loss_kernel<NT, EB, 1>), dim3(loss_blocks), dim3(kLossThreads), lds, stream, a);
+  else if (a.K <= 32)
+    hipLaunchKernelGGL((loss_kernel<NT, EB, 2>), dim3(loss_blocks), dim3(kLossThreads), lds, stream, a);
+  else
+    hipLaunchKernelGGL((loss_kernel<NT, EB, 4>), dim3(loss_blocks), dim3(kLossThreads), lds, stream, a);
+  if (grad_blocks > 0)
+    hipLaunchKernelGGL((wgrad_kernel<NT, EB>), dim3(grad_blocks), dim3(kGradThreads), 0, stream, a,
+                       child_blocks);
   return true;
 }
 
-// the instantiated shapes: E in {32, 64, 128} with E * ceil(m/16) * 16 <= 4096
-bool dispatch_train(const TrainArgs &a, int nt, int eb, int blocks, hipStream_t stream) {
-  return launch_train_t<1, 2>(a, nt, eb, blocks, stream) ||
-         launch_train_t<1, 4>(a, nt, eb, blocks, stream) ||
-         launch_train_t<1, 8>(a, nt, eb, blocks, stream) ||
-         launch_train_t<2, 2>(a, nt, eb, blocks, stream) ||
-         launch_train_t<2, 4>(a, nt, eb, blocks, stream) ||
-         launch_train_t<2, 8>(a, nt, eb, blocks, stream) ||
-         launch_train_t<3, 2>(a, nt, eb, blocks, stream) ||
-         launch_train_t<3, 4>(a, nt, eb, blocks, stream) ||
-         launch_train_t<4, 2>(a, nt, eb, blocks, stream) ||
-         launch_train_t<4, 4>(a, nt, eb, blocks, stream);
+// the instantiated shapes: E in {32, 64, 128} with E * M16 <= 4096
+bool dispatch(const TrainArgs &a, int nt, int eb, int lb, int cb, int gb, hipStream_t st) {
+  return launch_t<1, 2>(a, nt, eb, lb, cb, gb, st) || launch_t<1, 4>(a, nt, eb, lb, cb, gb, st) ||
+         launch_t<1, 8>(a, nt, eb, lb, cb, gb, st) || launch_t<2, 2>(a, nt, eb, lb, cb, gb, st) ||
+         launch_t<2, 4>(a, nt, eb, lb, cb, gb, st) || launch_t<2, 8>(a, nt, eb, lb, cb, gb, st) ||
+         launch_t<3, 2>(a, nt, eb, lb, cb, gb, st) || launch_t<3, 4>(a, nt, eb, lb, cb, gb, st) ||
+         launch_t<4, 2>(a, nt, eb, lb, cb, gb, st) || launch_t<4, 4>(a, nt, eb, lb, cb, gb, st);
 }
 
 }  // namespace
 
-int tdes_blocks(int G, int P) {
-  const int64_t cost = static_cast<int64_t>(G) + 2 * ((static_cast<int64_t>(P) + 7) / 8);
-  int64_t b = (cost + 2 * kTrainWaves - 1) / (2 * kTrainWaves);   // >= 2 items per wave
-  if (b < 1) b = 1;
-  if (b > kTdesMaxBlocks) b = kTdesMaxBlocks;
-  return static_cast<int>(b);
+TdesPlan tdes_plan(const graft_tdes_dims &d, int G, int P) {
+  TdesPlan p;
+  const int64_t items = static_cast<int64_t>(G) + (static_cast<int64_t>(P) + 7) / 8;
+  const int64_t lb = (items + 2 * kLossWaves - 1) / (2 * kLossWaves);   // about 2 items per wave
+  p.loss_blocks = static_cast<int>(lb < 1 ? 1 : lb > kTdesMaxLossBlocks ? kTdesMaxLossBlocks : lb);
+  const int64_t rc = static_cast<int64_t>(G) * d.top_k + 2 * static_cast<int64_t>(P);
+  const int64_t rp = static_cast<int64_t>(G) + 2 * static_cast<int64_t>(P);
+  p.child_blocks = static_cast<int>((rc + kGradRows - 1) / kGradRows);
+  p.parent_blocks = static_cast<int>((rp + kGradRows - 1) / kGradRows);
+  return p;
+}
+
+TdesWorkspace tdes_workspace(const graft_tdes_dims &d) {
+  const TdesPlan most = tdes_plan(d, d.max_groups, d.max_pairs);
+  const int64_t m16 = (d.score_dim + 15) / 16 * 16;
+  TdesWorkspace w;
+  w.dyc = (static_cast<int64_t>(d.max_groups) * d.top_k + 2 * static_cast<int64_t>(d.max_pairs)) * m16;
+  w.dyp = (static_cast<int64_t>(d.max_groups) + 2 * static_cast<int64_t>(d.max_pairs)) * m16;
+  w.part_u = chunked_size(d.num_pos * d.score_dim, kTdesMaxLossBlocks);
+  w.part_d = 4 * static_cast<int64_t>(kTdesMaxLossBlocks);
+  w.part_w = chunked_size(d.emb_dim * d.score_dim, most.child_blocks) +
+             chunked_size(d.emb_dim * d.score_dim, most.parent_blocks);
+  return w;
 }
 
 bool tdes_shape_supported(int E, int m, int L, int K) {
   const int m16 = (m + 15) / 16 * 16;
   const bool e_ok = E == 32 || E == 64 || E == 128;
   return e_ok && m >= 1 && m <= kMaxScoreDim && E * m16 <= kMaxEM && L >= 1 && L * m16 <= kMaxLM &&
-         K >= 1 && K <= kMaxK && E * (m16 + 4) <= kMaxGs;
+         K >= 1 && K <= kMaxK && loss_lds_bytes(E, m16, L) <= 64 * 1024;
 }
 
 hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *b,
@@ -636,7 +685,7 @@ hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_ba
   const graft_tdes_dims &d = t->dims;
   const int E = d.emb_dim, m = d.score_dim, L = d.num_pos, K = d.top_k;
   const int G = b->n_groups, P = b->n_pairs;
-  const int blocks = tdes_blocks(G, P);
+  const TdesPlan plan = tdes_plan(d, G, P);
   TrainArgs a;
   a.emb = emb;
   a.theta = theta;
@@ -659,10 +708,15 @@ hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_ba
   a.c_pair = P ? static_cast<float>(static_cast<double>(h->lambda_pair) / P) : 0.0f;
   a.gamma = h->gamma;
   a.w1 = h->w1;
-  a.part_g = t->part_g;
+  a.dyc = t->dyc;
+  a.dyp = t->dyp;
+  a.part_u = t->part_u;
   a.part_d = t->part_d;
+  a.part_w = t->part_w;
   a.error_flag = t->error_flag;
-  if (!dispatch_train(a, (m + 15) / 16, E / 16, blocks, stream)) return hipErrorInvalidValue;
+  const int grad_blocks = plan.child_blocks + plan.parent_blocks;
+  if (!dispatch(a, (m + 15) / 16, E / 16, plan.loss_blocks, plan.child_blocks, grad_blocks, stream))
+    return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   UpdateArgs u;
@@ -670,12 +724,17 @@ hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_ba
   u.m1 = m1;
   u.m2 = m2;
   u.grad_out = grad;
-  u.part_g = t->part_g;
+  u.part_u = t->part_u;
+  u.part_w = t->part_w;
   u.part_d = t->part_d;
   u.loss = loss;
+  u.E = E;
+  u.m = m;
+  u.L = L;
   u.n_params = 2 * E * m + L * m + 1;
-  u.n_g = 2 * E * m + L * m;
-  u.blocks = blocks;
+  u.loss_blocks = plan.loss_blocks;
+  u.child_blocks = plan.child_blocks;
+  u.parent_blocks = plan.parent_blocks;
   u.G = G;
   u.P = P;
   u.K = K;
@@ -689,7 +748,8 @@ hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_ba
   u.lambda_kl = h->lambda_kl;
   u.lambda_pair = h->lambda_pair;
   u.lambda_bce = h->lambda_bce;
-  hipLaunchKernelGGL(update_kernel, dim3((u.n_params + 255) / 256), dim3(256), 0, stream, u);
+  const int blocks = 2 * ((E * m + kChunk - 1) / kChunk) + (L * m + kChunk - 1) / kChunk + 1;
+  hipLaunchKernelGGL(update_kernel, dim3(blocks), dim3(kUpdThreads), 0, stream, u);
   return hipGetLastError();
 }
 
