@@ -349,8 +349,8 @@ GRAFT_API int64_t graft_tdes_param_count(const graft_tdes_dims *dims /* host */)
 /* One training step on `stream`: the objective and its gradient at theta for
  * the batch, then AdamW (decoupled weight decay on every parameter, bias
  * corrections for step `step` >= 1) updating theta, adam_m and adam_v in place
- * (device [param_count] fp32; the moments start at zero).  emb [V, E] fp32,
- * 16-byte aligned, frozen.  loss (device, 4 doubles: L, L_KL, L_pair, L_BCE at
+ * (device [param_count] fp32, theta 16-byte aligned; the moments start at
+ * zero).  emb [V, E] fp32, 16-byte aligned, frozen.  loss (device, 4 doubles: L, L_KL, L_pair, L_BCE at
  * theta before the update) and grad (device [param_count] fp32: dL/dtheta) may
  * be NULL.  The step is deterministic: partial gradients are summed in a
  * fixed order. */

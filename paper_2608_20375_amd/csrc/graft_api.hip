@@ -535,8 +535,8 @@ int graft_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *b,
     return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: a group array is NULL");
   if (b->n_pairs > 0 && !b->pairs)
     return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: pairs is NULL");
-  if (reinterpret_cast<uintptr_t>(emb) % 16 != 0)
-    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: emb must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(emb) % 16 != 0 || reinterpret_cast<uintptr_t>(theta) % 16 != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: emb and theta must be 16-byte aligned");
   if (step < 1) return fail(GRAFT_ERR_INVALID_ARG, "graft_tdes_step: step must be >= 1");
   const float hv[10] = {h->lambda_kl, h->lambda_pair, h->lambda_bce, h->gamma, h->w1,
                         h->lr, h->weight_decay, h->beta1, h->beta2, h->eps};

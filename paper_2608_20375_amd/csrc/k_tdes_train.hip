@@ -143,7 +143,6 @@ __device__ __forceinline__ void mma16(const float4 (&ev)[EB], const float *gs, v
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) y[nt] = mfma(e4[j], gb[j * SG + nt * 16], y[nt]);
-    __builtin_amdgcn_sched_barrier(0);   // bounds the LDS reads in flight (registers)
   }
 }
 template <int NT, int EB>
@@ -220,7 +219,6 @@ __device__ __forceinline__ void group_item(const TrainArgs &a, const LossLds &s,
         acc0 = fmaf(evp[kb].y, gcol[SG], acc0);
         acc0 = fmaf(evp[kb].z, gcol[2 * SG], acc0);
         acc0 = fmaf(evp[kb].w, gcol[3 * SG], acc0);
-        __builtin_amdgcn_sched_barrier(0);   // bounds the LDS reads in flight (registers)
       }
       abar[nt] = sum_rows(acc0) + us[nt * 16 + c16];
     }
@@ -397,11 +395,41 @@ loss_kernel(TrainArgs a) {
   const LossLds s = loss_lds(lds_raw, E, M16, a.L);
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int m = a.m, L = a.L;
-  for (int i = tid; i < E * SG; i += kLossThreads) {
-    const int k = i / SG, n = i % SG;
-    const bool in = n < m;
-    s.gs0[i] = in ? a.theta[k * m + n] : 0.0f;
-    s.gs1[i] = in ? a.theta[E * m + k * m + n] : 0.0f;
+  // stage g_parent, g_child as [E][SG] (columns m.. zero): with m a multiple
+  // of 4 every thread's float4 loads go out together
+  if (m % 4 == 0) {
+    const int n4 = E * m / 4;
+    for (int i = tid; i < E * SG; i += kLossThreads) {
+      const int n = i % SG;
+      if (n >= m) s.gs0[i] = s.gs1[i] = 0.0f;
+    }
+    constexpr int kPer = (E * M16 / 4 + kLossThreads - 1) / kLossThreads;
+    float4 v0[kPer], v1[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int v = tid + j * kLossThreads;
+      if (v < n4) {
+        v0[j] = ld4(a.theta + 4 * v);
+        v1[j] = ld4(a.theta + E * m + 4 * v);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int v = tid + j * kLossThreads;
+      if (v < n4) {
+        const int k = 4 * v / m, n = 4 * v % m;
+        float *d0 = s.gs0 + k * SG + n, *d1 = s.gs1 + k * SG + n;
+        d0[0] = v0[j].x, d0[1] = v0[j].y, d0[2] = v0[j].z, d0[3] = v0[j].w;
+        d1[0] = v1[j].x, d1[1] = v1[j].y, d1[2] = v1[j].z, d1[3] = v1[j].w;
+      }
+    }
+  } else {
+    for (int i = tid; i < E * SG; i += kLossThreads) {
+      const int k = i / SG, n = i % SG;
+      const bool in = n < m;
+      s.gs0[i] = in ? a.theta[k * m + n] : 0.0f;
+      s.gs1[i] = in ? a.theta[E * m + k * m + n] : 0.0f;
+    }
   }
   for (int i = tid; i < L * M16; i += kLossThreads) {
     const int l = i / M16, n = i % M16;
