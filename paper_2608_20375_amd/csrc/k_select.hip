@@ -149,10 +149,44 @@ __device__ int block_scan(SelMem &s, int32_t *data, int n) {
   return total;
 }
 
-static_assert(kBins == 32 * kWave, "one run of 32 bins per lane of a wave");
-// Histogram slot of a bin: bin 32 l + j of lane l's run is stored at j * 64 + l,
-// so the scan's reads (lane l, run position j) hit consecutive words.
-__device__ __forceinline__ int hslot(int bin) { return ((bin & 31) << 6) | (bin >> 5); }
+constexpr int kBinsPer = kBins / kSelThreads;   // bins per thread in the scan
+static_assert(kBins == kBinsPer * kSelThreads && kBinsPer == 4, "4 bins per thread");
+// Histogram slot of a bin: bin 4 t + j of thread t's run is stored at
+// j * kSelThreads + t, so the scan's reads (thread t, run position j) hit
+// consecutive words.
+__device__ __forceinline__ int hslot(int bin) { return ((bin & 3) << 9) | (bin >> 2); }
+
+// The bin holding the n_keep-th entry (bins in descending score order): every
+// thread scans its 4 bins and clears them, the waves' totals are combined in
+// LDS, and the one thread whose run holds the n_keep-th entry records the bin
+// (kBstar), the count before it (kA) and its own count (kBcnt).  Ends with a
+// barrier; hist is left cleared.
+__device__ __forceinline__ void hist_boundary(SelMem &s, int n_keep) {
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  int c[kBinsPer], sum = 0;
+#pragma unroll
+  for (int j = 0; j < kBinsPer; ++j) {
+    c[j] = s.u.b.hist[j * kSelThreads + tid];
+    sum += c[j];
+  }
+#pragma unroll
+  for (int j = 0; j < kBinsPer; ++j) s.u.b.hist[j * kSelThreads + tid] = 0;
+  const int inc = wave_incl_scan(sum);
+  if (lane == kWave - 1) s.wsum[wave] = inc;
+  __syncthreads();
+  int run = inc - sum;
+  for (int w = 0; w < wave; ++w) run += s.wsum[w];
+#pragma unroll
+  for (int j = 0; j < kBinsPer; ++j) {
+    if (run < n_keep && n_keep <= run + c[j]) {
+      s.sc[kBstar] = tid * kBinsPer + j;
+      s.sc[kA] = run;
+      s.sc[kBcnt] = c[j];
+    }
+    run += c[j];
+  }
+  __syncthreads();
+}
 
 __device__ __forceinline__ int score_bin(double v, double hi, double scale) {
   const double f = (hi - v) * scale;
@@ -172,35 +206,12 @@ __device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, do
     const int bin = score_bin(s.p_score[i], hi, scale);
     if (live) atomicAdd(&s.u.b.hist[hslot(bin)], 1);
   }
-  __syncthreads();
-  // wave 0: the bin holding the n_keep-th entry (bins are in descending score
-  // order), then clears the histogram for the next selection
-  if (wave == 0) {
-    constexpr int kPer = kBins / kWave;
-    int c[kPer], sum = 0;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      c[j] = s.u.b.hist[j * kWave + lane];
-      sum += c[j];
-    }
-    int run = wave_incl_scan(sum) - sum;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      if (run < n_keep && n_keep <= run + c[j]) {
-        s.sc[kBstar] = lane * kPer + j;
-        s.sc[kA] = run;
-        s.sc[kBcnt] = c[j];
-      }
-      run += c[j];
-    }
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) s.u.b.hist[j * kWave + lane] = 0;
-    if (lane == 0) {
-      s.sc[kG] = 0;
-      s.thkey = ~0ull;
-    }
+  if (tid == 0) {
+    s.sc[kG] = 0;
+    s.thkey = ~0ull;
   }
   __syncthreads();
+  hist_boundary(s, n_keep);
   // entries past the boundary bin die.  When the whole boundary bin is kept,
   // theta is its smallest score; otherwise its members are listed and ranked.
   const int bstar = s.sc[kBstar], need = n_keep - s.sc[kA];
@@ -414,24 +425,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
       }
   }
   __syncthreads();
-  if (wave == 0) {
-    constexpr int kPer = kBins / kWave;
-    int c[kPer], sum = 0;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      c[j] = s.u.b.hist[j * kWave + lane];
-      sum += c[j];
-    }
-    int run = wave_incl_scan(sum) - sum;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      if (run < n_keep && n_keep <= run + c[j]) s.sc[kBstar] = lane * kPer + j;
-      run += c[j];
-    }
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) s.u.b.hist[j * kWave + lane] = 0;
-  }
-  __syncthreads();
+  hist_boundary(s, n_keep);
   if (scale == 0.0) return -INFINITY;
   // every binned score in bins <= bstar exceeds hi - (bstar + 1) / scale up to
   // rounding, which the margin covers
