@@ -75,6 +75,7 @@ struct SelMem {
   uint32_t p_info[kPoolCap];
   int32_t map[kPoolCap];
   int32_t aux[kPoolCap + 1];
+  int32_t run[kPoolCap];   // sibling run of each entry: first index << 8 | length
   union {
     struct {
       int32_t hist[kBins + 1];
@@ -253,6 +254,7 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
   const int kept = block_scan(s, s.aux, n + 1);   // aux[i] = new index if kept
   double keep_s[kPerThread];
   uint32_t keep_i[kPerThread];
+  int32_t keep_r[kPerThread];
   int keep_to[kPerThread];
 #pragma unroll
   for (int k = 0; k < kPerThread; ++k) {
@@ -263,6 +265,10 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
       const int p = pi_parent(info);
       keep_s[k] = s.p_score[i];
       keep_i[k] = pinfo(p < 0 ? -1 : s.aux[p], pi_depth(info), pi_slot(info), pi_idr(info));
+      // the run keeps its kept members: aux[j] = new index of the first kept entry >= j
+      const int32_t rv = s.run[i];
+      const int r0 = rv >> 8, r1 = r0 + (rv & 255);
+      keep_r[k] = (s.aux[r0] << 8) | (s.aux[r1] - s.aux[r0]);
       keep_to[k] = s.aux[i];
     }
   }
@@ -273,6 +279,7 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
     if (keep_to[k] >= 0) {
       s.p_score[keep_to[k]] = keep_s[k];
       s.p_info[keep_to[k]] = keep_i[k];
+      s.run[keep_to[k]] = keep_r[k];
     }
   __syncthreads();
   return kept;
@@ -333,7 +340,7 @@ __device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv
 template <int KV>
 __device__ __forceinline__ double append_children(SelMem &s, const float *row, int kv,
                                                   double theta, int dst, int x, int d, double ps,
-                                                  const uint8_t *idr) {
+                                                  const uint8_t *idr, int32_t runv) {
   const float4 *r4 = reinterpret_cast<const float4 *>(row);
   float4 v[KV];
 #pragma unroll
@@ -350,6 +357,7 @@ __device__ __forceinline__ double append_children(SelMem &s, const float *row, i
         const int slot = q * 4 + k;
         s.p_score[dst] = sc;
         s.p_info[dst] = pinfo(x, d + 1, slot, idr[slot]);
+        s.run[dst] = runv;
         vmin = sc < vmin ? sc : vmin;
       }
       dst += take ? 1 : 0;
@@ -433,26 +441,29 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
   return edge - 1e-9 * (fabs(edge) + fabs(hi) + 1.0);
 }
 
-// Appends the children of pool entry x that reach theta at dst (the caller
-// counted them) and returns the smallest appended score.
+// Appends the c children of pool entry x that reach theta at dst (the caller
+// counted them), records their sibling run and returns the smallest appended
+// score.
 __device__ __forceinline__ double entry_append(SelMem &s, const float *rs, int x, int K, int kv,
-                                               int KVP, double theta, int dst) {
+                                               int KVP, double theta, int dst, int c) {
+  const int32_t runv = (dst << 8) | c;
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
   const int row = (d * K + pi_slot(info)) * K;
   const double ps = s.p_score[x];
   const uint8_t *idr = s.idr + d * K;
-  if (KVP == 1) return append_children<1>(s, rs + row, kv, theta, dst, x, d, ps, idr);
-  if (KVP == 2) return append_children<2>(s, rs + row, kv, theta, dst, x, d, ps, idr);
-  if (KVP == 4) return append_children<4>(s, rs + row, kv, theta, dst, x, d, ps, idr);
-  if (KVP == 8) return append_children<8>(s, rs + row, kv, theta, dst, x, d, ps, idr);
-  if (KVP == 16) return append_children<16>(s, rs + row, kv, theta, dst, x, d, ps, idr);
+  if (KVP == 1) return append_children<1>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
+  if (KVP == 2) return append_children<2>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
+  if (KVP == 4) return append_children<4>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
+  if (KVP == 8) return append_children<8>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
+  if (KVP == 16) return append_children<16>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
   double vmin = INFINITY;
   for (int r = 0; r < K; ++r) {
     const double sc = ps + static_cast<double>(rs[row + r]);
     if (sc >= theta) {
       s.p_score[dst] = sc;
       s.p_info[dst] = pinfo(x, d + 1, r, idr[r]);
+      s.run[dst] = runv;
       ++dst;
       vmin = sc < vmin ? sc : vmin;
     }
@@ -475,6 +486,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   for (int r = tid; r < K; r += kSelThreads) {
     s.p_score[r] = static_cast<double>(rs[r]);
     s.p_info[r] = pinfo(-1, 1, r, s.idr[r]);
+    s.run[r] = K;   // the depth-1 run starts at 0
   }
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
   // the depth-1 row's largest and smallest scores, in every wave (K <= 64)
@@ -579,18 +591,21 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       if (i >= lim) break;
       const int c = fit ? s.aux[i] : s.aux[i + 1] - s.aux[i];
       if (c > 0) {
-        const double v = entry_append(s, rs, x_lo + i, K, kv, KVP, theta, dst);
+        const double v = entry_append(s, rs, x_lo + i, K, kv, KVP, theta, dst, c);
         amin = v < amin ? v : amin;
       }
       dst += c;
     }
-    // the smallest appended score: one LDS atomic per wave
+    // the smallest appended score (needed only while theta is unset): one LDS
+    // atomic per wave
+    if (theta == -INFINITY) {
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const double ov = xor_lane_f64(amin, o);
-      amin = ov < amin ? ov : amin;
+      for (int o = 1; o < kWave; o <<= 1) {
+        const double ov = xor_lane_f64(amin, o);
+        amin = ov < amin ? ov : amin;
+      }
+      if (lane == 0 && amin < INFINITY) atomicMin(&s.lomin, ordered_f64(amin));
     }
-    if (lane == 0 && amin < INFINITY) atomicMin(&s.lomin, ordered_f64(amin));
     __syncthreads();
     n += grown;
     n_alive += grown;
@@ -625,12 +640,13 @@ __device__ void canon_preorder(SelMem &s, int L, int K, int n, int n_sel) {
   }
   __syncthreads();
   // map[i] = sizes of the subtrees of i's siblings with smaller token ids;
-  // siblings lie within K entries of i
+  // the siblings (dead ones included) form i's run
   for (int i = tid; i < n; i += kSelThreads) {
     const uint32_t info = s.p_info[i];
     if (!alive(info)) continue;
     const int p = pi_parent(info), mine = pi_idr(info);
-    const int lo = i - K + 1 > 0 ? i - K + 1 : 0, hi = i + K < n ? i + K : n;
+    const int32_t rv = s.run[i];
+    const int lo = rv >> 8, hi = lo + (rv & 255);
     int left = 0;
     for (int j0 = lo; j0 < hi; j0 += 16) {
       uint32_t o[16];
