@@ -317,3 +317,27 @@ def test_zero_budget_and_tiny_trees():
     a, nodes, bonus = [x.cpu().numpy() for x in acc]
     assert a[0] == 0 and bonus[0] == inp["target_depth"][0, 0]
     ctx.close()
+
+
+def test_flat_scores_force_pool_compaction():
+    """Uniform logits and a zero scorer make every edge score equal (and a few
+    tie levels in the second sequence): the first expansion overflows the
+    pool, partial expansions and tie ranking follow, and a later expansion
+    only fits after the dead entries are compacted (their sibling runs are
+    remapped).  The trees must still match the oracle bit for bit."""
+    w = S.workload(0, batch=2, V=3000, L=4, K=64, n_max=1024, fixed_budget=1024)
+    inp = S.gen_round(w, with_targets=False)
+    flat = np.zeros((w.L, w.V), np.float32)
+    g = np.random.default_rng(9)
+    levels = -g.integers(0, 3, size=(w.L, w.V)).astype(np.float32)
+    inp["logits"] = np.stack([S.bf16_from_f32(flat), S.bf16_from_f32(levels)])
+    sc = WL.scorer_inputs(w, "literal")
+    sc["g_parent"] = np.zeros_like(sc["g_parent"])
+    sc["g_child"] = np.zeros_like(sc["g_child"])
+    ctx = WL.gpu_context(w, sc, None, torch)
+    gr = WL.gpu_round(ctx, w, inp, torch)
+    assert gr["n_nodes"].tolist() == [1024, 1024]
+    assert (gr["edge_scores"][0, 1:] == gr["edge_scores"][0, 1, 0, 0]).all()
+    staged_check(w, gr, sc, None, inp, range(w.batch))
+    assert ctx.device_status() == 0
+    ctx.close()
