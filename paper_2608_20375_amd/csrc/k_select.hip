@@ -290,15 +290,18 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
 // child-slot order.  Every load is issued unconditionally (clamped to the
 // row) before any use, so one memory round trip covers the row.
 
+template <int KV>
+__device__ __forceinline__ void load_row(const float *row, int kv, float4 (&v)[KV]) {
+  const float4 *r4 = reinterpret_cast<const float4 *>(row);
+#pragma unroll
+  for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
+}
+
 // Number of children r < K with ps + row[r] >= theta (fp64 sums), and the
 // row's smallest edge score.
 template <int KV>
-__device__ __forceinline__ int count_reach(const float *row, int kv, double ps, double theta,
-                                           float &rmin) {
-  const float4 *r4 = reinterpret_cast<const float4 *>(row);
-  float4 v[KV];
-#pragma unroll
-  for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
+__device__ __forceinline__ int count_row(const float4 (&v)[KV], int kv, double ps, double theta,
+                                         float &rmin) {
   int c = 0;
   float mn = v[0].x;
 #pragma unroll
@@ -312,6 +315,13 @@ __device__ __forceinline__ int count_reach(const float *row, int kv, double ps, 
   }
   rmin = mn;
   return c;
+}
+template <int KV>
+__device__ __forceinline__ int count_reach(const float *row, int kv, double ps, double theta,
+                                           float &rmin) {
+  float4 v[KV];
+  load_row<KV>(row, kv, v);
+  return count_row<KV>(v, kv, ps, theta, rmin);
 }
 
 // Adds the children of a row that reach theta (scores ps + row[r]) to the
@@ -335,16 +345,12 @@ __device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv
 }
 
 // Appends the children of a row that reach theta at dst, dst + 1, ... in
-// child-slot order (scores ps + row[r], info with parent x at depth d + 1) and
-// returns the smallest appended score.
+// child-slot order (scores ps + row[r], info with parent x at depth d + 1,
+// sibling run runv) and returns the smallest appended score.
 template <int KV>
-__device__ __forceinline__ double append_children(SelMem &s, const float *row, int kv,
-                                                  double theta, int dst, int x, int d, double ps,
-                                                  const uint8_t *idr, int32_t runv) {
-  const float4 *r4 = reinterpret_cast<const float4 *>(row);
-  float4 v[KV];
-#pragma unroll
-  for (int q = 0; q < KV; ++q) v[q] = r4[q < kv ? q : kv - 1];
+__device__ __forceinline__ double append_row(SelMem &s, const float4 (&v)[KV], int kv,
+                                             double theta, int dst, int x, int d, double ps,
+                                             const uint8_t *idr, int32_t runv) {
   double vmin = INFINITY;
 #pragma unroll
   for (int q = 0; q < KV; ++q) {
@@ -364,6 +370,14 @@ __device__ __forceinline__ double append_children(SelMem &s, const float *row, i
     }
   }
   return vmin;
+}
+template <int KV>
+__device__ __forceinline__ double append_children(SelMem &s, const float *row, int kv,
+                                                  double theta, int dst, int x, int d, double ps,
+                                                  const uint8_t *idr, int32_t runv) {
+  float4 v[KV];
+  load_row<KV>(row, kv, v);
+  return append_row<KV>(s, v, kv, theta, dst, x, d, ps, idr, runv);
 }
 
 // Children of pool entry x (alive, depth < L) that reach theta, and the
@@ -471,18 +485,47 @@ __device__ __forceinline__ double entry_append(SelMem &s, const float *rs, int x
   return vmin;
 }
 
+// Cached variants: the caller keeps the entry's row (v) in registers from
+// the count to the append.
+template <int KV>
+__device__ __forceinline__ Counted entry_count_cached(const SelMem &s, const float *rs, int x,
+                                                      int L, int K, int kv, double theta,
+                                                      float4 (&v)[KV]) {
+  const uint32_t info = s.p_info[x];
+  const double ps = s.p_score[x];
+  if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
+  load_row<KV>(rs + (pi_depth(info) * K + pi_slot(info)) * K, kv, v);
+  float rmin = 0.f;
+  const int c = count_row<KV>(v, kv, ps, theta, rmin);
+  return {c, ps + static_cast<double>(rmin)};
+}
+template <int KV>
+__device__ __forceinline__ double entry_append_cached(SelMem &s, int x, int K, int kv,
+                                                      double theta, int dst, int c,
+                                                      const float4 (&v)[KV]) {
+  const uint32_t info = s.p_info[x];
+  const int d = pi_depth(info);
+  return append_row<KV>(s, v, kv, theta, dst, x, d, s.p_score[x], s.idr + d * K, (dst << 8) | c);
+}
+
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
 // alive unexpanded entry lies in [x_lo, n).  kLds: the edge rows are staged in
 // LDS (s.rows), else read from gs.
-template <bool kLds>
+template <bool kLds, int KVT>
 __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, const float *gs,
                                int n_target) {
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int L = a.L, K = a.K;
   const float *rs = kLds ? s.rows : gs;
-  // vector path: K % 4 == 0, kv = K / 4 groups, KVP = next power of two
+  // vector path: K % 4 == 0, kv = K / 4 groups, KVT = next power of two (0:
+  // the scalar path)
   const int kv = K / 4;
-  const int KVP = (K & 3) ? 0 : kv <= 1 ? 1 : kv <= 2 ? 2 : kv <= 4 ? 4 : kv <= 8 ? 8 : 16;
+  constexpr int KVP = KVT;
+  // the rows of a thread's first kCache entries stay in registers from the
+  // count to the append
+  constexpr int kCache = KVT == 0 ? 0 : KVT <= 8 ? 2 : 1;
+  constexpr int KVC = KVT > 0 ? KVT : 1;
+  float4 cache[kCache > 0 ? kCache : 1][KVC];
   for (int r = tid; r < K; r += kSelThreads) {
     s.p_score[r] = static_cast<double>(rs[r]);
     s.p_info[r] = pinfo(-1, 1, r, s.idr[r]);
@@ -518,7 +561,17 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
     const int i0 = tid * per;
     int sum = 0;
     double vmin = INFINITY;
-    for (int k = 0; k < per; ++k) {
+#pragma unroll
+    for (int k = 0; k < kCache; ++k) {
+      const int i = i0 + k;
+      if (k < per && i < m) {
+        const Counted e = entry_count_cached<KVC>(s, rs, x_lo + i, L, K, kv, theta, cache[k]);
+        s.aux[i] = e.c;
+        sum += e.c;
+        vmin = e.vmin < vmin ? e.vmin : vmin;
+      }
+    }
+    for (int k = kCache; k < per; ++k) {
       const int i = i0 + k;
       if (i >= m) break;
       const Counted e = entry_count(s, rs, x_lo + i, L, K, kv, KVP, theta);
@@ -586,7 +639,19 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       break;
     }
     double amin = INFINITY;
-    for (int k = 0; k < per; ++k) {
+#pragma unroll
+    for (int k = 0; k < kCache; ++k) {
+      const int i = i0 + k;
+      if (k < per && i < lim) {
+        const int c = fit ? s.aux[i] : s.aux[i + 1] - s.aux[i];
+        if (c > 0) {
+          const double v = entry_append_cached<KVC>(s, x_lo + i, K, kv, theta, dst, c, cache[k]);
+          amin = v < amin ? v : amin;
+        }
+        dst += c;
+      }
+    }
+    for (int k = kCache; k < per; ++k) {
       const int i = i0 + k;
       if (i >= lim) break;
       const int c = fit ? s.aux[i] : s.aux[i + 1] - s.aux[i];
@@ -617,6 +682,20 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
   for (int i = tid; i < kMaxL; i += kSelThreads) s.dcnt[i] = 0;
   return n;
+}
+
+// select_parallel for the row width of K: groups of four (kv = K / 4,
+// rounded up to a power of two) or the scalar path when K % 4 != 0.
+template <bool kLds>
+__device__ __forceinline__ int select_parallel_k(SelMem &s, const SelectArgs &a, const float *gs,
+                                                 int n_target) {
+  const int K = a.K, kv = K / 4;
+  if (K & 3) return select_parallel<kLds, 0>(s, a, gs, n_target);
+  if (kv <= 1) return select_parallel<kLds, 1>(s, a, gs, n_target);
+  if (kv <= 2) return select_parallel<kLds, 2>(s, a, gs, n_target);
+  if (kv <= 4) return select_parallel<kLds, 4>(s, a, gs, n_target);
+  if (kv <= 8) return select_parallel<kLds, 8>(s, a, gs, n_target);
+  return select_parallel<kLds, 16>(s, a, gs, n_target);
 }
 
 // Canonical numbering for the parallel selector's pool, where the children of
@@ -939,8 +1018,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   const bool mono = s.sc[kMono] != 0;
   if (mono) {
     if (n_target > 0) {
-      const int n_pool = staged ? select_parallel<true>(s, a, ss, n_target)
-                                : select_parallel<false>(s, a, ss, n_target);
+      const int n_pool = staged ? select_parallel_k<true>(s, a, ss, n_target)
+                                : select_parallel_k<false>(s, a, ss, n_target);
       if (tid == 0) s.sc[kNPool] = n_pool;
     } else if (tid == 0) {
       s.sc[kNPool] = 0;
