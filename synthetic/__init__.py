@@ -34,7 +34,7 @@ __all__ = [
     "Workload", "WORKLOADS", "workload", "bf16_from_f32", "f32_from_bf16",
     "gen_sequence_logits", "gen_round", "gen_scorer", "saba_params",
     "hist_ring_init", "node_targets", "splitmix64", "NODE_TARGET_P_NUM", "gen_hidden",
-    "gen_traces",
+    "gen_traces", "gen_replay",
 ]
 
 HIST_WINDOW = 4
@@ -396,3 +396,28 @@ def gen_traces(w: Workload, n_groups: int, n_pairs: int, step: int = 0) -> dict:
             pairs[i] = (p, c, d, q, c, d)
     return dict(parent=parent, depth=depth, child=child, logq=logq, z=z, target=target,
                 pairs=pairs)
+
+
+def gen_replay(n_rounds: int, grid=tuple(range(32, 513, 16)), phi=(6.0, 40.0, 30.0, 12.0),
+               c=(20.0, 0.05, 2e-5), tau_min=8.0, noise=0.0, seed=0) -> dict:
+    """A synthetic same-prefix budget-replay log for fitting SABA: every round
+    replayed with each budget of the grid.  States conf ~ U(0.2, 0.95),
+    degen ~ U(0.6, 1.4), hist ~ U(1, 12); prefix ~ U{64..4096}; the round's
+    scale A ~ U(2, 14); accepted length A (1 - exp(-B / tau)) (1 + noise N(0,1)),
+    tau = max(phi . [1, s], tau_min); latency (c0 + c1 B + c2 B prefix)
+    (1 + noise N(0,1)).  float32 / int32 arrays."""
+    g = np.random.default_rng([9009, n_rounds, seed])
+    T = n_rounds
+    B = np.asarray(grid, np.float64)
+    state = np.stack([g.uniform(0.2, 0.95, T), g.uniform(0.6, 1.4, T), g.uniform(1, 12, T)],
+                     axis=1)
+    prefix = g.integers(64, 4097, T)
+    tau = np.maximum(phi[0] + state @ np.asarray(phi[1:], np.float64), tau_min)
+    A = g.uniform(2, 14, T)
+    acc = A[:, None] * (1.0 - np.exp(-B[None, :] / tau[:, None]))
+    acc *= 1.0 + noise * g.standard_normal(acc.shape)
+    lat = c[0] + c[1] * B[None, :] + c[2] * B[None, :] * prefix[:, None]
+    lat = lat * (1.0 + noise * g.standard_normal(lat.shape))
+    return dict(budgets=np.asarray(grid, np.int32), state=state.astype(np.float32),
+                prefix=prefix.astype(np.int32), accepted=acc.astype(np.float32),
+                latency=lat.astype(np.float32), tau_min=float(tau_min))
