@@ -364,6 +364,42 @@ GRAFT_API int graft_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_
  * cleared). */
 GRAFT_API int graft_tdes_device_status(graft_tdes *t, graft_stream_t stream);
 
+/* ------------------------------------------------------------------------ */
+/* SABA parameter fit by same-prefix budget replay (the paper's SABA section:  */
+/* the gain and cost models are fitted on held-out replays and then fixed).     */
+/* ------------------------------------------------------------------------ */
+
+/* A replay log: round t of the validation set was decoded from one prefix with
+ * every budget of the grid, giving its accepted length and round latency.
+ * state, prefix, accepted, latency are device arrays; budgets is host. */
+typedef struct {
+    int32_t n_rounds;         /* T >= 1 */
+    int32_t n_budgets;        /* 1..64 */
+    const int32_t *budgets;   /* host [n_budgets], positive */
+    const float *state;       /* [T, 3]: conf, degen (or the entropy stand-in), hist */
+    const int32_t *prefix;    /* [T] prefix length of the round */
+    const float *accepted;    /* [T, n_budgets] accepted length a_t(B_j) */
+    const float *latency;     /* [T, n_budgets] round latency l_t(B_j), any unit */
+    float tau_min;            /* > 0, as in graft_saba_desc */
+} graft_saba_replay;
+
+/* Fits the cost c = (c0, c1, c2) of eq. saba-cost by least squares of
+ * l_t(B_j) on [1, B_j, B_j prefix_t], and phi of eq. saba-gain by
+ * Levenberg-Marquardt from phi_init: phi minimises
+ *   sum_{t,j} (A_t G_t(B_j) - a_t(B_j))^2,  G_t(B) = 1 - exp(-B / tau_t),
+ *   tau_t = max(phi . [1, s_t], tau_min),
+ * with each round's scale A_t eliminated in closed form (it cancels in the
+ * budget rule's argmax); rounds that accept nothing contribute nothing.  The
+ * sums over the log run on the device (fp64, fixed order: deterministic), the
+ * 4 x 4 steps on the host; synchronous on `stream`.  phi_out and c_out (host,
+ * 4 and 3 floats) are graft_saba_desc's phi and c0..c2; stats (host, 4 doubles,
+ * or NULL): the gain and cost sums of squares, the iterations taken, and 1 if
+ * the steps converged (0 if max_iter ran out or the system was singular, e.g.
+ * every tau clamped). */
+GRAFT_API int graft_saba_fit(const graft_saba_replay *log /* host */, const float *phi_init /* host [4] */,
+                             int32_t max_iter, float *phi_out, float *c_out, double *stats,
+                             graft_stream_t stream);
+
 GRAFT_API const char *graft_status_string(int status);
 GRAFT_API const char *graft_last_error(void);
 

@@ -12,8 +12,8 @@ import os
 
 import torch
 
-__all__ = ["Context", "TreeBuffers", "TdesTrainer", "TdesHyper", "lib", "library_path",
-           "GraftError", "EXPORTED_SYMBOLS"]
+__all__ = ["Context", "TreeBuffers", "TdesTrainer", "TdesHyper", "saba_fit", "lib",
+           "library_path", "GraftError", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libgraft.so")
@@ -24,7 +24,7 @@ EXPORTED_SYMBOLS = (
     "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
     "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
     "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create", "graft_tdes_destroy",
-    "graft_tdes_param_count", "graft_tdes_step", "graft_tdes_device_status",
+    "graft_tdes_param_count", "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit",
 )
 
 
@@ -92,6 +92,12 @@ class TdesHyper(C.Structure):
                          beta2, eps)
 
 
+class SabaReplay(C.Structure):
+    _fields_ = [("n_rounds", C.c_int32), ("n_budgets", C.c_int32), ("budgets", C.c_void_p),
+                ("state", C.c_void_p), ("prefix", C.c_void_p), ("accepted", C.c_void_p),
+                ("latency", C.c_void_p), ("tau_min", C.c_float)]
+
+
 class Targets(C.Structure):
     _fields_ = [("target_root", C.c_void_p), ("target_node", C.c_void_p),
                 ("target_depth", C.c_void_p)]
@@ -134,6 +140,9 @@ def lib():
         L.graft_tdes_step.argtypes = [vp, vp, C.POINTER(TdesBatch), C.POINTER(TdesHyper), i32, vp,
                                       vp, vp, vp, vp, vp]
         L.graft_tdes_device_status.argtypes = [vp, vp]
+        L.graft_saba_fit.argtypes = [C.POINTER(SabaReplay), C.POINTER(C.c_float), i32,
+                                     C.POINTER(C.c_float), C.POINTER(C.c_float),
+                                     C.POINTER(C.c_double), vp]
         L.graft_status_string.argtypes = [C.c_int]
         L.graft_status_string.restype = C.c_char_p
         L.graft_last_error.argtypes = []
@@ -142,7 +151,7 @@ def lib():
                   "graft_build_tree", "graft_accept", "graft_get_device_status",
                   "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
                   "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create",
-                  "graft_tdes_step", "graft_tdes_device_status"):
+                  "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -441,4 +450,33 @@ class TdesTrainer:
 
     def device_status(self) -> int:
         return lib().graft_tdes_device_status(self._h, _stream())
+
+
+def saba_fit(budgets, state, prefix, accepted, latency, tau_min, phi_init, max_iter=200):
+    """SABA's gain weights phi and cost c0..c2 fitted on a same-prefix replay
+    log (graft_saba_fit): budgets a host sequence of ints; state [T, 3],
+    prefix [T] int32, accepted and latency [T, n_budgets] float32 as CUDA
+    tensors.  Returns a dict with phi (4), c (3), gain_sse, cost_sse,
+    iterations and converged."""
+    import numpy as np
+    T = int(state.shape[0])
+    nb = len(budgets)
+    b = np.ascontiguousarray(np.asarray(budgets, np.int32))
+    for name, t, shape in (("state", state, (T, 3)), ("accepted", accepted, (T, nb)),
+                           ("latency", latency, (T, nb))):
+        if tuple(t.shape) != shape:
+            raise ValueError("%s must be %s" % (name, shape))
+    if tuple(prefix.shape) != (T,):
+        raise ValueError("prefix must be [T]")
+    log = SabaReplay(T, nb, b.ctypes.data, _ptr(state, torch.float32, "state"),
+                     _ptr(prefix, torch.int32, "prefix"), _ptr(accepted, torch.float32, "accepted"),
+                     _ptr(latency, torch.float32, "latency"), float(tau_min))
+    phi0 = (C.c_float * 4)(*[float(v) for v in phi_init])
+    phi = (C.c_float * 4)()
+    c = (C.c_float * 3)()
+    st = (C.c_double * 4)()
+    _check(lib().graft_saba_fit(C.byref(log), phi0, int(max_iter), phi, c, st, _stream()),
+           "graft_saba_fit")
+    return dict(phi=list(phi), c=list(c), gain_sse=st[0], cost_sse=st[1], iterations=int(st[2]),
+                converged=bool(st[3]))
 

@@ -1,6 +1,7 @@
 // graft_api.hip -- host side of the C ABI declared in include/graft.h:
 // validation, context and workspace ownership, kernel launches on the
 // caller's stream.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -460,6 +461,155 @@ int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t seed,
                                              parents, topk_ids, target_root, target_node,
                                              reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "graft_synth_node_targets");
+  return GRAFT_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Solves the n x n system M x = r (row-major, n <= 4) by Gaussian elimination
+// with partial pivoting; false when a pivot is not positive enough.
+bool solve_small(int n, double *M, double *r, double *x) {
+  for (int c = 0; c < n; ++c) {
+    int p = c;
+    for (int i = c + 1; i < n; ++i)
+      if (std::fabs(M[i * n + c]) > std::fabs(M[p * n + c])) p = i;
+    if (!(std::fabs(M[p * n + c]) > 1e-300)) return false;
+    if (p != c) {
+      for (int j = 0; j < n; ++j) std::swap(M[c * n + j], M[p * n + j]);
+      std::swap(r[c], r[p]);
+    }
+    for (int i = c + 1; i < n; ++i) {
+      const double f = M[i * n + c] / M[c * n + c];
+      for (int j = c; j < n; ++j) M[i * n + j] -= f * M[c * n + j];
+      r[i] -= f * r[c];
+    }
+  }
+  for (int c = n - 1; c >= 0; --c) {
+    double v = r[c];
+    for (int j = c + 1; j < n; ++j) v -= M[c * n + j] * x[j];
+    x[c] = v / M[c * n + c];
+    if (!std::isfinite(x[c])) return false;
+  }
+  return true;
+}
+
+// Symmetric matrix from its upper triangle (row by row).
+void unpack_sym(int n, const double *u, double *M) {
+  int k = 0;
+  for (int p = 0; p < n; ++p)
+    for (int q = p; q < n; ++q) M[p * n + q] = M[q * n + p] = u[k++];
+}
+
+}  // namespace
+
+extern "C" {
+
+int graft_saba_fit(const graft_saba_replay *log, const float *phi_init, int32_t max_iter,
+                   float *phi_out, float *c_out, double *stats, graft_stream_t stream) {
+  if (!log || !phi_init || !phi_out || !c_out)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_saba_fit: NULL argument");
+  const int T = log->n_rounds, nb = log->n_budgets;
+  if (T < 1 || nb < 1 || nb > 64 || max_iter < 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_saba_fit: need n_rounds >= 1, n_budgets in 1..64, max_iter >= 0");
+  if (!log->budgets || !log->state || !log->prefix || !log->accepted || !log->latency)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_saba_fit: a log array is NULL");
+  if (!(log->tau_min > 0.0f) || !std::isfinite(log->tau_min))
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_saba_fit: tau_min must be positive and finite");
+  for (int j = 0; j < nb; ++j)
+    if (log->budgets[j] < 1) return fail(GRAFT_ERR_INVALID_ARG, "graft_saba_fit: budgets must be positive");
+  for (int k = 0; k < 4; ++k)
+    if (!std::isfinite(phi_init[k])) return fail(GRAFT_ERR_INVALID_ARG, "graft_saba_fit: phi_init must be finite");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  int32_t *d_budgets = nullptr;
+  double *d_part = nullptr, *d_out = nullptr;
+  hipError_t e = dalloc(&d_budgets, static_cast<size_t>(nb));
+  if (e == hipSuccess) e = dalloc(&d_part, static_cast<size_t>(graft::kFitMaxBlocks) * graft::kFitSums);
+  if (e == hipSuccess) e = dalloc(&d_out, static_cast<size_t>(graft::kFitSums));
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(d_budgets, log->budgets, sizeof(int32_t) * nb, hipMemcpyHostToDevice, s);
+  double sums[graft::kFitSums];
+  const double tau_min = log->tau_min;
+  auto eval = [&](const double *phi, int with_cost, const double *cfit) -> hipError_t {
+    hipError_t err = graft::launch_replay_sums(T, nb, d_budgets, log->state, log->prefix,
+                                               log->accepted, log->latency, phi, tau_min, with_cost,
+                                               cfit, d_part, d_out, s);
+    if (err == hipSuccess)
+      err = hipMemcpyAsync(sums, d_out, sizeof(sums), hipMemcpyDeviceToHost, s);
+    if (err == hipSuccess) err = hipStreamSynchronize(s);
+    return err;
+  };
+  double phi[4] = {phi_init[0], phi_init[1], phi_init[2], phi_init[3]};
+  double c[3] = {0.0, 0.0, 0.0}, cost_sse = 0.0;
+  int iters = 0, converged = 0;
+  if (e == hipSuccess) e = eval(phi, 1, nullptr);
+  bool cost_ok = false;
+  if (e == hipSuccess) {
+    // cost: normal equations of the affine model
+    double M[9], r[3] = {sums[21], sums[22], sums[23]};
+    unpack_sym(3, sums + 15, M);
+    cost_ok = solve_small(3, M, r, c);
+    // the residuals summed directly (the normal-equation form cancels badly)
+    e = eval(phi, 2, c);
+    cost_sse = cost_ok ? sums[24] : 0.0;
+  }
+  if (e == hipSuccess) {
+    // gain: Levenberg-Marquardt with Marquardt's diagonal scaling
+    double F = sums[0], H[16], g[4];
+    unpack_sym(4, sums + 1, H);
+    for (int k = 0; k < 4; ++k) g[k] = sums[11 + k];
+    double lam = 1e-3;
+    while (iters < max_iter && e == hipSuccess) {
+      ++iters;
+      double A[16], b[4], d[4];
+      std::memcpy(A, H, sizeof A);
+      for (int k = 0; k < 4; ++k) {
+        A[k * 4 + k] += lam * (H[k * 4 + k] > 1e-300 ? H[k * 4 + k] : 1e-300);
+        b[k] = -g[k];
+      }
+      if (!solve_small(4, A, b, d)) break;   // singular: every tau clamped, or no data
+      double trial[4];
+      for (int k = 0; k < 4; ++k) trial[k] = phi[k] + d[k];
+      e = eval(trial, 0, nullptr);
+      if (e != hipSuccess) break;
+      if (sums[0] < F) {
+        const double rel = (F - sums[0]) / (F > 0.0 ? F : 1.0);
+        std::memcpy(phi, trial, sizeof phi);
+        F = sums[0];
+        unpack_sym(4, sums + 1, H);
+        for (int k = 0; k < 4; ++k) g[k] = sums[11 + k];
+        lam = lam / 10.0 > 1e-15 ? lam / 10.0 : 1e-15;
+        double step = 0.0, size = 0.0;
+        for (int k = 0; k < 4; ++k) {
+          step += d[k] * d[k];
+          size += phi[k] * phi[k];
+        }
+        if (rel < 1e-15 || step <= 1e-24 * (1.0 + size)) {
+          converged = 1;
+          break;
+        }
+      } else {
+        lam *= 10.0;
+        if (lam > 1e16) {
+          converged = 1;   // no descent left at machine precision
+          break;
+        }
+      }
+    }
+    if (stats) {
+      stats[0] = F;
+      stats[1] = cost_sse;
+      stats[2] = iters;
+      stats[3] = converged;
+    }
+  }
+  (void)hipFree(d_budgets);
+  (void)hipFree(d_part);
+  (void)hipFree(d_out);
+  if (e != hipSuccess) return hip_fail(e, "graft_saba_fit");
+  for (int k = 0; k < 4; ++k) phi_out[k] = static_cast<float>(phi[k]);
+  for (int k = 0; k < 3; ++k) c_out[k] = static_cast<float>(c[k]);
   return GRAFT_OK;
 }
 

@@ -15,6 +15,8 @@ constexpr int kMaxNodes = 1024;
 constexpr int kMaxGrid = 64;
 constexpr int kMaxScoreDim = 64;
 constexpr int kTdesMaxLossBlocks = 512;
+constexpr int kFitSums = 25;        // replay sums: SSE, J^T J (10), J^T r (4), X^T X (6), X^T y (3), y^T y
+constexpr int kFitMaxBlocks = 256;
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -305,6 +307,15 @@ bool tdes_shape_supported(int E, int m, int L, int K);
 hipError_t launch_tdes_step(graft_tdes *t, const float *emb, const graft_tdes_batch *b,
                             const graft_tdes_hyper *h, int32_t step, float *theta, float *m1,
                             float *m2, double *loss, float *grad, hipStream_t stream);
+
+// SABA fit: the replay sums at phi (kFitSums doubles into out, device), with
+// the cost's normal equations (with_cost 1) or the residual sum of squares of
+// cost c (with_cost 2); partial holds kFitMaxBlocks * kFitSums doubles.
+int saba_fit_blocks(int T);
+hipError_t launch_replay_sums(int T, int nb, const int32_t *budgets, const float *state,
+                              const int32_t *prefix, const float *accepted, const float *latency,
+                              const double phi[4], double tau_min, int with_cost,
+                              const double c[3], double *partial, double *out, hipStream_t stream);
 
 // Number of splits per row used by the logits pass for a given row count.
 int logits_splits(const graft_dims &d, int rows);
