@@ -192,6 +192,36 @@ def time_training(w, steps, torch, dev, G=4096, P=4096, cpu=True):
     return out
 
 
+def time_saba_fit(torch, dev, T=20000, cpu=True):
+    """SABA's parameter fit on a synthetic same-prefix replay log of T rounds
+    over the 32..512 grid (31 budgets, 5% noise): wall time of the whole fit
+    (device sums, host steps, synchronisations), iterations, and the oracle's
+    time for the same fit."""
+    import synthetic as S
+    import paper_2608_20375_amd as GR
+    r = S.gen_replay(T, noise=0.05, seed=11)
+    Tt = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    args = (r["budgets"], Tt(r["state"]), Tt(r["prefix"]), Tt(r["accepted"]), Tt(r["latency"]),
+            r["tau_min"], (10.0, 10.0, 10.0, 10.0))
+    GR.saba_fit(*args)
+    torch.cuda.synchronize()
+    t0 = time.time()
+    n = 5
+    for _ in range(n):
+        out = GR.saba_fit(*args)
+    dt = (time.time() - t0) / n
+    res = {"rounds": T, "budgets": int(len(r["budgets"])), "fit_ms": 1e3 * dt,
+           "iterations": out["iterations"], "phi": out["phi"], "c": out["c"],
+           "samples_per_s": T * len(r["budgets"]) * (out["iterations"] + 2) / dt}
+    if cpu:
+        from oracle import saba_fit as OF
+        t0 = time.time()
+        OF.fit(r["budgets"], r["state"].astype(np.float64), r["prefix"], r["accepted"],
+               r["latency"], r["tau_min"], (10.0, 10.0, 10.0, 10.0))
+        res["cpu_oracle_fit_ms"] = 1e3 * (time.time() - t0)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,6 +241,9 @@ def main():
     ap.add_argument("--train", action="store_true",
                     help="also time one TDES training step (4096 groups, 4096 pairs of synthetic "
                          "traces with the workload's vocabulary, L, K and scorer sizes)")
+    ap.add_argument("--saba-fit", action="store_true",
+                    help="also time SABA's parameter fit on a synthetic replay log (20000 "
+                         "rounds x 31 budgets)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
     args = ap.parse_args()
@@ -345,6 +378,11 @@ def main():
         training = time_training(w, args.steps, torch, dev, cpu=not args.no_cpu_baseline)
         log("tdes training step: %s" % training)
 
+    saba_fit = None
+    if args.saba_fit:
+        saba_fit = time_saba_fit(torch, dev, cpu=not args.no_cpu_baseline)
+        log("saba fit: %s" % saba_fit)
+
     nodes = tb.n_nodes.float().mean().item()
     budgets = tb.budget.float().mean().item()
     cpu = None
@@ -400,6 +438,8 @@ def main():
         result["verifier"] = verifier
     if training is not None:
         result["tdes_training"] = training
+    if saba_fit is not None:
+        result["saba_fit"] = saba_fit
     print(json.dumps(result), flush=True)
     ctx.close()
 

@@ -16,7 +16,7 @@ constexpr int kMaxGrid = 64;
 constexpr int kMaxScoreDim = 64;
 constexpr int kTdesMaxLossBlocks = 512;
 constexpr int kFitSums = 25;        // replay sums: SSE, J^T J (10), J^T r (4), X^T X (6), X^T y (3), y^T y
-constexpr int kFitMaxBlocks = 256;
+constexpr int kFitMaxBlocks = 1024;
 
 // ---------------------------------------------------------------------------
 // Device helpers

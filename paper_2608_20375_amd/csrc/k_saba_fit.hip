@@ -22,7 +22,7 @@ namespace {
 
 constexpr int kFitWaves = 8;
 constexpr int kFitThreads = kFitWaves * kWave;
-constexpr int kRedSlices = 8;
+constexpr int kRedSlices = 32;
 
 struct FitArgs {
   int T, nb;
@@ -111,8 +111,10 @@ __global__ void __launch_bounds__(kRedSlices * 32) replay_reduce_kernel(const do
   __shared__ double s_r[kRedSlices][32];
   const int k = threadIdx.x % 32, sl = threadIdx.x / 32;
   double v = 0.0;
-  if (k < kFitSums)
+  if (k < kFitSums) {
+#pragma unroll 8
     for (int b = sl; b < blocks; b += kRedSlices) v += partial[static_cast<int64_t>(b) * kFitSums + k];
+  }
   s_r[sl][k] = v;
   __syncthreads();
   if (sl == 0 && k < kFitSums) {
@@ -125,7 +127,7 @@ __global__ void __launch_bounds__(kRedSlices * 32) replay_reduce_kernel(const do
 }  // namespace
 
 int saba_fit_blocks(int T) {
-  const int b = (T + kFitWaves * 4 - 1) / (kFitWaves * 4);   // about 4 rounds per wave
+  const int b = (T + kFitWaves * 2 - 1) / (kFitWaves * 2);   // about 2 rounds per wave
   return b < 1 ? 1 : (b > kFitMaxBlocks ? kFitMaxBlocks : b);
 }
 
