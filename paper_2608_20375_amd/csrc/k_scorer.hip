@@ -85,19 +85,33 @@ struct SabaArgs {
 // exp(-B/tau)) / (c0 + c1 B + c2 B prefix) (eqs. saba-gain, saba-cost) for
 // every grid budget, one lane each in fp64; B_t = the smallest budget with the
 // largest U (eq. saba-objective).
-__device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int L) {
+// The budget's inputs, one wave's lanes; loaded before the edge work so that
+// their latency overlaps it.
+struct SabaIn {
+  float f_conf, f_ent, f_r, f_hist;
+  int32_t ring, prefix_i, fixed, grid;
+};
+__device__ __forceinline__ SabaIn saba_load(const SabaArgs &a, const SabaParams &sp, int b, int L) {
   const int lane = lane_id();
-  // every global load first
+  SabaIn in;
   const float *rs = a.row_stats + (static_cast<int64_t>(b) * L + (lane < L ? lane : 0)) * 3;
-  const float f_conf = rs[1], f_ent = rs[2];
+  in.f_conf = rs[1];
+  in.f_ent = rs[2];
   const int np = L - 1;
-  const float f_r = (a.adj_cos && lane < np) ? a.adj_cos[static_cast<int64_t>(b) * np + lane] : 0.f;
-  const float f_hist = a.hist ? a.hist[b] : 0.f;
-  const int32_t ring =
-      (!a.hist && lane < a.window) ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
-  const int32_t prefix_i = a.prefix_len ? a.prefix_len[b] : 0;
-  const int32_t fixed = a.fixed_budget ? a.fixed_budget[b] : 0;
-  const int32_t grid = lane < sp.n_grid ? sp.grid[lane] : 0;
+  in.f_r = (a.adj_cos && lane < np) ? a.adj_cos[static_cast<int64_t>(b) * np + lane] : 0.f;
+  in.f_hist = a.hist ? a.hist[b] : 0.f;
+  in.ring = (!a.hist && lane < a.window) ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
+  in.prefix_i = a.prefix_len ? a.prefix_len[b] : 0;
+  in.fixed = a.fixed_budget ? a.fixed_budget[b] : 0;
+  in.grid = lane < sp.n_grid ? sp.grid[lane] : 0;
+  return in;
+}
+
+__device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int L, const SabaIn &in) {
+  const int lane = lane_id();
+  const float f_conf = in.f_conf, f_ent = in.f_ent, f_r = in.f_r, f_hist = in.f_hist;
+  const int32_t ring = in.ring, prefix_i = in.prefix_i, fixed = in.fixed, grid = in.grid;
+  const int np = L - 1;
   double hist;
   if (a.hist) {
     hist = static_cast<double>(f_hist);
@@ -210,6 +224,8 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   const int n_par = (l == 0) ? 1 : K;
   const int64_t row = static_cast<int64_t>(b) * L + l;
   const int lane = threadIdx.x;
+  SabaIn saba_in{};
+  if (l == 0) saba_in = saba_load(sa, sp_saba, b, L);
 
   int32_t root = root_token[b];
   if (root < 0 || root >= V) {
@@ -333,7 +349,7 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   const bool any_pos = __ballot(pos) != 0ull;
   if (lane == 0) positive[row] = any_pos ? 1 : 0;
   // the depth-1 block (one parent, the lightest) also computes the budget
-  if (l == 0) saba_budget(sa, sp_saba, b, L);
+  if (l == 0) saba_budget(sa, sp_saba, b, L, saba_in);
 }
 
 }  // namespace
