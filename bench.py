@@ -359,6 +359,21 @@ def main():
     achieved = logit_bytes / k1_s / 1e9 if k1_s > 0 else 0.0
     traffic = stored_traffic(args.workload)
 
+    # a plain read of the same rotating buffers, back to back: the streaming
+    # read rate the logits pass is compared with
+    sink = torch.empty(G.READ_STREAM_SINK_WORDS, dtype=torch.int32, device=dev)
+    for i in range(3):
+        G.read_stream(bufs[i % R], sink)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(args.steps):
+        G.read_stream(bufs[i % R], sink)
+    e1.record()
+    torch.cuda.synchronize()
+    read_us = 1e3 * e0.elapsed_time(e1) / args.steps
+    read_gbs = logit_bytes / (read_us * 1e-6) / 1e9
+    log("plain read of one logits buffer: %.2f us = %.0f GB/s" % (read_us, read_gbs))
+
     if args.copy_calibration:
         n = 256 << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
@@ -431,6 +446,8 @@ def main():
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": logit_bytes,
+            "plain_read_gbs": read_gbs,
+            "frac_of_plain_read": achieved / read_gbs if read_gbs > 0 else None,
         },
         "cpu_baseline": cpu,
     }

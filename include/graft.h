@@ -400,6 +400,22 @@ GRAFT_API int graft_saba_fit(const graft_saba_replay *log /* host */, const floa
                              int32_t max_iter, float *phi_out, float *c_out, double *stats,
                              graft_stream_t stream);
 
+/* ------------------------------------------------------------------------ */
+/* Bandwidth reference                                                        */
+/* ------------------------------------------------------------------------ */
+
+#define GRAFT_READ_STREAM_SINK_WORDS 4096
+
+/* A plain read of `bytes` bytes at src (device, 16-byte aligned, bytes a
+ * positive multiple of 16) with the 16-byte non-temporal loads the logits pass
+ * uses and no other work: the HBM read rate a streaming kernel reaches, timed
+ * beside the logits pass in benchmarks.  sink (device, caller-owned,
+ * GRAFT_READ_STREAM_SINK_WORDS uint32) receives per-workgroup xors of the
+ * words read; the xor of all its words is the xor of every 32-bit word of the
+ * buffer.  Asynchronous on `stream`; GRAFT_ERR_INVALID_ARG for NULL pointers,
+ * misalignment or a bad size. */
+GRAFT_API int graft_read_stream(const void *src, int64_t bytes, uint32_t *sink, graft_stream_t stream);
+
 GRAFT_API const char *graft_status_string(int status);
 GRAFT_API const char *graft_last_error(void);
 

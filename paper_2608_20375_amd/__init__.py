@@ -12,7 +12,7 @@ import os
 
 import torch
 
-__all__ = ["Context", "TreeBuffers", "TdesTrainer", "TdesHyper", "saba_fit", "lib",
+__all__ = ["Context", "TreeBuffers", "TdesTrainer", "TdesHyper", "saba_fit", "read_stream", "lib",
            "library_path", "GraftError", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -25,7 +25,10 @@ EXPORTED_SYMBOLS = (
     "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
     "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create", "graft_tdes_destroy",
     "graft_tdes_param_count", "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit",
+    "graft_read_stream",
 )
+
+READ_STREAM_SINK_WORDS = 4096
 
 
 class GraftError(RuntimeError):
@@ -143,6 +146,7 @@ def lib():
         L.graft_saba_fit.argtypes = [C.POINTER(SabaReplay), C.POINTER(C.c_float), i32,
                                      C.POINTER(C.c_float), C.POINTER(C.c_float),
                                      C.POINTER(C.c_double), vp]
+        L.graft_read_stream.argtypes = [vp, C.c_int64, vp, vp]
         L.graft_status_string.argtypes = [C.c_int]
         L.graft_status_string.restype = C.c_char_p
         L.graft_last_error.argtypes = []
@@ -151,7 +155,8 @@ def lib():
                   "graft_build_tree", "graft_accept", "graft_get_device_status",
                   "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
                   "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create",
-                  "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit"):
+                  "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit",
+                  "graft_read_stream"):
             getattr(L, n).restype = C.c_int
         _lib = L
     return _lib
@@ -480,3 +485,18 @@ def saba_fit(budgets, state, prefix, accepted, latency, tau_min, phi_init, max_i
     return dict(phi=list(phi), c=list(c), gain_sse=st[0], cost_sse=st[1], iterations=int(st[2]),
                 converged=bool(st[3]))
 
+
+def read_stream(src, sink=None):
+    """A plain read of every byte of the contiguous CUDA tensor src
+    (graft_read_stream): the streaming read rate to compare the logits pass
+    with.  Returns the sink, READ_STREAM_SINK_WORDS int32 words whose xor is the
+    xor of src's 32-bit words."""
+    if not isinstance(src, torch.Tensor) or src.device.type != "cuda" or not src.is_contiguous():
+        raise TypeError("src must be a contiguous CUDA (HIP) tensor")
+    if sink is None:
+        sink = torch.empty(READ_STREAM_SINK_WORDS, dtype=torch.int32, device=src.device)
+    if sink.numel() < READ_STREAM_SINK_WORDS:
+        raise ValueError("sink must hold %d words" % READ_STREAM_SINK_WORDS)
+    _check(lib().graft_read_stream(src.data_ptr(), src.numel() * src.element_size(),
+                                   _ptr(sink, torch.int32, "sink"), _stream()), "graft_read_stream")
+    return sink

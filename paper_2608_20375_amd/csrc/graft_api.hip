@@ -506,6 +506,18 @@ void unpack_sym(int n, const double *u, double *M) {
 
 extern "C" {
 
+int graft_read_stream(const void *src, int64_t bytes, uint32_t *sink, graft_stream_t stream) {
+  if (!src || !sink) return fail(GRAFT_ERR_INVALID_ARG, "graft_read_stream: NULL argument");
+  if (bytes <= 0 || (bytes & 15) != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_read_stream: bytes %lld is not a positive multiple of 16",
+                static_cast<long long>(bytes));
+  if ((reinterpret_cast<uintptr_t>(src) & 15) != 0 || (reinterpret_cast<uintptr_t>(sink) & 3) != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_read_stream: misaligned src or sink");
+  hipError_t e = graft::launch_read_stream(src, bytes, sink, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graft_read_stream");
+  return GRAFT_OK;
+}
+
 int graft_saba_fit(const graft_saba_replay *log, const float *phi_init, int32_t max_iter,
                    float *phi_out, float *c_out, double *stats, graft_stream_t stream) {
   if (!log || !phi_init || !phi_out || !c_out)

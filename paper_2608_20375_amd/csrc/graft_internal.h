@@ -17,6 +17,7 @@ constexpr int kMaxScoreDim = 64;
 constexpr int kTdesMaxLossBlocks = 512;
 constexpr int kFitSums = 25;        // replay sums: SSE, J^T J (10), J^T r (4), X^T X (6), X^T y (3), y^T y
 constexpr int kFitMaxBlocks = 1024;
+constexpr int kReadSinkWords = GRAFT_READ_STREAM_SINK_WORDS;
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -316,6 +317,10 @@ hipError_t launch_replay_sums(int T, int nb, const int32_t *budgets, const float
                               const int32_t *prefix, const float *accepted, const float *latency,
                               const double phi[4], double tau_min, int with_cost,
                               const double c[3], double *partial, double *out, hipStream_t stream);
+
+// Plain read of bytes (a multiple of 16) at src (16-byte aligned); the sink
+// holds kReadSinkWords words.
+hipError_t launch_read_stream(const void *src, int64_t bytes, uint32_t *sink, hipStream_t stream);
 
 // Number of splits per row used by the logits pass for a given row count.
 int logits_splits(const graft_dims &d, int rows);
