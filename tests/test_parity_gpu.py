@@ -188,6 +188,32 @@ def test_round_parity(wid, mode):
     ctx.close()
 
 
+EDGE_SHAPES = [
+    # K, score dim m, embedding dim
+    (1, 8, 16),       # K = 1
+    (5, 30, 32),      # m % 4 != 0: the VALU path
+    (13, 20, 32),     # ragged parents and children inside one MFMA tile
+    (33, 64, 64),     # three column tiles, m = 64
+    (64, 64, 64),     # the largest K and m
+]
+
+
+@pytest.mark.parametrize("K,m,E", EDGE_SHAPES)
+@pytest.mark.parametrize("mode", ["literal", "paper"])
+def test_edge_score_shapes(K, m, E, mode):
+    """Edge scores (and the trees selected on them) at candidate counts and
+    score dimensions that the workloads above do not reach."""
+    _say("edge shapes", K, m, E, mode)
+    w = S.workload(0, batch=3, L=5, V=3000, K=K, n_max=128, fixed_budget=100, emb_dim=E, rank=m)
+    inp, sc, sp, results = WL.audited_round(w, 0, mode, seqs=None)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    end_to_end_check(w, g, inp, results)
+    staged_check(w, g, sc, sp, inp, range(w.batch))
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
 def test_budgets_spread_under_saba():
     """SABA picks several distinct budgets across the batch of workload 2."""
     w = S.workload(2)
