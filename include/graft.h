@@ -195,6 +195,16 @@ GRAFT_API int graft_set_saba(graft_ctx *ctx, const graft_saba_desc *desc /* host
  * are the accepted lengths of the previous rounds of sequence b. */
 GRAFT_API int graft_set_history(graft_ctx *ctx, int32_t batch, const int32_t *init, graft_stream_t stream);
 
+/* Copies the acceptance-history ring of the first `batch` sequences out (a
+ * checkpoint of the decoding state that feeds hist_t of the SABA state, Sec.
+ * SABA): ring [batch, hist_window] holds the stored accepted lengths in slot
+ * order, pos [batch] (or NULL) the slot the next graft_accept with
+ * update_history writes.  Both are device memory owned by the caller; the
+ * copies are ordered on `stream`.  GRAFT_ERR_INVALID_ARG for a NULL ring, a
+ * batch outside 1..max_batch or a context without a history ring. */
+GRAFT_API int graft_get_history(graft_ctx *ctx, int32_t batch, int32_t *ring, int32_t *pos,
+                                graft_stream_t stream);
+
 /* One round of draft-tree construction for the batch (steps 1-5 above). */
 GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host */,
                      const graft_tree_out *out /* host */, graft_stream_t stream);

@@ -21,6 +21,7 @@ _lib = None
 
 EXPORTED_SYMBOLS = (
     "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
+    "graft_get_history",
     "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
     "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
     "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create", "graft_tdes_destroy",
@@ -125,6 +126,7 @@ def lib():
         L.graft_set_scorer.argtypes = [vp, C.POINTER(ScorerDesc), vp]
         L.graft_set_saba.argtypes = [vp, C.POINTER(SabaDesc)]
         L.graft_set_history.argtypes = [vp, i32, vp, vp]
+        L.graft_get_history.argtypes = [vp, i32, vp, vp, vp]
         L.graft_build_tree.argtypes = [vp, C.POINTER(RoundIn), C.POINTER(TreeOut), vp]
         L.graft_accept.argtypes = [vp, i32, vp, vp, vp, C.POINTER(Targets), vp, vp, vp, i32, vp]
         L.graft_get_device_status.argtypes = [vp, vp]
@@ -152,6 +154,7 @@ def lib():
         L.graft_last_error.argtypes = []
         L.graft_last_error.restype = C.c_char_p
         for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
+                  "graft_get_history",
                   "graft_build_tree", "graft_accept", "graft_get_device_status",
                   "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
                   "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create",
@@ -172,6 +175,28 @@ def _ptr(t, dtype=None, name="tensor"):
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
     return t.data_ptr()
+
+
+def _need(t, name, *dims):
+    """Raises ValueError unless tensor t (when given) has one extent per entry of
+    dims: an int is the exact extent, a 1-tuple (n,) the least one.  Every
+    kernel indexes its buffers by the context's sizes and the call's batch, so
+    a buffer that is too small would be read or written out of bounds."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch tensor" % name)
+    ok = t.dim() == len(dims) and all(
+        (s >= d[0]) if isinstance(d, tuple) else (s == d) for s, d in zip(t.shape, dims))
+    if not ok:
+        want = ", ".join((">=%d" % d[0]) if isinstance(d, tuple) else str(d) for d in dims)
+        raise ValueError("%s must be [%s], got %s" % (name, want, list(t.shape)))
+
+
+def _batch_of(t, name):
+    if not isinstance(t, torch.Tensor) or t.dim() < 1:
+        raise ValueError("%s must be a tensor whose first extent is the batch" % name)
+    return int(t.shape[0])
 
 
 def _stream():
@@ -195,6 +220,7 @@ class TreeBuffers:
         i32 = dict(dtype=torch.int32, device=dev)
         f32 = dict(dtype=torch.float32, device=dev)
         self.batch = batch
+        self.sizes = (L, K, N)
         self.budget = torch.empty(batch, **i32)
         self.n_nodes = torch.empty(batch, **i32)
         self.tokens = torch.empty(batch, N, **i32)
@@ -246,6 +272,13 @@ class Context:
             pass
 
     def set_scorer(self, emb, g_parent, g_child, depth_emb=None, scale=1.0, beta=1.0, center=0):
+        dm = self.dims
+        _need(emb, "emb", dm.vocab, (1,))
+        E = int(emb.shape[1])
+        _need(g_parent, "g_parent", E, (1,))
+        m = int(g_parent.shape[1])
+        _need(g_child, "g_child", E, m)
+        _need(depth_emb, "depth_emb", dm.num_pos, m)
         d = ScorerDesc(_ptr(emb, torch.float32, "emb"), _ptr(g_parent, torch.float32, "g_parent"),
                        _ptr(g_child, torch.float32, "g_child"),
                        _ptr(depth_emb, torch.float32, "depth_emb"), emb.shape[1],
@@ -260,17 +293,41 @@ class Context:
         _check(lib().graft_set_saba(self._h, C.byref(d)), "graft_set_saba")
 
     def set_history(self, init):
+        _need(init, "init", (1,), self.dims.hist_window)
         _check(lib().graft_set_history(self._h, init.shape[0], _ptr(init, torch.int32, "init"),
                                        _stream()), "graft_set_history")
+
+    def get_history(self, batch: int):
+        """(ring [batch, hist_window], pos [batch]) int32 copies of the device
+        acceptance-history ring."""
+        dev = torch.device("cuda", torch.cuda.current_device())
+        ring = torch.empty(batch, self.dims.hist_window, dtype=torch.int32, device=dev)
+        pos = torch.empty(batch, dtype=torch.int32, device=dev)
+        _check(lib().graft_get_history(self._h, int(batch), _ptr(ring, torch.int32, "ring"),
+                                       _ptr(pos, torch.int32, "pos"), _stream()),
+               "graft_get_history")
+        return ring, pos
 
     def build_tree(self, logits, root_token, base_pos, prefix_len=None, hist=None,
                    fixed_budget=None, hidden=None, out: TreeBuffers | None = None,
                    **want) -> TreeBuffers:
         """hidden: optional [batch, L, H] bf16 bit patterns of the drafter's hidden
         states; with them the SABA state uses the degeneration signal."""
-        batch = logits.shape[0]
+        dm = self.dims
+        batch = _batch_of(logits, "logits")
+        _need(logits, "logits", batch, dm.num_pos, dm.vocab)
+        for name, t in (("root_token", root_token), ("base_pos", base_pos),
+                        ("prefix_len", prefix_len), ("hist", hist), ("fixed_budget", fixed_budget)):
+            _need(t, name, batch)
+        if root_token is None or base_pos is None:
+            raise ValueError("root_token and base_pos are required")
+        _need(hidden, "hidden", batch, dm.num_pos, (1,))
         if out is None:
             out = TreeBuffers(self, batch, **want)
+        elif out.batch < batch or out.sizes != (dm.num_pos, dm.top_k, dm.max_nodes):
+            raise ValueError("out holds %d sequences of sizes (L, K, max_nodes) = %s; this call "
+                             "needs %d of %s" % (out.batch, out.sizes, batch,
+                                                 (dm.num_pos, dm.top_k, dm.max_nodes)))
         if logits.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
             raise TypeError("logits must hold bf16 bit patterns")
         if hidden is not None and hidden.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
@@ -286,7 +343,17 @@ class Context:
 
     def accept(self, n_nodes, tokens, parents, target_root=None, target_node=None,
                target_depth=None, update_history=False, acc_len=None, acc_nodes=None, bonus=None):
-        batch = n_nodes.shape[0]
+        dm = self.dims
+        batch = _batch_of(n_nodes, "n_nodes")
+        _need(n_nodes, "n_nodes", batch)
+        _need(tokens, "tokens", (batch,), dm.max_nodes)
+        _need(parents, "parents", (batch,), dm.max_nodes)
+        _need(target_root, "target_root", (batch,))
+        _need(target_node, "target_node", (batch,), dm.max_nodes)
+        _need(target_depth, "target_depth", (batch,), dm.num_pos + 1)
+        _need(acc_len, "acc_len", (batch,))
+        _need(acc_nodes, "acc_nodes", (batch,), dm.num_pos)
+        _need(bonus, "bonus", (batch,))
         dev = n_nodes.device
         acc_len = torch.empty(batch, dtype=torch.int32, device=dev) if acc_len is None else acc_len
         acc_nodes = (torch.empty(batch, self.dims.num_pos, dtype=torch.int32, device=dev)
@@ -306,7 +373,15 @@ class Context:
 
     def synth_node_targets(self, seed, root_token, n_nodes, tokens, parents, topk_ids,
                            target_root=None, target_node=None):
-        batch = n_nodes.shape[0]
+        dm = self.dims
+        batch = _batch_of(n_nodes, "n_nodes")
+        _need(n_nodes, "n_nodes", batch)
+        _need(root_token, "root_token", (batch,))
+        _need(tokens, "tokens", (batch,), dm.max_nodes)
+        _need(parents, "parents", (batch,), dm.max_nodes)
+        _need(topk_ids, "topk_ids", (batch,), dm.num_pos, dm.top_k)
+        _need(target_root, "target_root", (batch,))
+        _need(target_node, "target_node", (batch,), dm.max_nodes)
         dev = n_nodes.device
         if target_root is None:
             target_root = torch.empty(batch, dtype=torch.int32, device=dev)
@@ -325,8 +400,10 @@ class Context:
         masks.  bias: [batch, max_nodes, >= max_nodes] tensor or strided view with
         unit stride along the last dimension (e.g. the tree columns of a wider
         bias); allocated as [batch, max_nodes, max_nodes] when None."""
-        batch = n_nodes.shape[0]
+        batch = _batch_of(n_nodes, "n_nodes")
         N = self.dims.max_nodes
+        _need(n_nodes, "n_nodes", batch)
+        _need(mask, "mask", (batch,), N, (N + 63) // 64)
         if bias is None:
             bias = torch.empty(batch, N, N, dtype=dtype, device=n_nodes.device)
         if bias.dtype not in (torch.float32, torch.bfloat16):
@@ -347,15 +424,20 @@ class Context:
         [planes, batch, rows, width] tensors (any dtype, unit stride along width);
         dst defaults to src (compaction in place)."""
         dst = src if dst is None else dst
+        batch = _batch_of(acc_len, "acc_len")
+        _need(acc_len, "acc_len", batch)
+        _need(acc_nodes, "acc_nodes", (batch,), self.dims.num_pos)
+        # node indices reach max_nodes - 1 in src; at most L rows are written in dst
+        _need(src, "src", (1,), (batch,), (self.dims.max_nodes,), (1,))
+        _need(dst, "dst", (1,), (batch,), (self.dims.num_pos,), (1,))
         for name, t in (("src", src), ("dst", dst)):
-            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dim() != 4:
-                raise TypeError("%s must be a 4-d CUDA tensor [planes, batch, rows, width]" % name)
+            if t.device.type != "cuda":
+                raise TypeError("%s must be a CUDA (HIP) tensor [planes, batch, rows, width]" % name)
             if t.stride(3) != 1:
                 raise ValueError("%s must have unit stride along its last dimension" % name)
         if src.dtype != dst.dtype or src.shape[0] != dst.shape[0] or src.shape[3] != dst.shape[3]:
             raise ValueError("src and dst must agree in dtype, planes and width")
         es = src.element_size()
-        batch = acc_len.shape[0]
         _check(lib().graft_commit_accepted(
             self._h, batch, _ptr(acc_len, torch.int32, "acc_len"),
             _ptr(acc_nodes, torch.int32, "acc_nodes"), src.data_ptr(), dst.data_ptr(),

@@ -232,6 +232,24 @@ int graft_set_history(graft_ctx *ctx, int32_t batch, const int32_t *init, graft_
   return GRAFT_OK;
 }
 
+int graft_get_history(graft_ctx *ctx, int32_t batch, int32_t *ring, int32_t *pos,
+                      graft_stream_t stream) {
+  if (!ctx || !ring) return fail(GRAFT_ERR_INVALID_ARG, "graft_get_history: NULL argument");
+  if (batch < 1 || batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_get_history: batch %d outside 1..%d", batch,
+                ctx->dims.max_batch);
+  if (!ctx->has_history)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_get_history: no history ring (graft_set_history)");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(ring, ctx->hist_ring,
+                                sizeof(int32_t) * batch * ctx->dims.hist_window,
+                                hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && pos)
+    e = hipMemcpyAsync(pos, ctx->hist_pos, sizeof(int32_t) * batch, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "graft_get_history");
+  return GRAFT_OK;
+}
+
 int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
                      graft_stream_t stream) {
   if (!ctx || !in || !out) return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: NULL argument");

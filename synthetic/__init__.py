@@ -32,9 +32,9 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "workload", "bf16_from_f32", "f32_from_bf16",
-    "gen_sequence_logits", "gen_round", "gen_scorer", "saba_params",
+    "gen_sequence_logits", "gen_sequence", "put_sequence", "gen_round", "gen_scorer", "saba_params",
     "hist_ring_init", "node_targets", "splitmix64", "NODE_TARGET_P_NUM", "gen_hidden",
-    "gen_traces", "gen_replay",
+    "gen_sequence_hidden", "gen_traces", "gen_replay",
 ]
 
 HIST_WINDOW = 4
@@ -164,6 +164,22 @@ def hist_ring_init(w: Workload, rnd: int = 0, attempts=None) -> np.ndarray:
     return out
 
 
+def gen_sequence(w: Workload, rnd: int, b: int, attempt: int = 0,
+                 with_targets: bool = True) -> dict:
+    """The per-round inputs of sequence b alone (draw `attempt`): logits [L, V]
+    bf16 bits, boosted ids, root token, prefix length, the initial history
+    window and, with per-depth targets, target_depth [L + 1]."""
+    logits, boost = gen_sequence_logits(w, rnd, b, attempt)
+    g = _rng(w, rnd, b, attempt, 3)
+    root = int(g.integers(0, w.V))
+    prefix = int(g.integers(64, 4097))
+    out = dict(logits=logits, boost_ids=boost, root_token=root, prefix_len=prefix,
+               hist_ring=_rng(w, rnd, b, attempt, 2).integers(0, 17))
+    if with_targets and w.targets == "depth":
+        out["target_depth"] = _depth_targets(w, rnd, b, attempt, boost)
+    return out
+
+
 def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = True,
               seqs=None) -> dict:
     """All per-round inputs for the batch (numpy, host memory).
@@ -183,13 +199,9 @@ def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = Tru
     ring = hist_ring_init(w, rnd, attempts)
 
     def one(b):
-        a = int(attempts[b])
-        logits[b], boost[b] = gen_sequence_logits(w, rnd, b, a)
-        g = _rng(w, rnd, b, a, 3)
-        root[b] = g.integers(0, w.V)
-        prefix[b] = g.integers(64, 4097)
-        if with_targets and w.targets == "depth":
-            tdepth[b] = _depth_targets(w, rnd, b, a, boost[b])
+        one = gen_sequence(w, rnd, b, int(attempts[b]), with_targets)
+        put_sequence(dict(logits=logits, boost_ids=boost, root_token=root, prefix_len=prefix,
+                          target_depth=tdepth), b, one)
 
     seqs = list(seqs)
     if len(seqs) > 1 and w.L * w.V * len(seqs) > (1 << 22):
@@ -210,6 +222,34 @@ def gen_round(w: Workload, rnd: int = 0, attempts=None, with_targets: bool = Tru
     return out
 
 
+def put_sequence(batch: dict, b: int, one: dict) -> None:
+    """Writes sequence b's draw (from gen_sequence) into the batch arrays of a
+    gen_round result; the derived base position, history window and hist are
+    refreshed when the batch holds them."""
+    for k in ("logits", "boost_ids", "target_depth"):
+        if k in one and k in batch:
+            batch[k][b] = one[k]
+    batch["root_token"][b] = one["root_token"]
+    batch["prefix_len"][b] = one["prefix_len"]
+    if "base_pos" in batch:
+        batch["base_pos"][b] = one["prefix_len"] - 1
+    if "hist_ring" in batch:
+        batch["hist_ring"][b] = one["hist_ring"]
+        batch["hist"][b] = np.float32(np.float64(one["hist_ring"]))
+
+
+def gen_sequence_hidden(w: Workload, rnd: int, b: int, hidden_dim: int = 4096,
+                        attempt: int = 0) -> np.ndarray:
+    """Drafter hidden states of sequence b alone: [L, H] bf16 bits (see gen_hidden)."""
+    L, H = w.L, int(hidden_dim)
+    ramp = 0.5 + 2.5 * np.arange(L, dtype=np.float32) / max(L - 1, 1)
+    g = _rng(w, rnd, b, int(attempt), 4)
+    c = g.standard_normal(H, dtype=np.float32)
+    n = g.standard_normal((L, H), dtype=np.float32)
+    s_b = np.float32(g.uniform(0.3, 1.5))
+    return bf16_from_f32((s_b * ramp)[:, None] * c[None, :] + n)
+
+
 def gen_hidden(w: Workload, rnd: int = 0, hidden_dim: int = 4096, attempts=None,
                seqs=None) -> np.ndarray:
     """Drafter hidden states [batch, L, H] as bf16 bits, one per drafted position.
@@ -224,13 +264,8 @@ def gen_hidden(w: Workload, rnd: int = 0, hidden_dim: int = 4096, attempts=None,
     attempts = np.zeros(B, dtype=np.int64) if attempts is None else np.asarray(attempts)
     seqs = range(B) if seqs is None else seqs
     out = np.zeros((B, L, H), dtype=np.uint16)
-    ramp = 0.5 + 2.5 * np.arange(L, dtype=np.float32) / max(L - 1, 1)
     for b in seqs:
-        g = _rng(w, rnd, b, int(attempts[b]), 4)
-        c = g.standard_normal(H, dtype=np.float32)
-        n = g.standard_normal((L, H), dtype=np.float32)
-        s_b = np.float32(g.uniform(0.3, 1.5))
-        out[b] = bf16_from_f32((s_b * ramp)[:, None] * c[None, :] + n)
+        out[b] = gen_sequence_hidden(w, rnd, b, H, int(attempts[b]))
     return out
 
 

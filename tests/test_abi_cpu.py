@@ -91,3 +91,82 @@ def test_ctypes_layout_matches_header(tmp_path):
             assert getattr(m[t], f).offset == int(v), k
         else:
             assert C.sizeof(m[k]) == int(v), k
+
+
+def _unbound_context(batch=4, L=3, V=100, K=2, N=32, window=4):
+    """A Context object with sizes but no library handle: the binding's shape
+    checks run (and raise) before anything reaches the library or a device."""
+    ctx = G.Context.__new__(G.Context)
+    ctx.dims = G.Dims(batch, L, V, K, N, window)
+    ctx._h = None
+    ctx._keep = []
+    return ctx
+
+
+def test_binding_rejects_mismatched_shapes_before_any_call():
+    torch = pytest.importorskip("torch")
+    ctx = _unbound_context()
+    i32 = dict(dtype=torch.int32)
+    z = lambda *s, **kw: torch.zeros(*s, **(kw or i32))
+    logits = z(2, 3, 100, dtype=torch.int16)
+    r2 = z(2)
+    bad_build = [
+        dict(logits=z(2, 4, 100, dtype=torch.int16), root_token=r2, base_pos=r2),   # L
+        dict(logits=z(2, 3, 99, dtype=torch.int16), root_token=r2, base_pos=r2),    # V
+        dict(logits=z(2, 300, dtype=torch.int16), root_token=r2, base_pos=r2),      # rank
+        dict(logits=logits, root_token=z(1), base_pos=r2),
+        dict(logits=logits, root_token=r2, base_pos=z(3)),
+        dict(logits=logits, root_token=r2, base_pos=r2, prefix_len=z(1)),
+        dict(logits=logits, root_token=r2, base_pos=r2, hist=z(1, dtype=torch.float32)),
+        dict(logits=logits, root_token=r2, base_pos=r2, fixed_budget=z(2, 1)),
+        dict(logits=logits, root_token=r2, base_pos=r2, hidden=z(2, 2, 8, dtype=torch.int16)),
+        dict(logits=logits, root_token=None, base_pos=r2),
+    ]
+    for kw in bad_build:
+        with pytest.raises(ValueError):
+            ctx.build_tree(**kw)
+    # output buffers made for fewer sequences or other sizes
+    small = G.TreeBuffers.__new__(G.TreeBuffers)
+    small.batch, small.sizes = 1, (3, 2, 32)
+    with pytest.raises(ValueError):
+        ctx.build_tree(logits, r2, r2, fixed_budget=r2, out=small)
+    other = G.TreeBuffers.__new__(G.TreeBuffers)
+    other.batch, other.sizes = 4, (3, 2, 64)
+    with pytest.raises(ValueError):
+        ctx.build_tree(logits, r2, r2, fixed_budget=r2, out=other)
+
+    n = z(2)
+    tk = z(2, 32)
+    bad_accept = [
+        dict(tokens=z(2, 31), parents=tk, target_depth=z(2, 4)),
+        dict(tokens=tk, parents=z(1, 32), target_depth=z(2, 4)),
+        dict(tokens=tk, parents=tk, target_depth=z(2, 3)),
+        dict(tokens=tk, parents=tk, target_depth=z(1, 4)),
+        dict(tokens=tk, parents=tk, target_root=z(2), target_node=z(2, 16)),
+        dict(tokens=tk, parents=tk, target_root=z(1), target_node=tk),
+        dict(tokens=tk, parents=tk, target_depth=z(2, 4), acc_nodes=z(2, 2)),
+        dict(tokens=tk, parents=tk, target_depth=z(2, 4), acc_len=z(1)),
+        dict(tokens=tk, parents=tk, target_depth=z(2, 4), bonus=z(1)),
+    ]
+    for kw in bad_accept:
+        with pytest.raises(ValueError):
+            ctx.accept(n, **kw)
+
+    emb = z(100, 8, dtype=torch.float32)
+    g = z(8, 4, dtype=torch.float32)
+    for args in ((z(99, 8, dtype=torch.float32), g, g, None),
+                 (emb, z(7, 4, dtype=torch.float32), g, None),
+                 (emb, g, z(8, 5, dtype=torch.float32), None),
+                 (emb, g, g, z(2, 4, dtype=torch.float32))):
+        with pytest.raises(ValueError):
+            ctx.set_scorer(*args)
+    with pytest.raises(ValueError):
+        ctx.set_history(z(2, 3))
+    with pytest.raises(ValueError):
+        ctx.synth_node_targets(1, r2, n, tk, tk, z(2, 3, 1))
+    with pytest.raises(ValueError):
+        ctx.mask_to_bias(n, z(2, 32, 2, dtype=torch.int64), bias=z(2, 32, 32,
+                                                                    dtype=torch.float32))
+    with pytest.raises(ValueError):
+        ctx.commit_accepted(n, z(2, 3), z(1, 2, 16, 16, dtype=torch.uint8),
+                            z(1, 2, 32, 16, dtype=torch.uint8))

@@ -136,9 +136,6 @@ def test_tdes_centering_and_beta():
         rows = 1 if l == 0 else K
         # centered residuals sum to zero over the children of each parent
         assert np.abs(resid[l, :rows].sum(axis=1)).max() < 1e-13
-        # and equal beta * (f - mean f)
-        ref = 0.3 * (f[l, :rows] - f[l, :rows].mean(axis=1, keepdims=True))
-        assert np.allclose(resid[l, :rows], ref, atol=1e-14)
     # beta = 0 -> DDTree edge score log q (eq. ddtree-path-score)
     sc0 = dict(sc, beta=0.0)
     e0, _ = oracle.edge_scores(oracle.make_params(L, K, 16, V, sc0), cand, logq, 3)
@@ -162,6 +159,57 @@ def test_tdes_parent_only_terms_cancel_under_centering():
         # uncentered f is the same for every child of a parent but not zero
         assert np.allclose(f[l, :rows], f[l, :rows, :1], atol=1e-14)
     assert np.abs(f[:, 0, 0]).max() > 1e-4
+
+
+def test_tdes_depth_embedding_closed_forms():
+    """Where u_d enters eq. tdes-bitower: it is added to both towers.
+    (a) G_p = G_c = 0: f = s |u_d|^2 / sqrt(m) for every pair (a u_d on one
+        tower only would give 0);
+    (b) G_c = 0: f = s (e_p G_p + u_d) . u_d / sqrt(m), one value per parent
+        (u_d on the child tower only would drop the |u_d|^2 term, on the parent
+        tower only would give 0);
+    (c) G_p = 0: f = s u_d . (e_c G_c + u_d) / sqrt(m), one value per child;
+    with centering on, (a)'s constant cancels and the edge score is log q."""
+    g = np.random.default_rng(17)
+    V, E, m, L, K = 90, 5, 4, 4, 3
+    sc = _scorer(g, V, E, m, L, 1.3, 0.7, 0)
+    cand, logq = _cands(g, V, L, K)
+    root = 11
+    emb = sc["emb"].astype(np.float64)
+    u = sc["depth_emb"].astype(np.float64)
+    s_m = 1.3 / math.sqrt(m)
+    zero = np.zeros_like(sc["g_parent"])
+
+    # (a)
+    sa = dict(sc, g_parent=zero, g_child=zero)
+    edge, f = oracle.edge_scores(oracle.make_params(L, K, 16, V, sa), cand, logq, root)
+    for l in range(L):
+        rows = 1 if l == 0 else K
+        want = s_m * float(u[l] @ u[l])
+        assert want > 1e-3
+        assert np.allclose(f[l, :rows], want, rtol=1e-12, atol=0)
+        assert np.allclose(edge[l, :rows], logq[l][None, :] + 0.7 * want, rtol=1e-13, atol=1e-14)
+    ec, _ = oracle.edge_scores(oracle.make_params(L, K, 16, V, dict(sa, center=1)), cand, logq,
+                               root)
+    for l in range(L):
+        rows = 1 if l == 0 else K
+        assert np.allclose(ec[l, :rows], logq[l][None, :], rtol=0, atol=1e-14)
+
+    # (b) and (c)
+    gp = sc["g_parent"].astype(np.float64)
+    gc = sc["g_child"].astype(np.float64)
+    _, fb = oracle.edge_scores(oracle.make_params(L, K, 16, V, dict(sc, g_child=zero)), cand,
+                               logq, root)
+    _, fc = oracle.edge_scores(oracle.make_params(L, K, 16, V, dict(sc, g_parent=zero)), cand,
+                               logq, root)
+    for l in range(L):
+        parents = [root] if l == 0 else list(cand[l - 1])
+        for p, pt in enumerate(parents):
+            want_b = s_m * float((emb[pt] @ gp + u[l]) @ u[l])
+            assert np.allclose(fb[l, p], want_b, rtol=1e-12, atol=1e-15)
+            for c in range(K):
+                want_c = s_m * float(u[l] @ (emb[cand[l, c]] @ gc + u[l]))
+                assert fc[l, p, c] == pytest.approx(want_c, rel=1e-12, abs=1e-15)
 
 
 def test_tdes_scale_and_dim_normalisation():

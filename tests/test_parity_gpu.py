@@ -10,6 +10,7 @@ budget) is bit-exact on every sequence.
 """
 import os
 import sys
+import time
 
 import numpy as np
 import pytest
@@ -132,10 +133,8 @@ def test_logits_pass_topk_and_stats(shape):
 
 
 # ---------------------------------------------------------------------------
-# whole round, every workload (full sizes; oracle on audited sequences)
+# whole round, every workload (full sizes; the oracle on every sequence)
 # ---------------------------------------------------------------------------
-
-AUDIT = {0: None, 1: None, 2: None, 3: [0, 17, 40, 63], 4: [0, 77, 127]}
 
 
 @pytest.mark.parametrize("wid", [0, 1, 2, 3, 4])
@@ -143,8 +142,12 @@ AUDIT = {0: None, 1: None, 2: None, 3: [0, 17, 40, 63], 4: [0, 77, 127]}
 def test_round_parity(wid, mode):
     w = S.workload(wid)
     _say("round parity workload", wid, mode)
-    inp, sc, sp, results = WL.audited_round(w, 0, mode, seqs=AUDIT[wid])
-    _say("  inputs ready; attempts", inp["attempts"][list(results)].tolist())
+    t0 = time.time()
+    inp, sc, sp, results = WL.audited_round(w, 0, mode)
+    assert len(results) == w.batch
+    _say("  inputs ready in %.1fs (%d oracle threads); attempts per sequence: mean %.2f, max %d"
+         % (time.time() - t0, WL.oracle_threads(), inp["attempts"].mean() + 1,
+            inp["attempts"].max() + 1))
     ctx = WL.gpu_context(w, sc, sp, torch)
     g = WL.gpu_round(ctx, w, inp, torch)
     _say("  gpu done; budgets", g["budget"][:8].tolist(), "nodes", g["n_nodes"][:8].tolist())
@@ -152,49 +155,240 @@ def test_round_parity(wid, mode):
     seqs = range(w.batch)
     staged_check(w, g, sc, sp, inp, seqs)
     saba_check(w, g, sc, sp, inp, seqs)
-    # acceptance
+    acc = accept_check(ctx, w, g, inp, results, w.seed)
+    _say("  accepted nodes per sequence: mean %.2f, max %d" % (acc.mean(), acc.max()))
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
+def accept_check(ctx, w, g, inp, results, seed, update_history=False):
+    """The acceptance walk on the GPU's trees against the oracle's walk, every
+    sequence: per-depth targets from the inputs, or per-node targets drawn on
+    the device (graft_synth_node_targets) and checked against their CPU twin on
+    the oracle's trees.  Returns the accepted lengths."""
+    out = g["_out"]
     if w.targets == "depth":
-        acc = ctx.accept(g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
-                         target_depth=torch.from_numpy(inp["target_depth"]).cuda())
+        acc = ctx.accept(out.n_nodes, out.tokens, out.parents,
+                         target_depth=torch.from_numpy(inp["target_depth"]).cuda(),
+                         update_history=update_history)
         acc = [a.cpu().numpy() for a in acc]
-        for b in seqs:
+        for b in range(w.batch):
             a, nodes, bonus = oracle.accept(g["n_nodes"][b], g["tokens"][b], g["parents"][b],
                                             w.L, target_depth=inp["target_depth"][b])
-            assert acc[0][b] == a and acc[2][b] == bonus
-            assert np.array_equal(acc[1][b], nodes)
-    else:
-        tr, tn = ctx.synth_node_targets(w.seed, torch.from_numpy(inp["root_token"]).cuda(),
-                                        g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
-                                        g["_out"].topk_ids)
-        acc = ctx.accept(g["_out"].n_nodes, g["_out"].tokens, g["_out"].parents,
-                         target_root=tr, target_node=tn)
-        acc = [a.cpu().numpy() for a in acc]
-        tr, tn = tr.cpu().numpy(), tn.cpu().numpy()
-        for b, r in results.items():
-            n = r["n_nodes"]
-            par, tok, dep = r["parents"][:n], r["tokens"][:n], r["depth"][:n]
-            ptok = np.where(par < 0, inp["root_token"][b], r["tokens"][np.maximum(par, 0)])
-            ref_nodes = S.node_targets(w.seed, b, dep, ptok, tok, r["topk_ids"], w.V, w.L, w.K)
-            ref_root = S.node_targets(w.seed, b, [0], [-1], [inp["root_token"][b]], r["topk_ids"],
-                                      w.V, w.L, w.K)[0]
-            assert tr[b] == ref_root
-            assert np.array_equal(tn[b][:n], ref_nodes)
-            a, nodes, bonus = oracle.accept(n, r["tokens"], r["parents"], w.L, int(ref_root),
-                                            target_node=np.concatenate(
-                                                [ref_nodes, -np.ones(w.n_max - n, np.int32)]))
-            assert acc[0][b] == a and acc[2][b] == bonus
-            assert np.array_equal(acc[1][b], nodes)
+            assert acc[0][b] == a and acc[2][b] == bonus, b
+            assert np.array_equal(acc[1][b], nodes), b
+        return acc[0]
+    tr, tn = ctx.synth_node_targets(seed, torch.from_numpy(inp["root_token"]).cuda(),
+                                    out.n_nodes, out.tokens, out.parents, out.topk_ids)
+    acc = ctx.accept(out.n_nodes, out.tokens, out.parents, target_root=tr, target_node=tn,
+                     update_history=update_history)
+    acc = [a.cpu().numpy() for a in acc]
+    tr, tn = tr.cpu().numpy(), tn.cpu().numpy()
+    assert len(results) == w.batch
+    for b, r in results.items():
+        n = r["n_nodes"]
+        par, tok, dep = r["parents"][:n], r["tokens"][:n], r["depth"][:n]
+        ptok = np.where(par < 0, inp["root_token"][b], r["tokens"][np.maximum(par, 0)])
+        ref_nodes = S.node_targets(seed, b, dep, ptok, tok, r["topk_ids"], w.V, w.L, w.K)
+        ref_root = S.node_targets(seed, b, [0], [-1], [inp["root_token"][b]], r["topk_ids"],
+                                  w.V, w.L, w.K)[0]
+        assert tr[b] == ref_root, b
+        assert np.array_equal(tn[b][:n], ref_nodes), b
+        a, nodes, bonus = oracle.accept(n, r["tokens"], r["parents"], w.L, int(ref_root),
+                                        target_node=np.concatenate(
+                                            [ref_nodes, -np.ones(w.n_max - n, np.int32)]))
+        assert acc[0][b] == a and acc[2][b] == bonus, b
+        assert np.array_equal(acc[1][b], nodes), b
+    return acc[0]
+
+
+CHAIN_ROUNDS = 5
+
+
+def test_chained_rounds_w4():
+    """Five consecutive full-size rounds of workload 4 (batch 128, L 32, V
+    151936, K 32), as its 50-round run chains them: each round's acceptance
+    pushes acc_len into the device history ring (window 4, so the fifth push
+    wraps to slot 0) and the next round's SABA reads the ring's mean as hist_t.
+    Round r is audited with the oracle after round r-1's acceptance, with the
+    oracle's hist equal to the ring mean; budgets, trees, masks, acceptance and
+    the ring contents are compared every round."""
+    w = S.workload(4)
+    sc, sp = WL.scorer_inputs(w, "literal"), WL.saba_inputs(w)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    ring = S.hist_ring_init(w)
+    ctx.set_history(torch.from_numpy(ring).cuda())
+    pos = np.zeros(w.batch, np.int64)
+    for rnd in range(CHAIN_ROUNDS):
+        t0 = time.time()
+        hist = ring.astype(np.float64).mean(axis=1)
+        inp, _, _, results = WL.audited_round(w, rnd, "literal", hist=hist)
+        _say("chained w4 round %d: audited in %.1fs, attempts mean %.2f" %
+             (rnd, time.time() - t0, inp["attempts"].mean() + 1))
+        g = WL.gpu_round(ctx, w, inp, torch, use_ring=True)
+        assert (g["saba_state"][:, 2] == hist.astype(np.float32)).all()
+        end_to_end_check(w, g, inp, results)
+        staged_check(w, g, sc, sp, inp, range(w.batch))
+        a = accept_check(ctx, w, g, inp, results, w.seed + rnd, update_history=True)
+        for b in range(w.batch):
+            ring[b, pos[b]] = a[b]
+        pos = (pos + 1) % S.HIST_WINDOW
+        dring, dpos = (x.cpu().numpy() for x in ctx.get_history(w.batch))
+        assert np.array_equal(dring, ring)
+        assert np.array_equal(dpos, pos)
+        _say("  accepted mean %.2f; ring pos %d" % (a.mean(), pos[0]))
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
+def _peaked_chain(b, logits):
+    """Even sequences: the rank-1 candidate of every depth gets +14, so its
+    probability is about 1 and the chain of rank-1 candidates reaches depth L."""
+    if b % 2:
+        return
+    x = S.f32_from_bf16(logits)
+    top = np.argmax(x, axis=1)
+    x[np.arange(x.shape[0]), top] += 14.0
+    logits[:] = S.bf16_from_f32(x)
+
+
+def test_deep_acceptance_w3():
+    """Acceptance walks that follow each tree's deepest root path to its end
+    (full-size workload 3; even sequences have a dominant chain, so their trees
+    reach depth L = 16 and the bonus token comes from target_depth[L]).  The
+    path's nodes lie past the first 64 canonical indices, so the walk scans
+    several 64-node chunks.  Per-depth and per-node targets."""
+    w = S.workload(3)
+    inp, sc, sp, results = WL.audited_round(w, 0, "literal", transform=_peaked_chain)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    end_to_end_check(w, g, inp, results)
+    rng = np.random.default_rng(4242)
+    td = rng.integers(0, w.V, size=(w.batch, w.L + 1)).astype(np.int32)
+    tnode = rng.integers(0, w.V, size=(w.batch, w.n_max)).astype(np.int32)
+    troot = rng.integers(0, w.V, size=w.batch).astype(np.int32)
+    want = []
+    for b in range(w.batch):
+        n = int(g["n_nodes"][b])
+        depth = np.zeros(n, np.int64)
+        for i in range(n):
+            p = g["parents"][b][i]
+            depth[i] = 1 if p < 0 else depth[p] + 1
+        leaf = int(np.argmax(depth))               # deepest node, lowest index first
+        path = []
+        j = leaf
+        while j >= 0:
+            path.append(j)
+            j = int(g["parents"][b][j])
+        path = path[::-1]
+        D = len(path)
+        if b % 2 == 0:
+            assert D == w.L, (b, D)
+        for k, j in enumerate(path):
+            td[b, k] = g["tokens"][b][j]
+        # per-node: the root's target is the path's first token, node path[k]'s
+        # the token of path[k + 1]
+        troot[b] = g["tokens"][b][path[0]]
+        for k in range(D - 1):
+            tnode[b, path[k]] = g["tokens"][b][path[k + 1]]
+        tnode[b, n:] = -1
+        want.append((D, path))
+    assert max(p[-1] for _, p in want) >= 64
+    out = g["_out"]
+    for mode in ("depth", "node"):
+        if mode == "depth":
+            acc = ctx.accept(out.n_nodes, out.tokens, out.parents,
+                             target_depth=torch.from_numpy(td).cuda())
+        else:
+            acc = ctx.accept(out.n_nodes, out.tokens, out.parents,
+                             target_root=torch.from_numpy(troot).cuda(),
+                             target_node=torch.from_numpy(tnode).cuda())
+        a, nodes, bonus = (x.cpu().numpy() for x in acc)
+        for b, (D, path) in enumerate(want):
+            assert a[b] == D, (mode, b, a[b], D)
+            assert np.array_equal(nodes[b][:D], path) and (nodes[b][D:] == -1).all()
+            ra, rn, rb = (oracle.accept(g["n_nodes"][b], g["tokens"][b], g["parents"][b], w.L,
+                                        target_depth=td[b]) if mode == "depth" else
+                          oracle.accept(g["n_nodes"][b], g["tokens"][b], g["parents"][b], w.L,
+                                        int(troot[b]), target_node=tnode[b]))
+            assert (ra, rb) == (a[b], bonus[b]) and np.array_equal(rn, nodes[b])
+            if mode == "depth":
+                assert bonus[b] == td[b, D]
+            else:
+                assert bonus[b] == tnode[b, path[-1]]
+    _say("deep acceptance: depths", sorted(set(D for D, _ in want)))
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
+def _frontier_check(w, g, b, logq):
+    """The selected set of sequence b is the first N prefixes of the whole trie
+    under the heap order (higher path score, then smaller depth, then the
+    smaller token path), with path scores the fp64 sums of the GPU's fp32 log q:
+    it is prefix-closed and no unselected child of a selected prefix (or of the
+    root) precedes its last selected prefix.  Valid because every score is <= 0,
+    so a child never precedes its parent."""
+    n = int(g["n_nodes"][b])
+    tok, par = g["tokens"][b][:n], g["parents"][b][:n]
+    ids = g["topk_ids"][b]
+    path, score = [], []
+    for i in range(n):
+        p = int(par[i])
+        d = 1 if p < 0 else len(path[p]) + 1
+        slot = int(np.flatnonzero(ids[d - 1] == tok[i])[0])
+        path.append((() if p < 0 else path[p]) + (int(tok[i]),))
+        score.append((0.0 if p < 0 else score[p]) + float(logq[d - 1][slot]))
+        assert score[i] == g["node_scores"][b][i]
+    key = lambda s, pth: (-s, len(pth), pth)
+    worst_selected = max(key(s, p) for s, p in zip(score, path))
+    chosen = set(path)
+    best_left = None
+    for parent_path, parent_score in [((), 0.0)] + list(zip(path, score)):
+        d = len(parent_path)
+        if d == w.L:
+            continue
+        for slot in range(w.K):
+            cp = parent_path + (int(ids[d][slot]),)
+            if cp in chosen:
+                continue
+            k = key(parent_score + float(logq[d][slot]), cp)
+            best_left = k if best_left is None or k < best_left else best_left
+    assert best_left is None or worst_selected < best_left
+
+
+def test_ddtree_mode_beta0_w3():
+    """DDTree mode on the HIP path (eq. ddtree-path-score): the paper-mode scorer
+    with beta = 0 leaves every edge score equal to log q of the child, so the
+    tree is the top-budget product-of-probability tree.  Exact ties between
+    sums of bf16 log-probabilities are common here; end-to-end parity holds on
+    sequences re-drawn until the boundary has a margin, staged parity on every
+    sequence, and each tree is checked to be the first N prefixes of the trie."""
+    w = S.workload(3)
+    sc = WL.scorer_inputs(w, "paper")
+    sc["beta"] = 0.0
+    inp, sc, sp, results = WL.audited_round(w, 0, "paper", scorer=sc)
+    _say("beta = 0: attempts per sequence mean %.2f" % (inp["attempts"].mean() + 1))
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    end_to_end_check(w, g, inp, results)
+    staged_check(w, g, sc, sp, inp, range(w.batch))
+    for b in range(w.batch):
+        lq = g["topk_logq"][b]
+        e = g["edge_scores"][b]
+        assert (e[0, 0] == lq[0]).all()
+        assert (e[1:] == lq[1:, None, :]).all()
+        _frontier_check(w, g, b, lq)
     assert ctx.device_status() == 0
     ctx.close()
 
 
 EDGE_SHAPES = [
     # K, score dim m, embedding dim
-    (1, 8, 16),       # K = 1
-    (5, 30, 32),      # m % 4 != 0: the VALU path
-    (13, 20, 32),     # ragged parents and children inside one MFMA tile
-    (33, 64, 64),     # three column tiles, m = 64
-    (64, 64, 64),     # the largest K and m
+    (1, 8, 16),       # K = 1: one lane per parent run, 64 parents a pass
+    (5, 30, 32),      # m % 4 != 0: the element-wise gathers instead of 16-byte ones
+    (13, 20, 32),     # K = 13 in runs of 16 lanes (3 idle lanes per parent), 4 parents a pass
+    (33, 64, 64),     # K = 33 in one 64-lane run per parent (31 idle lanes), m = 64
+    (64, 64, 64),     # the largest K and m: every lane a child, one parent a pass
 ]
 
 
@@ -325,6 +519,18 @@ def test_abi_errors_on_device():
     tk = torch.zeros(2, w.n_max, dtype=torch.int32, device="cuda")
     with pytest.raises(G.GraftError):
         ctx.accept(n, tk, tk)
+    # buffers of the wrong shape are refused by the binding before any launch
+    with pytest.raises(ValueError):
+        ctx.build_tree(logits[:, :, :-8], root, root, fixed_budget=root)
+    with pytest.raises(ValueError):
+        ctx.build_tree(logits, root[:1], root, fixed_budget=root)
+    with pytest.raises(ValueError):
+        ctx.accept(n, tk[:, :-1], tk, target_depth=torch.zeros(2, w.L + 1, dtype=torch.int32,
+                                                                device="cuda"))
+    with pytest.raises(ValueError):
+        ctx.accept(n, tk, tk, target_depth=torch.zeros(2, w.L, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):
+        ctx.set_scorer(T(sc["emb"][:-1]), T(sc["g_parent"]), T(sc["g_child"]), None, 1.0, 1.0, 0)
     ctx.close()
 
 

@@ -2,8 +2,11 @@
 C ABI) with the CPU oracle.
 
 Tolerances.  The sums are fp64 on both sides (fixed order here, numpy's
-there); the optimum of the cost fit is a 3 x 3 solve, so c agrees to 1e-9
-relative.  Both gain fits stop at the optimum of the same objective; on a
+there).  The cost fit is linear least squares on the columns [1, B,
+B * prefix]; scaled to unit columns their condition number is about 5.7 on
+these logs, so the library's fp64 normal equations and the oracle's SVD solve
+agree to about 1e-12 relative.  The library returns c in fp32, which adds at
+most 2**-24 (6e-8) relative: c is compared at 1e-7 relative.  Both gain fits stop at the optimum of the same objective; on a
 noisy log that optimum is flat to about 1e-6 relative in phi (the oracle pins
 measure convergence agreement at that level), so phi is compared at 1e-4
 relative and the objective at 1e-7 relative.  On an exact log both recover
@@ -34,7 +37,7 @@ def test_fit_matches_oracle(T, noise, seed):
     ref = F.fit(r["budgets"], r["state"].astype(np.float64), r["prefix"], r["accepted"],
                 r["latency"], r["tau_min"], phi0)
     assert got["converged"]
-    np.testing.assert_allclose(got["c"], ref["c"], rtol=1e-6)
+    np.testing.assert_allclose(got["c"], ref["c"], rtol=1e-7)
     assert got["cost_sse"] == pytest.approx(ref["cost_sse"], rel=1e-6, abs=1e-9)
     np.testing.assert_allclose(got["phi"], ref["phi"], rtol=1e-4)
     assert got["gain_sse"] == pytest.approx(ref["gain_sse"], rel=1e-7, abs=1e-12)

@@ -7,12 +7,15 @@ never the HIP path.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 import oracle
 import synthetic as S
 
-MAX_ATTEMPTS = 12
+MAX_ATTEMPTS = 24
 
 
 def scorer_inputs(w, mode):
@@ -33,45 +36,67 @@ def saba_inputs(w):
     return sp
 
 
+def oracle_threads() -> int:
+    """Worker threads for the oracle: the cores this process may use, at most 16
+    (the host share of one GPU).  The oracle's C calls release the GIL."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def audited_round(w, rnd=0, mode="literal", seqs=None, with_targets=True, hidden_dim=None,
-                  phi=None):
+                  phi=None, hist=None, transform=None, scorer=None):
     """Inputs for the whole batch; sequences in `seqs` (default: all) are
     audited with the oracle and re-drawn until their decisions are robust.
     With hidden_dim, drafter hidden states [batch, L, hidden_dim] are drawn too
     and the SABA state uses their degeneration signal.  phi overrides the SABA
-    state weights.
+    state weights; hist (fp64 [batch]) overrides the history feature the
+    oracle sees (a chained round reads it from the device ring); transform(b,
+    logits) may rewrite a draw's logits [L, V] in place before the audit;
+    scorer replaces the workload's scorer of `mode`.
+    Sequences are drawn and audited in parallel (one sequence per task).
     Returns (inputs, scorer, saba, {b: oracle result})."""
-    sc = scorer_inputs(w, mode)
+    sc = scorer_inputs(w, mode) if scorer is None else scorer
     sp = saba_inputs(w)
     if phi is not None and sp is not None:
         sp["phi"] = np.asarray(phi, np.float32)
-    seqs = list(range(w.batch)) if seqs is None else list(seqs)
+    audit = set(range(w.batch)) if seqs is None else set(seqs)
     attempts = np.zeros(w.batch, np.int64)
-    inp = S.gen_round(w, rnd, attempts, with_targets=with_targets)
+    inp = S.gen_round(w, rnd, attempts, with_targets=with_targets, seqs=[])
     if hidden_dim:
-        inp["hidden"] = S.gen_hidden(w, rnd, hidden_dim, attempts)
+        inp["hidden"] = np.zeros((w.batch, w.L, hidden_dim), np.uint16)
     P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
-    results = {}
-    for b in seqs:
-        for a in range(MAX_ATTEMPTS):
-            if a:
-                attempts[b] = a
-                one = S.gen_round(w, rnd, attempts, with_targets=with_targets, seqs=[b])
-                for k, v in one.items():
-                    if isinstance(v, np.ndarray) and v.shape and v.shape[0] == w.batch:
-                        inp[k][b] = v[b]
-                if hidden_dim:
-                    inp["hidden"][b] = S.gen_hidden(w, rnd, hidden_dim, attempts, seqs=[b])[b]
-            r = oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b],
-                                      inp["base_pos"][b], inp["prefix_len"][b],
-                                      inp["fixed_budget"][b] if "fixed_budget" in inp else 0,
-                                      float(inp["hist"][b]),
-                                      inp["hidden"][b] if hidden_dim else None)
+    fixed = w.fixed_budget if w.budget_mode == "fixed" else 0
+
+    def one(b):
+        for a in range(MAX_ATTEMPTS if b in audit else 1):
+            d = S.gen_sequence(w, rnd, b, a, with_targets)
+            if transform is not None:
+                transform(b, d["logits"])
+            h = S.gen_sequence_hidden(w, rnd, b, hidden_dim, a) if hidden_dim else None
+            if b not in audit:
+                return a, d, h, None
+            hv = float(np.float32(d["hist_ring"])) if hist is None else float(hist[b])
+            r = oracle.build_sequence(P, d["logits"], d["root_token"], d["prefix_len"] - 1,
+                                      d["prefix_len"], fixed, hv, h)
             if oracle.sequence_ok(r, w.L):
-                break
-        else:
-            raise RuntimeError("no robust draw for sequence %d" % b)
-        results[b] = r
+                return a, d, h, r
+        raise RuntimeError("no robust draw for sequence %d" % b)
+
+    with ThreadPoolExecutor(oracle_threads()) as ex:
+        done = list(ex.map(one, range(w.batch)))
+    results = {}
+    for b, (a, d, h, r) in enumerate(done):
+        attempts[b] = a
+        S.put_sequence(inp, b, d)
+        if hidden_dim:
+            inp["hidden"][b] = h
+        if r is not None:
+            results[b] = r
+    if hist is not None:
+        inp["hist"] = np.asarray(hist, np.float32)
     inp["attempts"] = attempts
     return inp, sc, sp, results
 
