@@ -209,6 +209,35 @@ GRAFT_API int graft_get_history(graft_ctx *ctx, int32_t batch, int32_t *ring, in
 GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host */,
                      const graft_tree_out *out /* host */, graft_stream_t stream);
 
+/* Size of the library's static scratch array used by graft_build_tree_static:
+ * 24 MiB, the per-round intermediates of a batch of 128 sequences at L = 32
+ * and K = 32 (about 18 MB).  Each GPU the library runs on holds one copy until
+ * the process ends. */
+#define GRAFT_STATIC_SCRATCH_BYTES (24ll * 1024 * 1024)
+
+/* graft_build_tree without any device allocation: for callers that cannot
+ * allocate memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, outputs and errors as
+ * graft_build_tree, and the same kernels, but the round's intermediates
+ * (split-row partials, candidates, row statistics, edge rows, id ranks,
+ * positive flags, hidden-state cosines) live in a static device array of
+ * GRAFT_STATIC_SCRATCH_BYTES per GPU instead of the context's workspace; the
+ * context still provides the scorer's projections, SABA parameters, the
+ * history ring and the device status.  The bytes needed grow with the batch:
+ * 256-byte aligned parts of B*L*K*(4 + 4 + 1) + B*L*(12 + 1) + B*L*K*K*4 +
+ * 4*B*max(L - 1, 1) bytes, plus 8*(3 + K) bytes per split-row partial when
+ * rows are split (fewer than about 1024 rows).  A batch whose need exceeds
+ * the array returns GRAFT_ERR_UNSUPPORTED before anything is enqueued.  The
+ * call allocates nothing (the array's address on each device is resolved
+ * once, when a context is created there).  Every call on one GPU shares that
+ * GPU's array, which keeps the last call's contents: calls that overlap on one
+ * GPU (on different streams, or from different contexts) race; calls ordered
+ * on one stream do not.  Nothing in the array needs clearing between calls:
+ * each round writes every intermediate before reading it. */
+GRAFT_API int graft_build_tree_static(graft_ctx *ctx, const graft_round_in *in /* host */,
+                                      const graft_tree_out *out /* host */,
+                                      graft_stream_t stream);
+
 /* Greedy acceptance walk over the trees of the batch.
  *   n_nodes [batch], tokens/parents [batch, max_nodes] as written by
  *   graft_build_tree; acc_len [batch], acc_nodes [batch, L] (canonical node

@@ -22,8 +22,8 @@ _lib = None
 EXPORTED_SYMBOLS = (
     "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
     "graft_get_history",
-    "graft_build_tree", "graft_accept", "graft_get_device_status", "graft_synth_node_targets",
-    "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
+    "graft_build_tree", "graft_build_tree_static", "graft_accept", "graft_get_device_status",
+    "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
     "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create", "graft_tdes_destroy",
     "graft_tdes_param_count", "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit",
     "graft_read_stream",
@@ -128,6 +128,7 @@ def lib():
         L.graft_set_history.argtypes = [vp, i32, vp, vp]
         L.graft_get_history.argtypes = [vp, i32, vp, vp, vp]
         L.graft_build_tree.argtypes = [vp, C.POINTER(RoundIn), C.POINTER(TreeOut), vp]
+        L.graft_build_tree_static.argtypes = [vp, C.POINTER(RoundIn), C.POINTER(TreeOut), vp]
         L.graft_accept.argtypes = [vp, i32, vp, vp, vp, C.POINTER(Targets), vp, vp, vp, i32, vp]
         L.graft_get_device_status.argtypes = [vp, vp]
         L.graft_synth_node_targets.argtypes = [vp, i32, C.c_uint64, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -155,7 +156,8 @@ def lib():
         L.graft_last_error.restype = C.c_char_p
         for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
                   "graft_get_history",
-                  "graft_build_tree", "graft_accept", "graft_get_device_status",
+                  "graft_build_tree", "graft_build_tree_static", "graft_accept",
+                  "graft_get_device_status",
                   "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
                   "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create",
                   "graft_tdes_step", "graft_tdes_device_status", "graft_saba_fit",
@@ -310,9 +312,11 @@ class Context:
 
     def build_tree(self, logits, root_token, base_pos, prefix_len=None, hist=None,
                    fixed_budget=None, hidden=None, out: TreeBuffers | None = None,
-                   **want) -> TreeBuffers:
+                   static_scratch=False, **want) -> TreeBuffers:
         """hidden: optional [batch, L, H] bf16 bit patterns of the drafter's hidden
-        states; with them the SABA state uses the degeneration signal."""
+        states; with them the SABA state uses the degeneration signal.
+        static_scratch: call graft_build_tree_static (no device allocation in the
+        library; pass preallocated `out` to allocate nothing here either)."""
         dm = self.dims
         batch = _batch_of(logits, "logits")
         _need(logits, "logits", batch, dm.num_pos, dm.vocab)
@@ -337,8 +341,8 @@ class Context:
                     _ptr(prefix_len, torch.int32, "prefix_len"), _ptr(hist, torch.float32, "hist"),
                     _ptr(fixed_budget, torch.int32, "fixed_budget"), _ptr(hidden, None, "hidden"),
                     0 if hidden is None else int(hidden.shape[-1]))
-        _check(lib().graft_build_tree(self._h, C.byref(r), C.byref(out._struct), _stream()),
-               "graft_build_tree")
+        fn = "graft_build_tree_static" if static_scratch else "graft_build_tree"
+        _check(getattr(lib(), fn)(self._h, C.byref(r), C.byref(out._struct), _stream()), fn)
         return out
 
     def accept(self, n_nodes, tokens, parents, target_root=None, target_node=None,

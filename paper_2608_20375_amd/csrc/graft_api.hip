@@ -6,11 +6,67 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "graft_internal.h"
 
+// The per-round intermediates of graft_build_tree_static live here instead of
+// in a context's workspace: one copy per GPU, held until the process ends.
+// Host code never uses this name as an address; it resolves the device address
+// once per device with hipGetSymbolAddress (static_scratch_on) and passes that.
+static __device__ __align__(256) uint64_t scratch[GRAFT_STATIC_SCRATCH_BYTES / 8];
+
+namespace graft {
+
+int64_t carve_round_scratch(const graft_dims &d, int batch, int64_t part_slots, char *base,
+                            RoundScratch *ws) {
+  const int64_t B = batch, L = d.num_pos, K = d.top_k;
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) -> char * {
+    char *p = base ? base + off : nullptr;
+    off += (bytes + 255) & ~int64_t{255};
+    return p;
+  };
+  RoundScratch w{};
+  w.part_slots = part_slots;
+  w.part_stats = reinterpret_cast<double *>(take(part_slots * 3 * int64_t{sizeof(double)}));
+  w.part_keys = reinterpret_cast<uint64_t *>(take(part_slots * K * int64_t{sizeof(uint64_t)}));
+  w.topk_ids = reinterpret_cast<int32_t *>(take(B * L * K * int64_t{sizeof(int32_t)}));
+  w.topk_logq = reinterpret_cast<float *>(take(B * L * K * int64_t{sizeof(float)}));
+  w.row_stats = reinterpret_cast<float *>(take(B * L * 3 * int64_t{sizeof(float)}));
+  w.edge_rows = reinterpret_cast<float *>(take(B * L * K * K * int64_t{sizeof(float)}));
+  w.id_rank = reinterpret_cast<uint8_t *>(take(B * L * K));
+  w.positive = reinterpret_cast<uint8_t *>(take(B * L));
+  w.adj_cos = reinterpret_cast<float *>(take(B * (L > 1 ? L - 1 : 1) * int64_t{sizeof(float)}));
+  if (ws) *ws = w;
+  return off;
+}
+
+}  // namespace graft
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device dev, which must be current: resolved
+// on first use per device and kept for the life of the process.
+hipError_t static_scratch_on(int dev, char **out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = static_cast<char *>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 thread_local char g_err[512] = "";
 
@@ -47,15 +103,7 @@ void prof_release(graft_ctx *c) {
 void free_ctx(graft_ctx *c) {
   if (!c) return;
   prof_release(c);
-  (void)hipFree(c->part_stats);
-  (void)hipFree(c->part_keys);
-  (void)hipFree(c->topk_ids);
-  (void)hipFree(c->topk_logq);
-  (void)hipFree(c->row_stats);
-  (void)hipFree(c->edge_rows);
-  (void)hipFree(c->id_rank);
-  (void)hipFree(c->positive);
-  (void)hipFree(c->adj_cos);
+  (void)hipFree(c->ws_base);
   (void)hipFree(c->proj_parent);
   (void)hipFree(c->proj_child);
   (void)hipFree(c->depth_emb);
@@ -63,6 +111,70 @@ void free_ctx(graft_ctx *c) {
   (void)hipFree(c->hist_pos);
   (void)hipFree(c->error_flag);
   delete c;
+}
+
+// Steps 1-5 of a round (graft_build_tree, graft_build_tree_static) with the
+// per-round intermediates in ws; `who` names the entry point in messages.
+int build_tree_with(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+                    const graft::RoundScratch &ws, graft_stream_t stream, const char *who) {
+  if (!ctx || !in || !out) return fail(GRAFT_ERR_INVALID_ARG, "%s: NULL argument", who);
+  const graft_dims &d = ctx->dims;
+  if (in->batch < 1 || in->batch > d.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "%s: batch %d outside 1..%d", who, in->batch,
+                d.max_batch);
+  if (!in->logits || !in->root_token || !in->base_pos)
+    return fail(GRAFT_ERR_INVALID_ARG, "%s: logits, root_token and base_pos are required", who);
+  if ((reinterpret_cast<uintptr_t>(in->logits) & 15u) != 0)
+    return fail(GRAFT_ERR_INVALID_ARG, "%s: logits must be 16-byte aligned", who);
+  if (!out->budget || !out->n_nodes || !out->tokens || !out->parents || !out->pos_ids)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "%s: budget, n_nodes, tokens, parents and pos_ids are required", who);
+  if (!ctx->has_scorer)
+    return fail(GRAFT_ERR_INVALID_ARG, "%s: no scorer installed (graft_set_scorer)", who);
+  if (!in->fixed_budget && !ctx->has_saba)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "%s: no fixed budgets and no SABA parameters (graft_set_saba)", who);
+  if (in->hidden) {
+    if (in->hidden_dim < 8 || in->hidden_dim > (1 << 20) || (in->hidden_dim & 7) != 0)
+      return fail(GRAFT_ERR_INVALID_ARG, "%s: hidden_dim %d must be a multiple of 8 in 8..1048576",
+                  who, in->hidden_dim);
+    if ((reinterpret_cast<uintptr_t>(in->hidden) & 15u) != 0)
+      return fail(GRAFT_ERR_INVALID_ARG, "%s: hidden must be 16-byte aligned", who);
+  }
+  if (!in->hist && !in->fixed_budget && !ctx->has_history)
+    return fail(GRAFT_ERR_INVALID_ARG,
+                "%s: no hist input and no history ring (graft_set_history)", who);
+  char what[96];
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipEvent_t *ev = nullptr;
+  if (ctx->prof_build && ctx->prof_nbuild < ctx->prof_cap) ev = ctx->prof_build + 4 * ctx->prof_nbuild++;
+  if (ev) (void)hipEventRecord(ev[0], s);
+  hipError_t e = graft::launch_logits_pass(ctx, ws, in->batch, in->logits, out, s);
+  if (e != hipSuccess) {
+    snprintf(what, sizeof what, "%s: logits pass", who);
+    return hip_fail(e, what);
+  }
+  if (ev) (void)hipEventRecord(ev[1], s);
+  if (in->hidden) {
+    e = graft::launch_degen(ctx, ws, in->batch, in->hidden, in->hidden_dim, out->adj_cos, s);
+    if (e != hipSuccess) {
+      snprintf(what, sizeof what, "%s: hidden-state cosines", who);
+      return hip_fail(e, what);
+    }
+  }
+  e = graft::launch_edge_scores(ctx, ws, in, out, s);
+  if (e != hipSuccess) {
+    snprintf(what, sizeof what, "%s: edge scores and budget", who);
+    return hip_fail(e, what);
+  }
+  if (ev) (void)hipEventRecord(ev[2], s);
+  e = graft::launch_select(ctx, ws, in, out, s);
+  if (e != hipSuccess) {
+    snprintf(what, sizeof what, "%s: selection", who);
+    return hip_fail(e, what);
+  }
+  if (ev) (void)hipEventRecord(ev[3], s);
+  return GRAFT_OK;
 }
 
 }  // namespace
@@ -109,20 +221,15 @@ int graft_create(const graft_dims *dims, graft_ctx **out) {
   if (!c) return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_create: host allocation failed");
   c->dims = d;
   (void)hipGetDevice(&c->device);
-  const size_t B = d.max_batch, L = d.num_pos, K = d.top_k;
-  c->part_slots = graft::logits_part_slots(d);
-  hipError_t e = hipSuccess;
+  const size_t B = d.max_batch;
+  const int64_t ws_bytes =
+      graft::carve_round_scratch(d, d.max_batch, graft::logits_part_slots(d), nullptr, nullptr);
+  hipError_t e = dalloc(&c->ws_base, static_cast<size_t>(ws_bytes));
+  if (e == hipSuccess)
+    graft::carve_round_scratch(d, d.max_batch, graft::logits_part_slots(d), c->ws_base, &c->ws);
+  if (e == hipSuccess) e = static_scratch_on(c->device, &c->static_scratch);
 #define GRAFT_ALLOC(ptr, n)              \
   if (e == hipSuccess) e = dalloc(&(ptr), (n));
-  GRAFT_ALLOC(c->part_stats, static_cast<size_t>(c->part_slots) * 3);
-  GRAFT_ALLOC(c->part_keys, static_cast<size_t>(c->part_slots) * K);
-  GRAFT_ALLOC(c->topk_ids, B * L * K);
-  GRAFT_ALLOC(c->topk_logq, B * L * K);
-  GRAFT_ALLOC(c->row_stats, B * L * 3);
-  GRAFT_ALLOC(c->edge_rows, B * L * K * K);
-  GRAFT_ALLOC(c->id_rank, B * L * K);
-  GRAFT_ALLOC(c->positive, B * L);
-  GRAFT_ALLOC(c->adj_cos, B * (L > 1 ? L - 1 : 1));
   GRAFT_ALLOC(c->hist_ring, B * d.hist_window);
   GRAFT_ALLOC(c->hist_pos, B);
   GRAFT_ALLOC(c->error_flag, 1);
@@ -252,52 +359,33 @@ int graft_get_history(graft_ctx *ctx, int32_t batch, int32_t *ring, int32_t *pos
 
 int graft_build_tree(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
                      graft_stream_t stream) {
-  if (!ctx || !in || !out) return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: NULL argument");
-  const graft_dims &d = ctx->dims;
-  if (in->batch < 1 || in->batch > d.max_batch)
-    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: batch %d outside 1..%d", in->batch,
-                d.max_batch);
-  if (!in->logits || !in->root_token || !in->base_pos)
-    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: logits, root_token and base_pos are required");
-  if ((reinterpret_cast<uintptr_t>(in->logits) & 15u) != 0)
-    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: logits must be 16-byte aligned");
-  if (!out->budget || !out->n_nodes || !out->tokens || !out->parents || !out->pos_ids)
-    return fail(GRAFT_ERR_INVALID_ARG,
-                "graft_build_tree: budget, n_nodes, tokens, parents and pos_ids are required");
-  if (!ctx->has_scorer)
-    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: no scorer installed (graft_set_scorer)");
-  if (!in->fixed_budget && !ctx->has_saba)
-    return fail(GRAFT_ERR_INVALID_ARG,
-                "graft_build_tree: no fixed budgets and no SABA parameters (graft_set_saba)");
-  if (in->hidden) {
-    if (in->hidden_dim < 8 || in->hidden_dim > (1 << 20) || (in->hidden_dim & 7) != 0)
-      return fail(GRAFT_ERR_INVALID_ARG,
-                  "graft_build_tree: hidden_dim %d must be a multiple of 8 in 8..1048576",
-                  in->hidden_dim);
-    if ((reinterpret_cast<uintptr_t>(in->hidden) & 15u) != 0)
-      return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: hidden must be 16-byte aligned");
-  }
-  if (!in->hist && !in->fixed_budget && !ctx->has_history)
-    return fail(GRAFT_ERR_INVALID_ARG,
-                "graft_build_tree: no hist input and no history ring (graft_set_history)");
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  hipEvent_t *ev = nullptr;
-  if (ctx->prof_build && ctx->prof_nbuild < ctx->prof_cap) ev = ctx->prof_build + 4 * ctx->prof_nbuild++;
-  if (ev) (void)hipEventRecord(ev[0], s);
-  hipError_t e = graft::launch_logits_pass(ctx, in->batch, in->logits, out, s);
-  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: logits pass");
-  if (ev) (void)hipEventRecord(ev[1], s);
-  if (in->hidden) {
-    e = graft::launch_degen(ctx, in->batch, in->hidden, in->hidden_dim, out->adj_cos, s);
-    if (e != hipSuccess) return hip_fail(e, "graft_build_tree: hidden-state cosines");
-  }
-  e = graft::launch_edge_scores(ctx, in, out, s);
-  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: edge scores and budget");
-  if (ev) (void)hipEventRecord(ev[2], s);
-  e = graft::launch_select(ctx, in, out, s);
-  if (e != hipSuccess) return hip_fail(e, "graft_build_tree: selection");
-  if (ev) (void)hipEventRecord(ev[3], s);
-  return GRAFT_OK;
+  if (!ctx) return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree: NULL argument");
+  return build_tree_with(ctx, in, out, ctx->ws, stream, "graft_build_tree");
+}
+
+int graft_build_tree_static(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+                            graft_stream_t stream) {
+  if (!ctx || !in || !out)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree_static: NULL argument");
+  if (in->batch < 1 || in->batch > ctx->dims.max_batch)
+    return fail(GRAFT_ERR_INVALID_ARG, "graft_build_tree_static: batch %d outside 1..%d",
+                in->batch, ctx->dims.max_batch);
+  if (!ctx->static_scratch)
+    return fail(GRAFT_ERR_HIP, "graft_build_tree_static: no static scratch on device %d",
+                ctx->device);
+  const int rows = in->batch * ctx->dims.num_pos;
+  const int splits = graft::logits_splits(ctx->dims, rows);
+  const int64_t parts = splits > 1 ? static_cast<int64_t>(rows) * splits : 0;
+  const int64_t need = graft::carve_round_scratch(ctx->dims, in->batch, parts, nullptr, nullptr);
+  if (need > GRAFT_STATIC_SCRATCH_BYTES)
+    return fail(GRAFT_ERR_UNSUPPORTED,
+                "graft_build_tree_static: a batch of %d needs %lld bytes of scratch; the static "
+                "buffer holds %lld (use graft_build_tree or a smaller batch)",
+                in->batch, static_cast<long long>(need),
+                static_cast<long long>(GRAFT_STATIC_SCRATCH_BYTES));
+  graft::RoundScratch ws;
+  graft::carve_round_scratch(ctx->dims, in->batch, parts, ctx->static_scratch, &ws);
+  return build_tree_with(ctx, in, out, ws, stream, "graft_build_tree_static");
 }
 
 int graft_accept(graft_ctx *ctx, int32_t batch, const int32_t *n_nodes, const int32_t *tokens,

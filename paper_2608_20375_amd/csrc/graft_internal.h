@@ -216,23 +216,39 @@ struct ScorerParams {
   int32_t has_depth_emb;
 };
 
+// Per-round intermediates of graft_build_tree, passed from one kernel of the
+// round to the next: written by each round before they are read, so nothing
+// in them carries over between rounds or needs clearing.
+struct RoundScratch {
+  int64_t part_slots;      // split-row partials available (rows * splits)
+  double *part_stats;      // [part_slots][3]: mL (log2-scaled max), S, T2
+  uint64_t *part_keys;     // [part_slots][K]
+  int32_t *topk_ids;       // [batch, L, K]
+  float *topk_logq;        // [batch, L, K]
+  float *row_stats;        // [batch, L, 3]: lse, maxprob, entropy
+  float *edge_rows;        // [batch, L, K, K] edge scores: [depth][parent slot][child slot]
+  uint8_t *id_rank;        // [batch, L, K] rank of each candidate's token id in its depth
+  uint8_t *positive;       // [batch, L] 1 if some edge score of that depth is > 0
+  float *adj_cos;          // [batch, max(L - 1, 1)] adjacent hidden-state cosines
+};
+
+// Byte layout of a RoundScratch for `batch` sequences and part_slots split-row
+// partials carved from one buffer at base (every part 256-byte aligned);
+// returns the bytes needed.  With base null only the size is computed.
+int64_t carve_round_scratch(const graft_dims &d, int batch, int64_t part_slots, char *base,
+                            RoundScratch *ws);
+
 }  // namespace graft
 
 struct graft_ctx {
   graft_dims dims;
   int device;
-  // K1 split-row partials
-  int32_t part_slots;
-  double *part_stats;      // [part_slots][3]: mL (log2-scaled max), S, T2
-  uint64_t *part_keys;     // [part_slots][K]
-  // per-round intermediates
-  int32_t *topk_ids;       // [max_batch, L, K]
-  float *topk_logq;        // [max_batch, L, K]
-  float *row_stats;        // [max_batch, L, 3]: lse, maxprob, entropy
-  float *edge_rows;        // [max_batch, L, K, K] edge scores: [depth][parent slot][child slot]
-  uint8_t *id_rank;        // [max_batch, L, K] rank of each candidate's token id in its depth
-  uint8_t *positive;       // [max_batch, L] 1 if some edge score of that depth is > 0
-  float *adj_cos;          // [max_batch, max(L - 1, 1)] adjacent hidden-state cosines
+  // per-round intermediates for max_batch sequences, one device allocation
+  graft::RoundScratch ws;
+  char *ws_base;
+  // the library's static scratch array on this context's device
+  // (graft_build_tree_static), resolved when the context is created
+  char *static_scratch;
   // scorer
   float *proj_parent;      // [V, m]
   float *proj_child;       // [V, m]
@@ -266,15 +282,17 @@ struct graft_tdes {
 namespace graft {
 
 // Launchers (stream-ordered, no synchronization).  They return hipError_t.
-hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
-                              const graft_tree_out *out, hipStream_t stream);
-hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStream_t stream);
-hipError_t launch_degen(graft_ctx *ctx, int batch, const uint16_t *hidden, int hidden_dim,
-                        float *adj_cos_out, hipStream_t stream);
-hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
+hipError_t launch_logits_pass(graft_ctx *ctx, const RoundScratch &ws, int batch,
+                              const uint16_t *logits, const graft_tree_out *out,
                               hipStream_t stream);
-hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
-                         hipStream_t stream);
+hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStream_t stream);
+hipError_t launch_degen(graft_ctx *ctx, const RoundScratch &ws, int batch,
+                        const uint16_t *hidden, int hidden_dim, float *adj_cos_out,
+                        hipStream_t stream);
+hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
+                              const graft_tree_out *out, hipStream_t stream);
+hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
+                         const graft_tree_out *out, hipStream_t stream);
 hipError_t launch_accept(graft_ctx *ctx, int batch, const int32_t *n_nodes,
                          const int32_t *tokens, const int32_t *parents,
                          const graft_targets *t, int32_t *acc_len, int32_t *acc_nodes,

@@ -102,13 +102,14 @@ degen_kernel(const uint16_t *__restrict__ hidden, int L, int H, int runs,
 
 }  // namespace
 
-hipError_t launch_degen(graft_ctx *ctx, int batch, const uint16_t *hidden, int hidden_dim,
-                        float *adj_cos_out, hipStream_t stream) {
+hipError_t launch_degen(graft_ctx *ctx, const RoundScratch &ws, int batch,
+                        const uint16_t *hidden, int hidden_dim, float *adj_cos_out,
+                        hipStream_t stream) {
   const int L = ctx->dims.num_pos;
   if (L < 2) return hipSuccess;
   const int runs = (L - 1 + kPairs - 1) / kPairs;
   hipLaunchKernelGGL(degen_kernel, dim3(static_cast<unsigned>(batch * runs)),
-                     dim3(kDegenThreads), 0, stream, hidden, L, hidden_dim, runs, ctx->adj_cos,
+                     dim3(kDegenThreads), 0, stream, hidden, L, hidden_dim, runs, ws.adj_cos,
                      adj_cos_out);
   return hipGetLastError();
 }

@@ -797,17 +797,18 @@ int logits_part_slots(const graft_dims &d) {
   return static_cast<int>(best > 0 ? best : 1);
 }
 
-hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
-                              const graft_tree_out *out, hipStream_t stream) {
+hipError_t launch_logits_pass(graft_ctx *ctx, const RoundScratch &ws, int batch,
+                              const uint16_t *logits, const graft_tree_out *out,
+                              hipStream_t stream) {
   const graft_dims &d = ctx->dims;
   const int rows = batch * d.num_pos;
   const int splits = logits_splits(d, rows);
-  if (splits > 1 && static_cast<int64_t>(rows) * splits > ctx->part_slots)
+  if (splits > 1 && static_cast<int64_t>(rows) * splits > ws.part_slots)
     return hipErrorInvalidValue;
   RowOut o;
-  o.ids = ctx->topk_ids;
-  o.logq = ctx->topk_logq;
-  o.stats = ctx->row_stats;
+  o.ids = ws.topk_ids;
+  o.logq = ws.topk_logq;
+  o.stats = ws.row_stats;
   o.o_ids = out ? out->topk_ids : nullptr;
   o.o_logq = out ? out->topk_logq : nullptr;
   o.o_lse = out ? out->row_lse : nullptr;
@@ -817,16 +818,16 @@ hipError_t launch_logits_pass(graft_ctx *ctx, int batch, const uint16_t *logits,
   const int64_t V = d.vocab;
   if (d.top_k <= 32) {
     hipLaunchKernelGGL(logits_pass_kernel<128>, grid, dim3(kThreads), 0, stream, logits, V,
-                       splits, d.top_k, ctx->part_stats, ctx->part_keys, o);
+                       splits, d.top_k, ws.part_stats, ws.part_keys, o);
     if (splits > 1)
       hipLaunchKernelGGL(merge_kernel<128>, dim3(rows), dim3(kWave), 0, stream, splits, d.top_k,
-                         ctx->part_stats, ctx->part_keys, o);
+                         ws.part_stats, ws.part_keys, o);
   } else {
     hipLaunchKernelGGL(logits_pass_kernel<256>, grid, dim3(kThreads), 0, stream, logits, V,
-                       splits, d.top_k, ctx->part_stats, ctx->part_keys, o);
+                       splits, d.top_k, ws.part_stats, ws.part_keys, o);
     if (splits > 1)
       hipLaunchKernelGGL(merge_kernel<256>, dim3(rows), dim3(kWave), 0, stream, splits, d.top_k,
-                         ctx->part_stats, ctx->part_keys, o);
+                         ws.part_stats, ws.part_keys, o);
   }
   return hipGetLastError();
 }

@@ -364,19 +364,19 @@ hipError_t launch_projection(graft_ctx *ctx, const graft_scorer_desc *d, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
-                              hipStream_t stream) {
+hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
+                              const graft_tree_out *out, hipStream_t stream) {
   const graft_dims &d = ctx->dims;
   const int batch = in->batch;
   const int32_t *root_token = in->root_token;
   float *edge_out = out->edge_scores;
   SabaArgs sa;
-  sa.row_stats = ctx->row_stats;
+  sa.row_stats = ws.row_stats;
   sa.hist = in->hist;
   sa.hist_ring = ctx->hist_ring;
   sa.prefix_len = in->prefix_len;
   sa.fixed_budget = in->fixed_budget;
-  sa.adj_cos = in->hidden ? ctx->adj_cos : nullptr;
+  sa.adj_cos = in->hidden ? ws.adj_cos : nullptr;
   sa.window = d.hist_window;
   sa.budget = out->budget;
   sa.saba_state = out->saba_state;
@@ -388,10 +388,10 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const graft_round_in *in, const gr
   const dim3 grid(batch * d.num_pos), block(kEdgeThreads);
 #define GRAFT_EDGE(SEG)                                                                        \
   hipLaunchKernelGGL(edge_kernel<SEG>, grid, block, lds, stream, d.num_pos, K, m,            \
-                     static_cast<int64_t>(d.vocab), mdiv4, ctx->topk_ids, ctx->topk_logq,     \
+                     static_cast<int64_t>(d.vocab), mdiv4, ws.topk_ids, ws.topk_logq,       \
                      root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
-                     ctx->scorer, ctx->edge_rows, ctx->id_rank,                               \
-                     ctx->positive, edge_out, ctx->error_flag, sa, ctx->saba)
+                     ctx->scorer, ws.edge_rows, ws.id_rank,                                 \
+                     ws.positive, edge_out, ctx->error_flag, sa, ctx->saba)
   if (K <= 1) GRAFT_EDGE(1);
   else if (K <= 2) GRAFT_EDGE(2);
   else if (K <= 4) GRAFT_EDGE(4);

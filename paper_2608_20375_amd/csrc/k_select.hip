@@ -1112,18 +1112,18 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
 
 }  // namespace
 
-hipError_t launch_select(graft_ctx *ctx, const graft_round_in *in, const graft_tree_out *out,
-                         hipStream_t stream) {
+hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
+                         const graft_tree_out *out, hipStream_t stream) {
   const graft_dims &d = ctx->dims;
   SelectArgs a;
   a.L = d.num_pos;
   a.K = d.top_k;
   a.n_max = d.max_nodes;
   a.words = (d.max_nodes + 63) / 64;
-  a.edge_rows = ctx->edge_rows;
-  a.topk_ids = ctx->topk_ids;
-  a.id_rank = ctx->id_rank;
-  a.positive = ctx->positive;
+  a.edge_rows = ws.edge_rows;
+  a.topk_ids = ws.topk_ids;
+  a.id_rank = ws.id_rank;
+  a.positive = ws.positive;
   a.base_pos = in->base_pos;
   a.budget = out->budget;
   a.n_nodes = out->n_nodes;
