@@ -14,8 +14,11 @@ the logits pass against the HBM roofline, its duration from HIP events
 recorded around every stage while the same K rounds run a second time (each
 event adds the same few microseconds of stream time: that cost, measured as
 the difference between the two passes per event, is subtracted from every
-stage, and the events stay out of the headline figure); and the CPU oracle
-timed on a bounded sample on this host.
+stage, and the events stay out of the headline figure), beside the duration
+the committed rocprofv3 summary of the same command reports; the CPU oracle
+timed on bounded samples on this host (one thread, and every core of the
+process's share over sequences); and, after the headline, the batch-128
+workload's 50 rounds chained through the device history ring ("config4").
 """
 from __future__ import annotations
 
@@ -65,28 +68,63 @@ def stored_traffic(workload: int):
         return None
 
 
-def cpu_baseline(w, inp, sc, sp, seconds: float):
+def cpu_baseline(w, inp, sc, sp, seconds: float, threads: int = 1):
+    """The oracle (plain C, fp64) on this host: whole sequences of the timed
+    round (row statistics, top-K, edge scores, budget, selection, emission,
+    acceptance walk) until `seconds` have passed, over `threads` threads (one
+    sequence per task; the oracle's calls release the GIL).  Scaled to whole
+    rounds."""
     import oracle
+    import synthetic as S
+    from concurrent.futures import ThreadPoolExecutor
     P = oracle.make_params(w.L, w.K, w.n_max, w.V, sc, sp)
     fb = inp.get("fixed_budget")
+    td = inp.get("target_depth")
+
+    def one(b):
+        r = oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b], inp["base_pos"][b],
+                                  inp["prefix_len"][b], 0 if fb is None else fb[b],
+                                  float(inp["hist"][b]))
+        if td is not None:
+            oracle.accept(r["n_nodes"], r["tokens"], r["parents"], w.L, target_depth=td[b])
+        else:
+            # per-node targets from the synthetic target model's CPU twin, as
+            # the GPU round draws them on the device
+            n = r["n_nodes"]
+            par, tok = r["parents"][:n], r["tokens"][:n]
+            ptok = np.where(par < 0, inp["root_token"][b], r["tokens"][np.maximum(par, 0)])
+            tn = S.node_targets(w.seed, b, r["depth"][:n], ptok, tok, r["topk_ids"], w.V, w.L, w.K)
+            troot = S.node_targets(w.seed, b, [0], [-1], [inp["root_token"][b]], r["topk_ids"],
+                                   w.V, w.L, w.K)[0]
+            oracle.accept(n, r["tokens"], r["parents"], w.L, int(troot),
+                          target_node=np.concatenate([tn, -np.ones(w.n_max - n, np.int32)]))
+        return 1
+
     done = 0
     t0 = time.perf_counter()
-    while done < w.batch:
-        b = done
-        oracle.build_sequence(P, inp["logits"][b], inp["root_token"][b], inp["base_pos"][b],
-                              inp["prefix_len"][b], 0 if fb is None else fb[b],
-                              float(inp["hist"][b]))
-        if w.targets == "depth":
-            pass  # acceptance cost is negligible next to the logits pass
-        done += 1
-        if time.perf_counter() - t0 >= seconds:
-            break
+    with ThreadPoolExecutor(threads) as ex:
+        while True:
+            n = min(threads, w.batch) if threads > 1 else 1
+            done += sum(ex.map(one, [(done + i) % w.batch for i in range(n)]))
+            if time.perf_counter() - t0 >= seconds and done >= threads:
+                break
     el = time.perf_counter() - t0
     rounds_per_s = (done / w.batch) / el
-    return {"value": rounds_per_s, "unit": "rounds/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d sequences of one round (%d rows x %d bf16 logits each), "
-                      "single thread, fp64, scaled to whole rounds" % (done, w.batch, w.L, w.V),
+    return {"value": rounds_per_s, "unit": "rounds/s", "cores": threads, "kind": "oracle",
+            "sample": "%d sequences (%.2f rounds) of the timed round (%d rows x %d bf16 logits "
+                      "each; row statistics, top-K, edges, budget, selection, emission, "
+                      "acceptance), %d thread%s, fp64, scaled to whole rounds" % (
+                          done, done / w.batch, w.L, w.V, threads, "s" if threads > 1 else ""),
             "seconds": el}
+
+
+def host_threads() -> int:
+    """Cores this process may run on, at most 16 (the host share of one GPU)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def time_verifier(ctx, w, tb, acc_len, acc_nodes, steps, torch, dev):
@@ -222,6 +260,164 @@ def time_saba_fit(torch, dev, T=20000, cpu=True):
     return res
 
 
+def run_workload(wid, steps, warmup, rotate, hidden_dim, torch, dev, chain=None):
+    """Times `steps` rounds of workload wid back to back on one stream after
+    `warmup` untimed ones (graft_build_tree + graft_accept over rotating logit
+    buffers), then the same rounds again with the library's stage events, then
+    a plain read of the same buffers.  Per-node workloads chain their rounds
+    through the device history ring (acceptance pushes acc_len, the next
+    round's SABA reads the ring mean)."""
+    import synthetic as S
+    import paper_2608_20375_amd as G
+    w = S.workload(wid)
+    t0 = time.time()
+    inp = S.gen_round(w, 0)
+    sc = S.gen_scorer(w, "literal")
+    sp = S.saba_params(w) if w.budget_mode == "saba" else None
+    log("workload %d: inputs generated in %.1fs" % (wid, time.time() - t0))
+
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    ctx = G.Context(w.batch, w.L, w.V, w.K, w.n_max, S.HIST_WINDOW)
+    ctx.set_scorer(T(sc["emb"]), T(sc["g_parent"]), T(sc["g_child"]),
+                   None if sc["depth_emb"] is None else T(sc["depth_emb"]),
+                   sc["scale"], sc["beta"], sc["center"])
+    if sp is not None:
+        ctx.set_saba(list(sp["grid"]), list(sp["phi"]), sp["tau_min"], sp["c0"], sp["c1"], sp["c2"])
+
+    logit_bytes = w.batch * w.L * w.V * 2
+    R = rotate or max(2, math.ceil((1 << 30) / logit_bytes))
+    base_logits = T(inp["logits"].view(np.int16))
+    bufs = [base_logits] + [base_logits.clone() for _ in range(R - 1)]
+    root, base_pos = T(inp["root_token"]), T(inp["base_pos"])
+    prefix = T(inp["prefix_len"])
+    fixed = T(inp["fixed_budget"]) if "fixed_budget" in inp else None
+    node_mode = w.targets == "node"
+    hist = None if node_mode else T(inp["hist"])
+    if node_mode:
+        ctx.set_history(T(inp["hist_ring"]))
+    tdepth = T(inp["target_depth"]) if not node_mode else None
+    hidden = None
+    if hidden_dim:
+        hidden = T(S.gen_hidden(w, 0, hidden_dim).view(np.int16))
+    tb = G.TreeBuffers(ctx, w.batch)
+    acc_len = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    acc_nodes = torch.empty(w.batch, w.L, dtype=torch.int32, device=dev)
+    bonus = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    troot = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    tnode = torch.empty(w.batch, w.n_max, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+
+    def one_round(i):
+        ctx.build_tree(bufs[i % R], root, base_pos, prefix_len=prefix, hist=hist,
+                       fixed_budget=fixed, hidden=hidden, out=tb)
+        if node_mode:
+            ctx.synth_node_targets(w.seed + i, root, tb.n_nodes, tb.tokens, tb.parents,
+                                   tb.topk_ids, troot, tnode)
+            ctx.accept(tb.n_nodes, tb.tokens, tb.parents, target_root=troot, target_node=tnode,
+                       update_history=True, acc_len=acc_len, acc_nodes=acc_nodes, bonus=bonus)
+        else:
+            ctx.accept(tb.n_nodes, tb.tokens, tb.parents, target_depth=tdepth, acc_len=acc_len,
+                       acc_nodes=acc_nodes, bonus=bonus)
+
+    for i in range(warmup):
+        one_round(i)
+    torch.cuda.synchronize()
+    log("workload %d: warmup done (%d rounds)" % (wid, warmup))
+
+    # timed region: `steps` rounds back to back, bracketed by synchronizations
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_host = time.perf_counter()
+    e0.record()
+    for i in range(steps):
+        one_round(warmup + i)
+    e1.record()
+    torch.cuda.synchronize()
+    host_s = time.perf_counter() - t_host
+    ms_per_step = e0.elapsed_time(e1) / steps
+    log("workload %d: timed %d rounds: %.4f ms/round (host clock %.4f ms/round)" %
+        (wid, steps, ms_per_step, 1e3 * host_s / steps))
+
+    # the same rounds again with HIP events recorded around every stage (on the
+    # library's stream): per-stage durations, and the logits pass for the roofline
+    ctx.profile_begin(steps)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(steps):
+        one_round(warmup + i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_events = e0.elapsed_time(e1) / steps
+    stage_ms, stage_n = ctx.profile_end()
+    stage_avg = [m / n if n else 0.0 for m, n in zip(stage_ms, stage_n)]
+    log("workload %d: with stage events: %.4f ms/round; stages ms %s" %
+        (wid, ms_events, ["%.4f" % x for x in stage_avg]))
+
+    # Every recorded event adds the same stream time (a marker packet), and a
+    # stage's interval holds exactly one of them: take that per-event cost from
+    # the two timed passes (with and without events; 4 events per
+    # graft_build_tree, 2 per graft_accept) and subtract it from every stage.
+    events_per_round = 6
+    event_ms = max(0.0, (ms_events - ms_per_step) / events_per_round)
+    stage_net = [max(0.0, x - event_ms) for x in stage_avg]
+    log("workload %d: per-event stream cost %.4f ms; stages net of it %s" %
+        (wid, event_ms, ["%.4f" % x for x in stage_net]))
+    k1_s = stage_net[0] * 1e-3
+    achieved = logit_bytes / k1_s / 1e9 if k1_s > 0 else 0.0
+
+    # a plain read of the same rotating buffers, back to back: the streaming
+    # read rate the logits pass is compared with
+    sink = torch.empty(G.READ_STREAM_SINK_WORDS, dtype=torch.int32, device=dev)
+    for i in range(3):
+        G.read_stream(bufs[i % R], sink)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(steps):
+        G.read_stream(bufs[i % R], sink)
+    e1.record()
+    torch.cuda.synchronize()
+    read_us = 1e3 * e0.elapsed_time(e1) / steps
+    read_gbs = logit_bytes / (read_us * 1e-6) / 1e9
+    log("workload %d: plain read of one logits buffer: %.2f us = %.0f GB/s" % (wid, read_us, read_gbs))
+    return dict(w=w, inp=inp, sc=sc, sp=sp, ctx=ctx, tb=tb, bufs=bufs, R=R,
+                logit_bytes=logit_bytes, ms_per_step=ms_per_step, ms_events=ms_events,
+                stage_avg=stage_avg, stage_net=stage_net, event_ms=event_ms, achieved=achieved,
+                read_us=read_us, read_gbs=read_gbs, acc_len=acc_len, acc_nodes=acc_nodes,
+                node_mode=node_mode)
+
+
+def workload_text(w, R, node_mode):
+    return ("B=%d sequences, L=%d, V=%d bf16 logits, K=%d, %s, N_max=%d, scorer d=%d rank %d, "
+            "%s targets, %d rotating logit buffers" % (
+                w.batch, w.L, w.V, w.K,
+                "SABA budgets %d..%d" % (min(w.grid), max(w.grid))
+                if w.budget_mode == "saba" else "fixed budget %d" % w.fixed_budget,
+                w.n_max, w.emb_dim, w.rank,
+                "per-node (device history ring chained round to round)" if node_mode
+                else "per-depth", R))
+
+
+def stored_kernel_us(workload: int):
+    """Average duration of the logits pass at this workload from the committed
+    rocprofv3 kernel-trace summary of the default bench.py command (which
+    times the batch-64 headline and then the batch-128 chained rounds), valid
+    only for the kernel source it was measured on."""
+    p = os.path.join(ROOT, "profiles", "kernels_w3_kernel_trace.txt")
+    if not os.path.exists(p):
+        return None
+    kv = {}
+    for line in open(p):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("k_logits_sha256_16") != source_digest():
+        return None
+    try:
+        return float(kv["logits_pass_avg_us_w%d" % workload])
+    except (KeyError, ValueError):
+        return None
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -229,7 +425,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--rotate", type=int, default=0, help="logit buffers (0: >= 1 GiB total)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="single-thread oracle leg: seconds of sequences to time")
+    ap.add_argument("--cpu-seconds-all", type=float, default=3.0,
+                    help="all-cores oracle leg (threads over sequences): seconds to time")
+    ap.add_argument("--config4-steps", type=int, default=50,
+                    help="after the batch-64 headline, time this many chained rounds of the "
+                         "batch-128 workload (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hidden-dim", type=int, default=0,
                     help="also pass drafter hidden states of this width (SABA uses their "
@@ -262,117 +464,17 @@ def main():
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    w = S.workload(args.workload)
-    t0 = time.time()
-    inp = S.gen_round(w, 0)
-    sc = S.gen_scorer(w, "literal")
-    sp = S.saba_params(w) if w.budget_mode == "saba" else None
-    log("inputs generated in %.1fs" % (time.time() - t0))
-
-    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    ctx = G.Context(w.batch, w.L, w.V, w.K, w.n_max, S.HIST_WINDOW)
-    ctx.set_scorer(T(sc["emb"]), T(sc["g_parent"]), T(sc["g_child"]),
-                   None if sc["depth_emb"] is None else T(sc["depth_emb"]),
-                   sc["scale"], sc["beta"], sc["center"])
-    if sp is not None:
-        ctx.set_saba(list(sp["grid"]), list(sp["phi"]), sp["tau_min"], sp["c0"], sp["c1"], sp["c2"])
-
-    logit_bytes = w.batch * w.L * w.V * 2
-    R = args.rotate or max(2, math.ceil((1 << 30) / logit_bytes))
-    base_logits = T(inp["logits"].view(np.int16))
-    bufs = [base_logits] + [base_logits.clone() for _ in range(R - 1)]
-    root, base_pos = T(inp["root_token"]), T(inp["base_pos"])
-    prefix = T(inp["prefix_len"])
-    fixed = T(inp["fixed_budget"]) if "fixed_budget" in inp else None
-    node_mode = w.targets == "node"
-    hist = None if node_mode else T(inp["hist"])
-    if node_mode:
-        ctx.set_history(T(inp["hist_ring"]))
-    tdepth = T(inp["target_depth"]) if not node_mode else None
-    hidden = None
-    if args.hidden_dim:
-        hidden = T(S.gen_hidden(w, 0, args.hidden_dim).view(np.int16))
-    tb = G.TreeBuffers(ctx, w.batch)
-    acc_len = torch.empty(w.batch, dtype=torch.int32, device=dev)
-    acc_nodes = torch.empty(w.batch, w.L, dtype=torch.int32, device=dev)
-    bonus = torch.empty(w.batch, dtype=torch.int32, device=dev)
-    troot = torch.empty(w.batch, dtype=torch.int32, device=dev)
-    tnode = torch.empty(w.batch, w.n_max, dtype=torch.int32, device=dev)
-    torch.cuda.synchronize()
-
-    def one_round(i):
-        ctx.build_tree(bufs[i % R], root, base_pos, prefix_len=prefix, hist=hist,
-                       fixed_budget=fixed, hidden=hidden, out=tb)
-        if node_mode:
-            ctx.synth_node_targets(w.seed + i, root, tb.n_nodes, tb.tokens, tb.parents,
-                                   tb.topk_ids, troot, tnode)
-            ctx.accept(tb.n_nodes, tb.tokens, tb.parents, target_root=troot, target_node=tnode,
-                       update_history=True, acc_len=acc_len, acc_nodes=acc_nodes, bonus=bonus)
-        else:
-            ctx.accept(tb.n_nodes, tb.tokens, tb.parents, target_depth=tdepth, acc_len=acc_len,
-                       acc_nodes=acc_nodes, bonus=bonus)
-
-    for i in range(args.warmup):
-        one_round(i)
-    torch.cuda.synchronize()
-    log("warmup done (%d rounds)" % args.warmup)
-
-    # timed region: K rounds back to back, bracketed by synchronizations
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_host = time.perf_counter()
-    e0.record()
-    for i in range(args.steps):
-        one_round(args.warmup + i)
-    e1.record()
-    torch.cuda.synchronize()
-    host_s = time.perf_counter() - t_host
-    ms_per_step = e0.elapsed_time(e1) / args.steps
-    log("timed %d rounds: %.4f ms/round (host clock %.4f ms/round)" %
-        (args.steps, ms_per_step, 1e3 * host_s / args.steps))
-
-    # the same rounds again with HIP events recorded around every stage (on the
-    # library's stream): per-stage durations, and the logits pass for the roofline
-    ctx.profile_begin(args.steps)
-    torch.cuda.synchronize()
-    e0.record()
-    for i in range(args.steps):
-        one_round(args.warmup + i)
-    e1.record()
-    torch.cuda.synchronize()
-    ms_events = e0.elapsed_time(e1) / args.steps
-    stage_ms, stage_n = ctx.profile_end()
-    stage_avg = [m / n if n else 0.0 for m, n in zip(stage_ms, stage_n)]
-    log("with stage events: %.4f ms/round; stages ms %s" %
-        (ms_events, ["%.4f" % x for x in stage_avg]))
-
-    # Every recorded event adds the same stream time (a marker packet), and a
-    # stage's interval holds exactly one of them: take that per-event cost from
-    # the two timed passes (with and without events; 4 events per
-    # graft_build_tree, 2 per graft_accept) and subtract it from every stage.
-    events_per_round = 6
-    event_ms = max(0.0, (ms_events - ms_per_step) / events_per_round)
-    stage_net = [max(0.0, x - event_ms) for x in stage_avg]
-    log("per-event stream cost %.4f ms; stages net of it %s" %
-        (event_ms, ["%.4f" % x for x in stage_net]))
-    k1_s = stage_net[0] * 1e-3
-    achieved = logit_bytes / k1_s / 1e9 if k1_s > 0 else 0.0
+    run = run_workload(args.workload, args.steps, args.warmup, args.rotate, args.hidden_dim,
+                       torch, dev)
+    w, ctx, tb = run["w"], run["ctx"], run["tb"]
+    bufs, R = run["bufs"], run["R"]
+    logit_bytes = run["logit_bytes"]
+    ms_per_step, ms_events = run["ms_per_step"], run["ms_events"]
+    stage_avg, stage_net, event_ms = run["stage_avg"], run["stage_net"], run["event_ms"]
+    achieved, read_gbs = run["achieved"], run["read_gbs"]
+    acc_len, acc_nodes = run["acc_len"], run["acc_nodes"]
     traffic = stored_traffic(args.workload)
-
-    # a plain read of the same rotating buffers, back to back: the streaming
-    # read rate the logits pass is compared with
-    sink = torch.empty(G.READ_STREAM_SINK_WORDS, dtype=torch.int32, device=dev)
-    for i in range(3):
-        G.read_stream(bufs[i % R], sink)
-    torch.cuda.synchronize()
-    e0.record()
-    for i in range(args.steps):
-        G.read_stream(bufs[i % R], sink)
-    e1.record()
-    torch.cuda.synchronize()
-    read_us = 1e3 * e0.elapsed_time(e1) / args.steps
-    read_gbs = logit_bytes / (read_us * 1e-6) / 1e9
-    log("plain read of one logits buffer: %.2f us = %.0f GB/s" % (read_us, read_gbs))
+    prof_us = stored_kernel_us(args.workload)
 
     if args.copy_calibration:
         n = 256 << 20
@@ -402,9 +504,48 @@ def main():
     budgets = tb.budget.float().mean().item()
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, inp, sc, sp, args.cpu_seconds)
-        log("cpu baseline: %.4f rounds/s over %.1fs" % (cpu["value"], cpu["seconds"]))
+        inp, sc, sp = run["inp"], run["sc"], run["sp"]
+        one = cpu_baseline(w, inp, sc, sp, args.cpu_seconds)
+        log("cpu baseline, 1 thread: %.4f rounds/s over %.1fs" % (one["value"], one["seconds"]))
+        nt = host_threads()
+        cpu = cpu_baseline(w, inp, sc, sp, args.cpu_seconds_all, threads=nt)
+        log("cpu baseline, %d threads: %.4f rounds/s over %.1fs" % (nt, cpu["value"], cpu["seconds"]))
         cpu.pop("seconds")
+        one.pop("seconds")
+        cpu["single_thread"] = one
+
+    # the batch-128 workload (L=32, V=151936, K=32), 50 rounds chained through
+    # the device history ring on one stream: its own round time and logits-pass
+    # roofline (no CPU leg)
+    config4 = None
+    if args.workload == 3 and args.config4_steps > 0:
+        del bufs, run
+        ctx.close()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        r4 = run_workload(4, args.config4_steps, 5, 0, 0, torch, dev)
+        k1 = r4["stage_net"][0]
+        config4 = {
+            "workload": workload_text(r4["w"], r4["R"], r4["node_mode"]),
+            "rounds": args.config4_steps,
+            "us_per_round": 1e3 * r4["ms_per_step"],
+            "rounds_per_s": 1e3 / r4["ms_per_step"],
+            "mean_nodes": r4["tb"].n_nodes.float().mean().item(),
+            "stage_us": {"logits_pass": 1e3 * k1, "edge_scores_and_saba": 1e3 * r4["stage_net"][1],
+                         "select_emit_mask": 1e3 * r4["stage_net"][2],
+                         "accept": 1e3 * r4["stage_net"][3]},
+            "logits_pass": {"achieved": r4["achieved"], "unit": "GB/s",
+                            "frac": r4["achieved"] / HBM_PEAK_GBS,
+                            "algorithmic_bytes_per_launch": r4["logit_bytes"],
+                            "plain_read_gbs": r4["read_gbs"],
+                            "profile_kernel_us": stored_kernel_us(4)},
+        }
+        if config4["logits_pass"]["profile_kernel_us"]:
+            config4["logits_pass"]["profile_frac"] = (
+                r4["logit_bytes"] / (config4["logits_pass"]["profile_kernel_us"] * 1e-6) / 1e9
+                / HBM_PEAK_GBS)
+        r4["ctx"].close()
+        ctx = None
 
     result = {
         "metric": METRIC,
@@ -422,12 +563,7 @@ def main():
         "dtype": "fp32",
         "data": "synthetic",
         "config": {
-            "workload": "B=%d sequences, L=%d, V=%d bf16 logits, K=%d, %s, N_max=%d, scorer "
-                        "d=%d rank %d, %s targets, %d rotating logit buffers" % (
-                            w.batch, w.L, w.V, w.K,
-                            "SABA budgets %d..%d" % (min(w.grid), max(w.grid))
-                            if w.budget_mode == "saba" else "fixed budget %d" % w.fixed_budget,
-                            w.n_max, w.emb_dim, w.rank, "per-node" if node_mode else "per-depth", R),
+            "workload": workload_text(w, R, w.targets == "node"),
             "global_batch": w.batch,
             "hidden_dim": args.hidden_dim,
             "mean_budget": budgets,
@@ -448,9 +584,15 @@ def main():
             "algorithmic_bytes_per_launch": logit_bytes,
             "plain_read_gbs": read_gbs,
             "frac_of_plain_read": achieved / read_gbs if read_gbs > 0 else None,
+            "kernel_us": 1e3 * stage_net[0],
+            "profile_kernel_us": prof_us,
+            "profile_frac": (logit_bytes / (prof_us * 1e-6) / 1e9 / HBM_PEAK_GBS
+                             if prof_us else None),
         },
         "cpu_baseline": cpu,
     }
+    if config4 is not None:
+        result["config4"] = config4
     if verifier is not None:
         result["verifier"] = verifier
     if training is not None:
@@ -458,7 +600,8 @@ def main():
     if saba_fit is not None:
         result["saba_fit"] = saba_fit
     print(json.dumps(result), flush=True)
-    ctx.close()
+    if ctx is not None:
+        ctx.close()
 
 
 if __name__ == "__main__":
