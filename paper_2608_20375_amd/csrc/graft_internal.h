@@ -226,7 +226,7 @@ struct RoundScratch {
   int32_t *topk_ids;       // [batch, L, K]
   float *topk_logq;        // [batch, L, K]
   float *row_stats;        // [batch, L, 3]: lse, maxprob, entropy
-  float *edge_rows;        // [batch, L, K, K] edge scores: [depth][parent slot][child slot]
+  float *edge_rows;        // [batch, L, K, K] edge scores: [depth][parent id rank][child id rank]
   uint8_t *id_rank;        // [batch, L, K] rank of each candidate's token id in its depth
   uint8_t *positive;       // [batch, L] 1 if some edge score of that depth is > 0
   float *adj_cos;          // [batch, max(L - 1, 1)] adjacent hidden-state cosines

@@ -8,9 +8,11 @@
 //   candidates of the previous depth) into LDS, forms every parent-child dot
 //   product (eq. tdes-bitower), centers over the children of each parent when
 //   asked (eq. tdes-center) and adds log q of the child (eq. tdes-score).
-//   Row (depth, parent) of the output holds the scores of the K children in
-//   candidate-slot order; selection filters a row against its threshold and
-//   needs no ranking.
+//   Selection's copy of the scores is indexed by token-id rank: row (depth,
+//   rank of the parent's id) holds the K children in the order of their ids,
+//   so selection appends a parent's children in canonical order by filtering
+//   the row against its threshold, with no ranking; the exported table keeps
+//   the candidates' logit-rank order.
 // The K x m x K contraction is at most 64 x 64 x 64 per (sequence, depth):
 // VALU work, each lane keeping one child's projection in registers and
 // reading the parents' rows from LDS as broadcasts; there is no dense tile to
@@ -192,7 +194,8 @@ __device__ __forceinline__ float seg_sum(float v) {
 // One wave per (sequence b, depth l).  Dynamic LDS: parents [K][mp],
 // children [K][mp] (rows of m floats padded to a multiple of 4 plus 4: 16-byte
 // aligned rows that start on different banks), depth embedding [m], log q [K],
-// token ids [K], their ranks by id [K], clamped child and parent ids [K].
+// token ids [K], their ranks by id [K], clamped child and parent ids [K],
+// parent tokens [K] and their ranks by id [K].
 // The (parent, child) pairs are processed SEG lanes per parent (SEG = K
 // rounded up to a power of two), kRows = 64 / SEG parents at a time: lane c of
 // a run keeps child c's row in registers, reads the parent's row from LDS (one
@@ -218,6 +221,8 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   int32_t *s_idr = s_tok + K;
   int32_t *s_cid = s_idr + K;
   int32_t *s_pid = s_cid + K;
+  int32_t *s_ptok = s_pid + K;     // parent tokens (depth >= 2)
+  int32_t *s_pidr = s_ptok + K;    // rank of each parent's token id in its depth
 
   const int b = blockIdx.x / L;
   const int l = blockIdx.x % L;
@@ -241,6 +246,7 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
     s_lq[lane] = topk_logq[row * K + lane];
     s_cid[lane] = (ct < 0 || ct >= V) ? 0 : ct;
     s_pid[lane] = (pt < 0 || pt >= V) ? 0 : pt;
+    s_ptok[lane] = pt;
   }
   for (int j = lane; j < m; j += kEdgeThreads) s_u[j] = sp.has_depth_emb ? depth_emb[l * m + j] : 0.f;
   __syncthreads();
@@ -252,6 +258,13 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
     for (int c2 = 0; c2 < K; ++c2) r += s_tok[c2] < tc;
     s_idr[lane] = r;
     id_rank[row * K + lane] = static_cast<uint8_t>(r);
+    int rp = 0;
+    if (l > 0) {
+      const int32_t tp = s_ptok[lane];
+#pragma unroll 8
+      for (int c2 = 0; c2 < K; ++c2) rp += s_ptok[c2] < tp;
+    }
+    s_pidr[lane] = rp;
   }
   // projections of children and parents plus the depth embedding, 16 bytes a
   // load when m % 4 == 0; every load of a batch is issued before any store
@@ -339,7 +352,9 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
     if (sp.center) mean = seg_sum<SEG>(valid ? f : 0.f) / static_cast<float>(K);
     const float S = (lq + sp.beta * (f - mean)) + 0.0f;   // -0 -> +0
     if (valid) {
-      edge_rows[base + p * K + c] = S;
+      // selection's copy is indexed by token-id rank (parent row, child
+      // column); the exported table keeps the candidates' rank order
+      edge_rows[base + s_pidr[p] * K + s_idr[c]] = S;
       if (edge_out) edge_out[base + p * K + c] = S;
     }
     pos |= valid && S > 0.f;
@@ -383,7 +398,7 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graf
   const int K = d.top_k, m = ctx->scorer.score_dim;
   const size_t mp = ((m + 3) & ~3) + 4;
   const size_t lds = sizeof(float) * (2 * static_cast<size_t>(K) * mp + K + m) +
-                     sizeof(int32_t) * 4 * K;
+                     sizeof(int32_t) * 6 * K;
   const FastDiv mdiv4 = make_fastdiv(static_cast<uint32_t>(m >= 4 ? m / 4 : 1));
   const dim3 grid(batch * d.num_pos), block(kEdgeThreads);
 #define GRAFT_EDGE(SEG)                                                                        \

@@ -56,18 +56,17 @@ struct SelectArgs {
   uint32_t *error_flag;
 };
 
-// Pool entry info: parent + 1 (13 bits) | depth - 1 (6) | slot of the token
-// among its depth's candidates (6) | rank of the token id in that depth (6) |
-// dead (1)
+// Pool entry info: parent + 1 (13 bits) | depth - 1 (6) | rank of the token id
+// among its depth's candidates (6) | dead (1).  The edge rows are indexed by
+// these ranks (row = parent's rank, column = child's rank).
 constexpr uint32_t kDead = 1u << 31;
-__device__ __forceinline__ uint32_t pinfo(int parent, int depth, int slot, int idr) {
+__device__ __forceinline__ uint32_t pinfo(int parent, int depth, int rank) {
   return static_cast<uint32_t>(parent + 1) | (static_cast<uint32_t>(depth - 1) << 13) |
-         (static_cast<uint32_t>(slot) << 19) | (static_cast<uint32_t>(idr) << 25);
+         (static_cast<uint32_t>(rank) << 19);
 }
 __device__ __forceinline__ int pi_parent(uint32_t v) { return static_cast<int>(v & 0x1FFF) - 1; }
 __device__ __forceinline__ int pi_depth(uint32_t v) { return static_cast<int>((v >> 13) & 63) + 1; }
-__device__ __forceinline__ int pi_slot(uint32_t v) { return static_cast<int>((v >> 19) & 63); }
-__device__ __forceinline__ int pi_idr(uint32_t v) { return static_cast<int>((v >> 25) & 63); }
+__device__ __forceinline__ int pi_rank(uint32_t v) { return static_cast<int>((v >> 19) & 63); }
 __device__ __forceinline__ bool alive(uint32_t v) { return (v & kDead) == 0; }
 
 struct SelMem {
@@ -86,8 +85,7 @@ struct SelMem {
       uint32_t info[kMaxNodes + 1];
     } heap;
   } u;
-  int32_t cand[kMaxL * kMaxK];
-  uint8_t idr[kMaxL * kMaxK];
+  int32_t cand[kMaxL * kMaxK];   // candidate tokens of each depth, by token-id rank
   // edge rows of the sequence, staged when they fit
   alignas(16) float rows[kStageRows];
   // reductions and scalars
@@ -100,10 +98,11 @@ struct SelMem {
   int32_t sc[16];
 };
 
-enum { kNPool = 0, kBudget, kMono, kBstar, kA, kBcnt, kG, kXfit, kMaxDepth, kNSel, kDepthN };
+enum { kNPool = 0, kBudget, kMono, kBstar, kA, kBcnt, kG, kXfit, kMaxDepth, kNSel, kDepthN,
+       kMixed };
 
 __device__ __forceinline__ int32_t ptoken(const SelMem &s, int K, uint32_t info) {
-  return s.cand[(pi_depth(info) - 1) * K + pi_slot(info)];
+  return s.cand[(pi_depth(info) - 1) * K + pi_rank(info)];
 }
 
 // Is pool entry a ranked before pool entry b?  (score desc, depth asc, token path asc)
@@ -264,7 +263,7 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
       const uint32_t info = s.p_info[i];
       const int p = pi_parent(info);
       keep_s[k] = s.p_score[i];
-      keep_i[k] = pinfo(p < 0 ? -1 : s.aux[p], pi_depth(info), pi_slot(info), pi_idr(info));
+      keep_i[k] = pinfo(p < 0 ? -1 : s.aux[p], pi_depth(info), pi_rank(info));
       // the run keeps its kept members: aux[j] = new index of the first kept entry >= j
       const int32_t rv = s.run[i];
       const int r0 = rv >> 8, r1 = r0 + (rv & 255);
@@ -345,12 +344,12 @@ __device__ __forceinline__ void bin_children(SelMem &s, const float *row, int kv
 }
 
 // Appends the children of a row that reach theta at dst, dst + 1, ... in
-// child-slot order (scores ps + row[r], info with parent x at depth d + 1,
+// token-id order (scores ps + row[r], info with parent x at depth d + 1,
 // sibling run runv) and returns the smallest appended score.
 template <int KV>
 __device__ __forceinline__ double append_row(SelMem &s, const float4 (&v)[KV], int kv,
                                              double theta, int dst, int x, int d, double ps,
-                                             const uint8_t *idr, int32_t runv) {
+                                             int32_t runv) {
   double vmin = INFINITY;
 #pragma unroll
   for (int q = 0; q < KV; ++q) {
@@ -362,7 +361,7 @@ __device__ __forceinline__ double append_row(SelMem &s, const float4 (&v)[KV], i
       if (take) {
         const int slot = q * 4 + k;
         s.p_score[dst] = sc;
-        s.p_info[dst] = pinfo(x, d + 1, slot, idr[slot]);
+        s.p_info[dst] = pinfo(x, d + 1, slot);
         s.run[dst] = runv;
         vmin = sc < vmin ? sc : vmin;
       }
@@ -374,10 +373,10 @@ __device__ __forceinline__ double append_row(SelMem &s, const float4 (&v)[KV], i
 template <int KV>
 __device__ __forceinline__ double append_children(SelMem &s, const float *row, int kv,
                                                   double theta, int dst, int x, int d, double ps,
-                                                  const uint8_t *idr, int32_t runv) {
+                                                  int32_t runv) {
   float4 v[KV];
   load_row<KV>(row, kv, v);
-  return append_row<KV>(s, v, kv, theta, dst, x, d, ps, idr, runv);
+  return append_row<KV>(s, v, kv, theta, dst, x, d, ps, runv);
 }
 
 // Children of pool entry x (alive, depth < L) that reach theta, and the
@@ -391,7 +390,7 @@ __device__ __forceinline__ Counted entry_count(const SelMem &s, const float *rs,
   const uint32_t info = s.p_info[x];
   const double ps = s.p_score[x];
   if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
-  const float *row = rs + (pi_depth(info) * K + pi_slot(info)) * K;
+  const float *row = rs + (pi_depth(info) * K + pi_rank(info)) * K;
   float rmin = 0.f;
   int c = 0;
   if (KVP == 1) c = count_reach<1>(row, kv, ps, theta, rmin);
@@ -433,7 +432,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
     if (c == 0) continue;
     const int x = x_lo + i;
     const uint32_t info = s.p_info[x];
-    const float *row = rs + (pi_depth(info) * K + pi_slot(info)) * K;
+    const float *row = rs + (pi_depth(info) * K + pi_rank(info)) * K;
     const double ps = s.p_score[x];
     if (KVP == 1) bin_children<1>(s, row, kv, theta, ps, hi, scale);
     else if (KVP == 2) bin_children<2>(s, row, kv, theta, ps, hi, scale);
@@ -463,20 +462,19 @@ __device__ __forceinline__ double entry_append(SelMem &s, const float *rs, int x
   const int32_t runv = (dst << 8) | c;
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
-  const int row = (d * K + pi_slot(info)) * K;
+  const int row = (d * K + pi_rank(info)) * K;
   const double ps = s.p_score[x];
-  const uint8_t *idr = s.idr + d * K;
-  if (KVP == 1) return append_children<1>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
-  if (KVP == 2) return append_children<2>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
-  if (KVP == 4) return append_children<4>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
-  if (KVP == 8) return append_children<8>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
-  if (KVP == 16) return append_children<16>(s, rs + row, kv, theta, dst, x, d, ps, idr, runv);
+  if (KVP == 1) return append_children<1>(s, rs + row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 2) return append_children<2>(s, rs + row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 4) return append_children<4>(s, rs + row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 8) return append_children<8>(s, rs + row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 16) return append_children<16>(s, rs + row, kv, theta, dst, x, d, ps, runv);
   double vmin = INFINITY;
   for (int r = 0; r < K; ++r) {
     const double sc = ps + static_cast<double>(rs[row + r]);
     if (sc >= theta) {
       s.p_score[dst] = sc;
-      s.p_info[dst] = pinfo(x, d + 1, r, idr[r]);
+      s.p_info[dst] = pinfo(x, d + 1, r);
       s.run[dst] = runv;
       ++dst;
       vmin = sc < vmin ? sc : vmin;
@@ -494,7 +492,7 @@ __device__ __forceinline__ Counted entry_count_cached(const SelMem &s, const flo
   const uint32_t info = s.p_info[x];
   const double ps = s.p_score[x];
   if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
-  load_row<KV>(rs + (pi_depth(info) * K + pi_slot(info)) * K, kv, v);
+  load_row<KV>(rs + (pi_depth(info) * K + pi_rank(info)) * K, kv, v);
   float rmin = 0.f;
   const int c = count_row<KV>(v, kv, ps, theta, rmin);
   return {c, ps + static_cast<double>(rmin)};
@@ -505,7 +503,7 @@ __device__ __forceinline__ double entry_append_cached(SelMem &s, int x, int K, i
                                                       const float4 (&v)[KV]) {
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
-  return append_row<KV>(s, v, kv, theta, dst, x, d, s.p_score[x], s.idr + d * K, (dst << 8) | c);
+  return append_row<KV>(s, v, kv, theta, dst, x, d, s.p_score[x], (dst << 8) | c);
 }
 
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
@@ -528,7 +526,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   float4 cache[kCache > 0 ? kCache : 1][KVC];
   for (int r = tid; r < K; r += kSelThreads) {
     s.p_score[r] = static_cast<double>(rs[r]);
-    s.p_info[r] = pinfo(-1, 1, r, s.idr[r]);
+    s.p_info[r] = pinfo(-1, 1, r);
     s.run[r] = K;   // the depth-1 run starts at 0
   }
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
@@ -620,8 +618,12 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
     }
     int lim = m, dst = n + base + inc - sum;
     if (!fit) {
-      // expand the longest run of [x_lo, n) whose children fit
-      if (tid == 0) s.aux[m] = 0;
+      // expand the longest run of [x_lo, n) whose children fit; the pool no
+      // longer holds one depth per expansion (see canon_levels)
+      if (tid == 0) {
+        s.aux[m] = 0;
+        s.sc[kMixed] = 1;
+      }
       __syncthreads();
       block_scan(s, s.aux, m + 1);                      // aux[i] = offset, aux[m] = total
       const int room = kPoolCap - n;
@@ -698,6 +700,33 @@ __device__ __forceinline__ int select_parallel_k(SelMem &s, const SelectArgs &a,
   return select_parallel<kLds, 16>(s, a, gs, n_target);
 }
 
+// Canonical numbering for the parallel selector's pool when every expansion
+// appended one whole depth: the depth-1 entries are in token-id order, and an
+// expansion walks the previous depth in pool order appending each entry's
+// children in token-id order, so by induction the pool holds the depths in
+// ascending order, each in canonical (token path) order, dead entries
+// interleaved.  The canonical index of an alive entry is then the number of
+// alive entries before it: one block-wide count.  Leaves map[i] = canonical
+// index.
+__device__ void canon_levels(SelMem &s, int n) {
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int per = (n + kSelThreads - 1) / kSelThreads;
+  const int lo = tid * per, hi = lo + per < n ? lo + per : n;
+  int cnt = 0;
+  for (int i = lo; i < hi; ++i) cnt += alive(s.p_info[i]) ? 1 : 0;
+  const int inc = wave_incl_scan(cnt);
+  if (lane == kWave - 1) s.wsum[wave] = inc;
+  __syncthreads();
+  int run = inc - cnt;
+  for (int w = 0; w < wave; ++w) run += s.wsum[w];
+  for (int i = lo; i < hi; ++i) {
+    const bool a = alive(s.p_info[i]);
+    s.map[i] = run;
+    run += a ? 1 : 0;
+  }
+  __syncthreads();
+}
+
 // Canonical numbering for the parallel selector's pool, where the children of
 // a node occupy one contiguous run (dead entries included).  The canonical
 // order is depth ascending, then token path ascending; among nodes of one
@@ -723,7 +752,7 @@ __device__ void canon_preorder(SelMem &s, int L, int K, int n, int n_sel) {
   for (int i = tid; i < n; i += kSelThreads) {
     const uint32_t info = s.p_info[i];
     if (!alive(info)) continue;
-    const int p = pi_parent(info), mine = pi_idr(info);
+    const int p = pi_parent(info), mine = pi_rank(info);
     const int32_t rv = s.run[i];
     const int lo = rv >> 8, hi = lo + (rv & 255);
     int left = 0;
@@ -739,7 +768,7 @@ __device__ void canon_preorder(SelMem &s, int L, int K, int n, int n_sel) {
 #pragma unroll
       for (int k = 0; k < 16; ++k) {
         const int sib = static_cast<int>(alive(o[k])) & static_cast<int>(pi_parent(o[k]) == p) &
-                        static_cast<int>(pi_idr(o[k]) < mine);
+                        static_cast<int>(pi_rank(o[k]) < mine);
         left += sib ? z[k] : 0;
       }
     }
@@ -858,19 +887,19 @@ __device__ void heap_pop_root(SelMem &s, int K, int &n) {
 }
 
 // Rank key of child slot c of a row: larger = earlier in (edge score desc,
-// token id asc).  idr is the depth's rank of each candidate's token id.
-__device__ __forceinline__ uint64_t child_key(const float *row, const uint8_t *idr, int c) {
+// token id asc).  Rows are in token-id order, so column c is the id rank.
+__device__ __forceinline__ uint64_t child_key(const float *row, int c) {
   return (static_cast<uint64_t>(ordered_f32(row[c] + 0.0f)) << 32) |
-         (static_cast<uint64_t>(63 - idr[c]) << 6) | static_cast<uint64_t>(c);
+         static_cast<uint64_t>(63 - c);
 }
 
 // The child of a row that follows key `after` in rank order (~0 for the
 // first), by a scan of the row; -1 when none is left.
-__device__ __forceinline__ int next_child(const float *row, const uint8_t *idr, int K, uint64_t after) {
+__device__ __forceinline__ int next_child(const float *row, int K, uint64_t after) {
   uint64_t best = 0ull;
   int slot = -1;
   for (int c = 0; c < K; ++c) {
-    const uint64_t k = child_key(row, idr, c);
+    const uint64_t k = child_key(row, c);
     if (k < after && k > best) {
       best = k;
       slot = c;
@@ -883,7 +912,7 @@ __device__ void select_serial(SelMem &s, const SelectArgs &a, const float *rs, i
   const int L = a.L, K = a.K;
   int hn = 0, n_sel = 0;
   if (n_target > 0) {
-    const int c0 = next_child(rs, s.idr, K, ~0ull);
+    const int c0 = next_child(rs, K, ~0ull);
     heap_push(s, K, hn, static_cast<double>(rs[c0]), hinfo(-1, c0, 1));
   }
   while (n_sel < n_target && hn > 0) {
@@ -893,18 +922,17 @@ __device__ void select_serial(SelMem &s, const SelectArgs &a, const float *rs, i
     const int p = hi_parent(info), slot = hi_slot(info), d = hi_depth(info);
     const int i = n_sel++;
     s.p_score[i] = score;
-    s.p_info[i] = pinfo(p, d, slot, s.idr[(d - 1) * K + slot]);
+    s.p_info[i] = pinfo(p, d, slot);
     {   // next sibling under the same parent, in rank order
-      const int pslot = p < 0 ? 0 : pi_slot(s.p_info[p]);
+      const int pslot = p < 0 ? 0 : pi_rank(s.p_info[p]);
       const double pscore = p < 0 ? 0.0 : s.p_score[p];
       const float *row = rs + ((d - 1) * K + pslot) * K;
-      const uint8_t *idr = s.idr + (d - 1) * K;
-      const int nx = next_child(row, idr, K, child_key(row, idr, slot));
+      const int nx = next_child(row, K, child_key(row, slot));
       if (nx >= 0) heap_push(s, K, hn, pscore + static_cast<double>(row[nx]), hinfo(p, nx, d));
     }
     if (d < L) {       // best child of the new node
       const float *row = rs + (d * K + slot) * K;
-      const int c0 = next_child(row, s.idr + d * K, K, ~0ull);
+      const int c0 = next_child(row, K, ~0ull);
       heap_push(s, K, hn, score + static_cast<double>(row[c0]), hinfo(i, c0, d + 1));
     }
   }
@@ -935,7 +963,7 @@ __device__ void canon_by_depth(SelMem &s, int K, int n) {
       const uint32_t info = s.p_info[i];
       if (pi_depth(info) != d) continue;
       const int p = pi_parent(info);
-      const int key = (p < 0 ? 0 : s.aux[p]) * K + pi_idr(info);
+      const int key = (p < 0 ? 0 : s.aux[p]) * K + pi_rank(info);
       atomicOr(reinterpret_cast<uint32_t *>(&bits[key >> 5]), 1u << (key & 31));
       atomicAdd(&s.sc[kDepthN], 1);
     }
@@ -948,7 +976,7 @@ __device__ void canon_by_depth(SelMem &s, int K, int n) {
       const uint32_t info = s.p_info[i];
       if (pi_depth(info) != d) continue;
       const int p = pi_parent(info);
-      const int key = (p < 0 ? 0 : s.aux[p]) * K + pi_idr(info);
+      const int key = (p < 0 ? 0 : s.aux[p]) * K + pi_rank(info);
       const uint32_t word = static_cast<uint32_t>(bits[key >> 5]);
       const int rank = pcnt[key >> 5] + __popc(word & ((1u << (key & 31)) - 1u));
       s.aux[i] = rank;          // parents (depth d-1) are not touched here
@@ -976,8 +1004,9 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   }
   // candidates and their rank by token id
   for (int i = tid; i < L * K; i += kSelThreads) {
-    s.cand[i] = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
-    s.idr[i] = a.id_rank[static_cast<int64_t>(b) * L * K + i];
+    const int32_t tok = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
+    const int r = a.id_rank[static_cast<int64_t>(b) * L * K + i];
+    s.cand[(i / K) * K + (r < K ? r : K - 1)] = tok;
   }
   // waves 1.. stage the edge rows (16-byte loads, all issued before the
   // stores) while wave 0 computes the budget
@@ -1008,6 +1037,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
     if (tid == 0) {
       s.sc[kBudget] = budget0;
       s.sc[kMono] = mono ? 1 : 0;
+      s.sc[kMixed] = 0;
     }
   }
   __syncthreads();
@@ -1035,7 +1065,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   if (tid == 0) a.n_nodes[b] = n_sel;
 
   // ---------------- canonical numbering ----------------
-  if (mono) canon_preorder(s, L, K, n, n_sel);
+  if (mono && s.sc[kMixed] == 0) canon_levels(s, n);
+  else if (mono) canon_preorder(s, L, K, n, n_sel);
   else canon_by_depth(s, K, n);
 
   // ---------------- emission ----------------
