@@ -240,7 +240,9 @@ GRAFT_API int graft_build_tree_static(graft_ctx *ctx, const graft_round_in *in /
 
 /* Greedy acceptance walk over the trees of the batch.
  *   n_nodes [batch], tokens/parents [batch, max_nodes] as written by
- *   graft_build_tree; acc_len [batch], acc_nodes [batch, L] (canonical node
+ *   graft_build_tree (every node after its parent, as canonical numbering
+ *   guarantees; a child listed before its parent is not found, and the walk
+ *   stops there); acc_len [batch], acc_nodes [batch, L] (canonical node
  *   indices along the accepted path, -1 padded) and bonus [batch] (the target
  *   token after the last accepted node) are written.  With update_history
  *   nonzero, acc_len is pushed into the context's history ring. */

@@ -4,7 +4,8 @@
 // draft path (the paper's Preliminaries, tree-based speculative decoding; a_t
 // in the speculative-decoding paragraph).  Greedy walk: from the root, move to
 // the child whose token equals the target's token after the current node; stop
-// when no child matches.  One wave per sequence scans the nodes 64 at a time.
+// when no child matches.  A workgroup per sequence stages the tree in LDS with
+// one round of loads; one wave then scans it 64 nodes at a time.
 // The number of accepted nodes feeds hist_t of the SABA state (mean of the last
 // w accepted lengths), kept in a per-sequence device ring.
 //
@@ -16,8 +17,12 @@
 namespace graft {
 namespace {
 
-constexpr int kAccThreads = 64;
+constexpr int kAccThreads = 256;
 
+// One workgroup per sequence.  Every thread issues its loads of the tree
+// (parents, tokens and, in per-node mode, the targets of all max_nodes slots;
+// the padding beyond n_nodes is part of the caller's arrays) before any is
+// used, so the walk costs one memory round trip; wave 0 then walks in LDS.
 __global__ void __launch_bounds__(kAccThreads)
 accept_kernel(int n_max, int L, int window, const int32_t *__restrict__ n_nodes,
               const int32_t *__restrict__ tokens, const int32_t *__restrict__ parents,
@@ -25,20 +30,32 @@ accept_kernel(int n_max, int L, int window, const int32_t *__restrict__ n_nodes,
               const int32_t *__restrict__ target_depth, int32_t *__restrict__ acc_len,
               int32_t *__restrict__ acc_nodes, int32_t *__restrict__ bonus,
               int32_t *__restrict__ ring, int32_t *__restrict__ ring_pos, int update) {
+  __shared__ int32_t s_par[kMaxNodes], s_tok[kMaxNodes], s_tgt[kMaxNodes + 1];
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = lane_id();
   const int64_t ob = static_cast<int64_t>(b) * n_max;
-  int n = n_nodes[b];
-  if (n > n_max) n = n_max;
+  const int n_raw = n_nodes[b];
+  const int t_root = target_node ? target_root[b] : 0;
+  for (int i = tid; i < n_max; i += kAccThreads) {
+    s_par[i] = parents[ob + i];
+    s_tok[i] = tokens[ob + i];
+    if (target_node) s_tgt[i] = target_node[ob + i];
+  }
+  if (!target_node)
+    for (int i = tid; i <= L; i += kAccThreads) s_tgt[i] = target_depth[static_cast<int64_t>(b) * (L + 1) + i];
+  __syncthreads();
+  if (tid >= kWave) return;
+  const int n = n_raw < n_max ? (n_raw < 0 ? 0 : n_raw) : n_max;
   int cur = -1, a = 0;
-  int t = target_node ? target_root[b] : target_depth[static_cast<int64_t>(b) * (L + 1)];
-  // a path has at most L nodes; the bound also ends the walk on malformed trees
+  int t = target_node ? t_root : s_tgt[0];
+  // a path has at most L nodes; the bound also ends the walk on malformed
+  // trees.  The children of cur are contiguous and follow it in canonical
+  // order, so the scan starts after cur.
   while (a < L) {
     int next = -1;
-    // children of cur are contiguous in canonical order; a plain scan suffices
-    for (int base = 0; base < n; base += kWave) {
+    for (int base = cur + 1; base < n; base += kWave) {
       const int j = base + lane;
-      const bool hit = j < n && parents[ob + j] == cur && tokens[ob + j] == t;
+      const bool hit = j < n && s_par[j] == cur && s_tok[j] == t;
       const uint64_t m = __ballot(hit);
       if (m) {
         next = base + __builtin_ctzll(m);
@@ -49,7 +66,7 @@ accept_kernel(int n_max, int L, int window, const int32_t *__restrict__ n_nodes,
     if (lane == 0) acc_nodes[static_cast<int64_t>(b) * L + a] = next;
     ++a;
     cur = next;
-    t = target_node ? target_node[ob + cur] : target_depth[static_cast<int64_t>(b) * (L + 1) + a];
+    t = target_node ? s_tgt[cur] : s_tgt[a];
   }
   for (int i = a + lane; i < L; i += kWave) acc_nodes[static_cast<int64_t>(b) * L + i] = -1;
   if (lane == 0) {
