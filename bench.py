@@ -331,12 +331,13 @@ def run_workload(wid, steps, warmup, rotate, hidden_dim, torch, dev, chain=None)
     e0.record()
     for i in range(steps):
         one_round(warmup + i)
+    enqueue_s = time.perf_counter() - t_host
     e1.record()
     torch.cuda.synchronize()
     host_s = time.perf_counter() - t_host
     ms_per_step = e0.elapsed_time(e1) / steps
-    log("workload %d: timed %d rounds: %.4f ms/round (host clock %.4f ms/round)" %
-        (wid, steps, ms_per_step, 1e3 * host_s / steps))
+    log("workload %d: timed %d rounds: %.4f ms/round (host clock %.4f ms/round; host enqueue "
+        "%.4f ms/round)" % (wid, steps, ms_per_step, 1e3 * host_s / steps, 1e3 * enqueue_s / steps))
 
     # the same rounds again with HIP events recorded around every stage (on the
     # library's stream): per-stage durations, and the logits pass for the roofline

@@ -545,6 +545,41 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   double theta = -INFINITY;
   bool pruned = false;
   int n = K, n_alive = K, x_lo = 0;
+  if (L > 1 && K <= n_target && K + K * K > n_target) {
+    // The first expansion keeps every depth-1 prefix and its K * K children
+    // all reach theta = -inf, more than N together: bound the N-th score by a
+    // histogram of these K + K * K prefixes over [smallest child score, hi]
+    // (the bound the prune step below would take after counting them), one
+    // (parent rank, child rank) pair per thread.  Depth-1 prefix r scores
+    // rs[r] and its row is rs[K * K + r * K ...].
+    const int pairs = K * K;
+    double pmin = INFINITY;
+    for (int j = tid; j < pairs; j += kSelThreads) {
+      const double v = static_cast<double>(rs[j / K]) + static_cast<double>(rs[pairs + j]);
+      pmin = v < pmin ? v : pmin;
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const double ov = xor_lane_f64(pmin, o);
+      pmin = ov < pmin ? ov : pmin;
+    }
+    if (lane == 0 && pmin < INFINITY) atomicMin(&s.lomin, ordered_f64(pmin));
+    __syncthreads();
+    const double lo = unordered_f64(s.lomin);
+    const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
+    if (tid < K) atomicAdd(&s.u.b.hist[hslot(score_bin(s.p_score[tid], hi, scale))], 1);
+    for (int j = tid; j < pairs; j += kSelThreads) {
+      const double v = static_cast<double>(rs[j / K]) + static_cast<double>(rs[pairs + j]);
+      atomicAdd(&s.u.b.hist[hslot(score_bin(v, hi, scale))], 1);
+    }
+    __syncthreads();
+    hist_boundary(s, n_target);
+    if (scale > 0.0) {
+      const double edge = hi - static_cast<double>(s.sc[kBstar] + 1) / scale;
+      theta = edge - 1e-9 * (fabs(edge) + fabs(hi) + 1.0);
+    }
+    pruned = true;
+  }
   for (;;) {
     if (n_alive > n_target) {
       // all alive scores are >= theta (or >= the smallest appended score)
@@ -1130,9 +1165,20 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       const int rows = a.n_max - base < kWave ? a.n_max - base : kWave;
-      for (int t = lane; t < rows * words; t += kWave) {
+      // every LDS read of the copy is issued before its stores
+      constexpr int kCopy = kMaxNodes / 64;        // words <= kCopy
+      const int total = rows * words;
+      uint64_t cv[kCopy];
+#pragma unroll
+      for (int k = 0; k < kCopy; ++k) {
+        const int t = lane + k * kWave;
         const int rr = static_cast<int>((static_cast<uint32_t>(t) * recip) >> 16);
-        mseq[static_cast<int64_t>(base) * words + t] = stage[t + rr];
+        cv[k] = t < total ? stage[t + rr] : 0ull;
+      }
+#pragma unroll
+      for (int k = 0; k < kCopy; ++k) {
+        const int t = lane + k * kWave;
+        if (t < total) mseq[static_cast<int64_t>(base) * words + t] = cv[k];
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
