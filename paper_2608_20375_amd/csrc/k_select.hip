@@ -16,7 +16,7 @@
 //           members are ranked with the full order); let theta be the N-th;
 //           expand every kept prefix not yet expanded, adding only children
 //           whose score reaches theta (a parent's edge row is filtered in
-//           child-slot order; no ranking of the row is needed);
+//           token-id order; no ranking of the row by score is needed);
 //           stop when an expansion adds nothing.
 //   A prefix outside the kept set can only gain better competitors, and a
 //   skipped child is worse than theta, which only rises, so the result is the
@@ -44,7 +44,7 @@ constexpr int kStageRows = 4096;   // L * K * K edges staged in LDS up to this s
 
 struct SelectArgs {
   int L, K, n_max, words;
-  const float *edge_rows;       // [B, L, K, K] edge scores, [depth][parent slot][child slot]
+  const float *edge_rows;       // [B, L, K, K] edge scores, [depth][parent id rank][child id rank]
   const int32_t *topk_ids;      // [B, L, K]
   const uint8_t *id_rank;       // [B, L, K] rank of each candidate's token id in its depth
   const uint8_t *positive;      // [B, L] some edge score of that depth is > 0
