@@ -557,6 +557,29 @@ def test_zero_budget_and_tiny_trees():
     ctx.close()
 
 
+@pytest.mark.parametrize("L,K,V,n_max", [(6, 8, 3000, 128), (20, 16, 5000, 512)])
+def test_first_expansion_bound_budget_edges(L, K, V, n_max):
+    """Budgets on both sides of K and of K + K^2, where the selector switches
+    between bounding the first expansion by one histogram of the depth-1 and
+    depth-2 prefixes and counting the depth-1 children first; the first shape
+    stages its edge rows in LDS, the second (L * K * K > 4096) reads them from
+    device memory.  beta = 0 (edge scores = log q <= 0) keeps every sequence
+    on the parallel selector."""
+    budgets = [K - 1, K, K + 1, K + K * K - 1, K + K * K, K + K * K + 1]
+    w = S.workload(0, batch=len(budgets), L=L, K=K, V=V, n_max=n_max, fixed_budget=n_max)
+    inp = S.gen_round(w)
+    inp["fixed_budget"] = np.array(budgets, np.int32)
+    sc = WL.scorer_inputs(w, "paper")
+    sc["beta"] = 0.0
+    ctx = WL.gpu_context(w, sc, None, torch)
+    g = WL.gpu_round(ctx, w, inp, torch)
+    assert (g["edge_scores"] <= 0).all()
+    assert g["n_nodes"].tolist() == budgets
+    staged_check(w, g, sc, None, inp, range(w.batch))
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
 def test_flat_scores_force_pool_compaction():
     """Uniform logits and a zero scorer make every edge score equal (and a few
     tie levels in the second sequence): the first expansion overflows the
