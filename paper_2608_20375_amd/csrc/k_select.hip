@@ -1165,20 +1165,9 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       const int rows = a.n_max - base < kWave ? a.n_max - base : kWave;
-      // every LDS read of the copy is issued before its stores
-      constexpr int kCopy = kMaxNodes / 64;        // words <= kCopy
-      const int total = rows * words;
-      uint64_t cv[kCopy];
-#pragma unroll
-      for (int k = 0; k < kCopy; ++k) {
-        const int t = lane + k * kWave;
+      for (int t = lane; t < rows * words; t += kWave) {
         const int rr = static_cast<int>((static_cast<uint32_t>(t) * recip) >> 16);
-        cv[k] = t < total ? stage[t + rr] : 0ull;
-      }
-#pragma unroll
-      for (int k = 0; k < kCopy; ++k) {
-        const int t = lane + k * kWave;
-        if (t < total) mseq[static_cast<int64_t>(base) * words + t] = cv[k];
+        mseq[static_cast<int64_t>(base) * words + t] = stage[t + rr];
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
