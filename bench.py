@@ -68,6 +68,27 @@ def stored_traffic(workload: int):
         return None
 
 
+def stored_valu(workload: int):
+    """VALU issue of the logits pass from the committed rocprofv3 SQ counter
+    summary: (fraction of the kernel's span a SIMD issues VALU, that time in
+    us), valid only for the kernel source it was measured on."""
+    p = os.path.join(ROOT, "profiles", "logits_pass_valu_counters.txt")
+    if not os.path.exists(p):
+        return None
+    kv = {}
+    for line in open(p):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("k_logits_sha256_16") != source_digest():
+        return None
+    try:
+        return (float(kv["valu_busy_frac_w%d" % workload]),
+                float(kv["valu_us_per_simd_w%d" % workload]))
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w, inp, sc, sp, seconds: float, threads: int = 1):
     """The oracle (plain C, fp64) on this host: whole sequences of the timed
     round (row statistics, top-K, edge scores, budget, selection, emission,
@@ -476,6 +497,7 @@ def main():
     acc_len, acc_nodes = run["acc_len"], run["acc_nodes"]
     traffic = stored_traffic(args.workload)
     prof_us = stored_kernel_us(args.workload)
+    valu = stored_valu(args.workload)
 
     if args.copy_calibration:
         n = 256 << 20
@@ -539,7 +561,8 @@ def main():
                             "frac": r4["achieved"] / HBM_PEAK_GBS,
                             "algorithmic_bytes_per_launch": r4["logit_bytes"],
                             "plain_read_gbs": r4["read_gbs"],
-                            "profile_kernel_us": stored_kernel_us(4)},
+                            "profile_kernel_us": stored_kernel_us(4),
+                            "valu_busy_frac": (stored_valu(4) or (None,))[0]},
         }
         if config4["logits_pass"]["profile_kernel_us"]:
             config4["logits_pass"]["profile_frac"] = (
@@ -589,6 +612,10 @@ def main():
             "profile_kernel_us": prof_us,
             "profile_frac": (logit_bytes / (prof_us * 1e-6) / 1e9 / HBM_PEAK_GBS
                              if prof_us else None),
+            # the secondary bound: share of the kernel's span a SIMD spends
+            # issuing VALU, from the committed SQ counter summary
+            "valu_busy_frac": valu[0] if valu else None,
+            "valu_us_per_simd": valu[1] if valu else None,
         },
         "cpu_baseline": cpu,
     }
