@@ -40,7 +40,7 @@ constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kPoolCap = 4096;
 constexpr int kPerThread = kPoolCap / kSelThreads;
 constexpr int kBins = 2048;
-constexpr int kStageRows = 4096;   // L * K * K edges staged in LDS up to this size
+constexpr int kStageRows = 4096;   // edge-row floats staged in LDS (all of a sequence's, or its first depths')
 
 struct SelectArgs {
   int L, K, n_max, words;
@@ -284,6 +284,24 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
   return kept;
 }
 
+// Where selection reads the edge rows of a sequence ([depth][parent rank]
+// [child rank], rows of K): all of them staged in LDS, or the rows of the
+// first depths staged (as many whole depths as the stage holds) and the
+// deeper ones read from device memory.
+struct LdsRows {
+  const float *p;
+  __device__ __forceinline__ const float *row(int off) const { return p + off; }
+  __device__ __forceinline__ float at(int i) const { return p[i]; }
+};
+struct SplitRows {
+  const float *lds, *glb;
+  int split;   // staged floats: [0, split) in LDS, a whole number of depths
+  __device__ __forceinline__ const float *row(int off) const {
+    return off < split ? lds + off : glb + off;
+  }
+  __device__ __forceinline__ float at(int i) const { return i < split ? lds[i] : glb[i]; }
+};
+
 // Edge-row helpers for K % 4 == 0 with kv = K / 4 groups of four, KV the
 // next power of two >= kv.  A row holds the K children's edge scores in
 // child-slot order.  Every load is issued unconditionally (clamped to the
@@ -385,12 +403,13 @@ struct Counted {
   int c;
   double vmin;
 };
-__device__ __forceinline__ Counted entry_count(const SelMem &s, const float *rs, int x, int L,
+template <class RS>
+__device__ __forceinline__ Counted entry_count(const SelMem &s, const RS &rs, int x, int L,
                                                int K, int kv, int KVP, double theta) {
   const uint32_t info = s.p_info[x];
   const double ps = s.p_score[x];
   if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
-  const float *row = rs + (pi_depth(info) * K + pi_rank(info)) * K;
+  const float *row = rs.row((pi_depth(info) * K + pi_rank(info)) * K);
   float rmin = 0.f;
   int c = 0;
   if (KVP == 1) c = count_reach<1>(row, kv, ps, theta, rmin);
@@ -413,11 +432,10 @@ __device__ __forceinline__ Counted entry_count(const SelMem &s, const float *rs,
 // [x_lo, n): these are all distinct prefixes, so the score at the start of the
 // bin that holds the N-th of them bounds the final N-th score from below.
 // All the scores lie in [lo, hi]; hist[] is cleared before and after.
-template <bool kLds>
-__device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K, int kv, int KVP, int n, int x_lo,
+template <class RS>
+__device__ __forceinline__ double prune_bound(SelMem &s, const RS &rs, int K, int kv, int KVP, int n, int x_lo,
                               int i0, int per, int n_keep, double theta, double lo, double hi) {
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  const float *rs = kLds ? s.rows : gs;
   const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
   for (int i = tid; i < n; i += kSelThreads) {
     const bool live = alive(s.p_info[i]);
@@ -432,7 +450,7 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
     if (c == 0) continue;
     const int x = x_lo + i;
     const uint32_t info = s.p_info[x];
-    const float *row = rs + (pi_depth(info) * K + pi_rank(info)) * K;
+    const float *row = rs.row((pi_depth(info) * K + pi_rank(info)) * K);
     const double ps = s.p_score[x];
     if (KVP == 1) bin_children<1>(s, row, kv, theta, ps, hi, scale);
     else if (KVP == 2) bin_children<2>(s, row, kv, theta, ps, hi, scale);
@@ -457,21 +475,22 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const float *gs, int K,
 // Appends the c children of pool entry x that reach theta at dst (the caller
 // counted them), records their sibling run and returns the smallest appended
 // score.
-__device__ __forceinline__ double entry_append(SelMem &s, const float *rs, int x, int K, int kv,
+template <class RS>
+__device__ __forceinline__ double entry_append(SelMem &s, const RS &rs, int x, int K, int kv,
                                                int KVP, double theta, int dst, int c) {
   const int32_t runv = (dst << 8) | c;
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
-  const int row = (d * K + pi_rank(info)) * K;
+  const float *row = rs.row((d * K + pi_rank(info)) * K);
   const double ps = s.p_score[x];
-  if (KVP == 1) return append_children<1>(s, rs + row, kv, theta, dst, x, d, ps, runv);
-  if (KVP == 2) return append_children<2>(s, rs + row, kv, theta, dst, x, d, ps, runv);
-  if (KVP == 4) return append_children<4>(s, rs + row, kv, theta, dst, x, d, ps, runv);
-  if (KVP == 8) return append_children<8>(s, rs + row, kv, theta, dst, x, d, ps, runv);
-  if (KVP == 16) return append_children<16>(s, rs + row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 1) return append_children<1>(s, row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 2) return append_children<2>(s, row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 4) return append_children<4>(s, row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 8) return append_children<8>(s, row, kv, theta, dst, x, d, ps, runv);
+  if (KVP == 16) return append_children<16>(s, row, kv, theta, dst, x, d, ps, runv);
   double vmin = INFINITY;
   for (int r = 0; r < K; ++r) {
-    const double sc = ps + static_cast<double>(rs[row + r]);
+    const double sc = ps + static_cast<double>(row[r]);
     if (sc >= theta) {
       s.p_score[dst] = sc;
       s.p_info[dst] = pinfo(x, d + 1, r);
@@ -485,14 +504,14 @@ __device__ __forceinline__ double entry_append(SelMem &s, const float *rs, int x
 
 // Cached variants: the caller keeps the entry's row (v) in registers from
 // the count to the append.
-template <int KV>
-__device__ __forceinline__ Counted entry_count_cached(const SelMem &s, const float *rs, int x,
+template <int KV, class RS>
+__device__ __forceinline__ Counted entry_count_cached(const SelMem &s, const RS &rs, int x,
                                                       int L, int K, int kv, double theta,
                                                       float4 (&v)[KV]) {
   const uint32_t info = s.p_info[x];
   const double ps = s.p_score[x];
   if (!alive(info) || pi_depth(info) >= L) return {0, INFINITY};
-  load_row<KV>(rs + (pi_depth(info) * K + pi_rank(info)) * K, kv, v);
+  load_row<KV>(rs.row((pi_depth(info) * K + pi_rank(info)) * K), kv, v);
   float rmin = 0.f;
   const int c = count_row<KV>(v, kv, ps, theta, rmin);
   return {c, ps + static_cast<double>(rmin)};
@@ -507,14 +526,13 @@ __device__ __forceinline__ double entry_append_cached(SelMem &s, int x, int K, i
 }
 
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
-// alive unexpanded entry lies in [x_lo, n).  kLds: the edge rows are staged in
-// LDS (s.rows), else read from gs.
-template <bool kLds, int KVT>
-__device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, const float *gs,
+// alive unexpanded entry lies in [x_lo, n).  rs: where the edge rows are read
+// (LdsRows, SplitRows).
+template <class RS, int KVT>
+__device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, const RS &rs,
                                int n_target) {
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int L = a.L, K = a.K;
-  const float *rs = kLds ? s.rows : gs;
   // vector path: K % 4 == 0, kv = K / 4 groups, KVT = next power of two (0:
   // the scalar path)
   const int kv = K / 4;
@@ -525,13 +543,14 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   constexpr int KVC = KVT > 0 ? KVT : 1;
   float4 cache[kCache > 0 ? kCache : 1][KVC];
   for (int r = tid; r < K; r += kSelThreads) {
-    s.p_score[r] = static_cast<double>(rs[r]);
+    s.p_score[r] = static_cast<double>(rs.at(r));
     s.p_info[r] = pinfo(-1, 1, r);
     s.run[r] = K;   // the depth-1 run starts at 0
   }
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
   // the depth-1 row's largest and smallest scores, in every wave (K <= 64)
-  float r_hi = lane < K ? rs[lane] : -INFINITY, r_lo = lane < K ? rs[lane] : INFINITY;
+  const float r0 = lane < K ? rs.at(lane) : 0.f;
+  float r_hi = lane < K ? r0 : -INFINITY, r_lo = lane < K ? r0 : INFINITY;
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1) {
     r_hi = fmaxf(r_hi, __uint_as_float(xor_lane(__float_as_uint(r_hi), o)));
@@ -555,7 +574,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
     const int pairs = K * K;
     double pmin = INFINITY;
     for (int j = tid; j < pairs; j += kSelThreads) {
-      const double v = static_cast<double>(rs[j / K]) + static_cast<double>(rs[pairs + j]);
+      const double v = static_cast<double>(rs.at(j / K)) + static_cast<double>(rs.at(pairs + j));
       pmin = v < pmin ? v : pmin;
     }
 #pragma unroll
@@ -569,7 +588,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
     const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
     if (tid < K) atomicAdd(&s.u.b.hist[hslot(score_bin(s.p_score[tid], hi, scale))], 1);
     for (int j = tid; j < pairs; j += kSelThreads) {
-      const double v = static_cast<double>(rs[j / K]) + static_cast<double>(rs[pairs + j]);
+      const double v = static_cast<double>(rs.at(j / K)) + static_cast<double>(rs.at(pairs + j));
       atomicAdd(&s.u.b.hist[hslot(score_bin(v, hi, scale))], 1);
     }
     __syncthreads();
@@ -635,7 +654,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       // the children, then count again against the tighter bound
       const double lo = theta > -INFINITY ? theta : unordered_f64(s.lomin);
       const double bound =
-          prune_bound<kLds>(s, gs, K, kv, KVP, n, x_lo, i0, per, n_target, theta, lo, hi);
+          prune_bound(s, rs, K, kv, KVP, n, x_lo, i0, per, n_target, theta, lo, hi);
       pruned = true;
       if (bound > theta) {
         theta = bound;
@@ -723,16 +742,16 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
 
 // select_parallel for the row width of K: groups of four (kv = K / 4,
 // rounded up to a power of two) or the scalar path when K % 4 != 0.
-template <bool kLds>
-__device__ __forceinline__ int select_parallel_k(SelMem &s, const SelectArgs &a, const float *gs,
+template <class RS>
+__device__ __forceinline__ int select_parallel_k(SelMem &s, const SelectArgs &a, const RS &rs,
                                                  int n_target) {
   const int K = a.K, kv = K / 4;
-  if (K & 3) return select_parallel<kLds, 0>(s, a, gs, n_target);
-  if (kv <= 1) return select_parallel<kLds, 1>(s, a, gs, n_target);
-  if (kv <= 2) return select_parallel<kLds, 2>(s, a, gs, n_target);
-  if (kv <= 4) return select_parallel<kLds, 4>(s, a, gs, n_target);
-  if (kv <= 8) return select_parallel<kLds, 8>(s, a, gs, n_target);
-  return select_parallel<kLds, 16>(s, a, gs, n_target);
+  if (K & 3) return select_parallel<RS, 0>(s, a, rs, n_target);
+  if (kv <= 1) return select_parallel<RS, 1>(s, a, rs, n_target);
+  if (kv <= 2) return select_parallel<RS, 2>(s, a, rs, n_target);
+  if (kv <= 4) return select_parallel<RS, 4>(s, a, rs, n_target);
+  if (kv <= 8) return select_parallel<RS, 8>(s, a, rs, n_target);
+  return select_parallel<RS, 16>(s, a, rs, n_target);
 }
 
 // Canonical numbering for the parallel selector's pool when every expansion
@@ -1044,16 +1063,18 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
     s.cand[(i / K) * K + (r < K ? r : K - 1)] = tok;
   }
   // waves 1.. stage the edge rows (16-byte loads, all issued before the
-  // stores) while wave 0 computes the budget
-  const bool staged = L * K * K <= kStageRows;
+  // stores) while wave 0 computes the budget: all of them when they fit, else
+  // those of the first depths (as many whole depths as the stage holds)
+  const int n_stage = (L * K * K <= kStageRows ? L : kStageRows / (K * K)) * K * K;
+  const bool staged = n_stage == L * K * K;
   constexpr int kStageThreads = kSelThreads - kWave;
-  if (staged && tid >= kWave && (L * K * K) % 4 != 0) {
-    for (int i = tid - kWave; i < L * K * K; i += kStageThreads) s.rows[i] = ss[i];
-  } else if (staged && tid >= kWave) {
+  if (tid >= kWave && ((L * K * K) % 4 != 0 || n_stage % 4 != 0)) {
+    for (int i = tid - kWave; i < n_stage; i += kStageThreads) s.rows[i] = ss[i];
+  } else if (tid >= kWave) {
     // L*K*K is a multiple of 4 here, so the sequence's base is 16-byte aligned
     constexpr int kF4 = (kStageRows / 4 + kStageThreads - 1) / kStageThreads;
     const int t = tid - kWave;
-    const int nf4 = L * K * K / 4;
+    const int nf4 = n_stage / 4;
     const float4 *src_f = reinterpret_cast<const float4 *>(ss);
     float4 vf[kF4];
 #pragma unroll
@@ -1083,8 +1104,9 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   const bool mono = s.sc[kMono] != 0;
   if (mono) {
     if (n_target > 0) {
-      const int n_pool = staged ? select_parallel_k<true>(s, a, ss, n_target)
-                                : select_parallel_k<false>(s, a, ss, n_target);
+      const int n_pool = staged ? select_parallel_k(s, a, LdsRows{s.rows}, n_target)
+                                : select_parallel_k(s, a, SplitRows{s.rows, ss, n_stage},
+                                                    n_target);
       if (tid == 0) s.sc[kNPool] = n_pool;
     } else if (tid == 0) {
       s.sc[kNPool] = 0;
