@@ -224,8 +224,12 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   int32_t *s_ptok = s_pid + K;     // parent tokens (depth >= 2)
   int32_t *s_pidr = s_ptok + K;    // rank of each parent's token id in its depth
 
-  const int b = blockIdx.x / L;
-  const int l = blockIdx.x % L;
+  // depth-major blocks: with a batch that is a multiple of the 8 XCDs, every
+  // depth of sequence b runs on the XCD that the select block of b (block b)
+  // runs on, so selection's reads of the rows find them in that XCD's L2
+  const int batch = static_cast<int>(gridDim.x) / L;
+  const int b = blockIdx.x % batch;
+  const int l = blockIdx.x / batch;
   const int n_par = (l == 0) ? 1 : K;
   const int64_t row = static_cast<int64_t>(b) * L + l;
   const int lane = threadIdx.x;
