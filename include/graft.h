@@ -219,8 +219,9 @@ GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host 
  * allocate memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid hipMalloc).  Same arguments, outputs and errors as
  * graft_build_tree, and the same kernels, but the round's intermediates
- * (split-row partials, candidates, row statistics, edge rows, id ranks,
- * positive flags, hidden-state cosines) live in a static device array of
+ * (split-row partials, candidates, row statistics, edge rows, candidate
+ * tables in token-id order, positive flags, hidden-state cosines) live in a
+ * static device array of
  * GRAFT_STATIC_SCRATCH_BYTES per GPU instead of the context's workspace; the
  * context still provides the scorer's projections, SABA parameters, the
  * history ring and the device status.  The bytes needed grow with the batch:

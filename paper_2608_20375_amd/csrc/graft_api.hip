@@ -36,7 +36,7 @@ int64_t carve_round_scratch(const graft_dims &d, int batch, int64_t part_slots, 
   w.topk_logq = reinterpret_cast<float *>(take(B * L * K * int64_t{sizeof(float)}));
   w.row_stats = reinterpret_cast<float *>(take(B * L * 3 * int64_t{sizeof(float)}));
   w.edge_rows = reinterpret_cast<float *>(take(B * L * K * K * int64_t{sizeof(float)}));
-  w.id_rank = reinterpret_cast<uint8_t *>(take(B * L * K));
+  w.cand_by_rank = reinterpret_cast<int32_t *>(take(B * L * K * int64_t{sizeof(int32_t)}));
   w.positive = reinterpret_cast<uint8_t *>(take(B * L));
   w.adj_cos = reinterpret_cast<float *>(take(B * (L > 1 ? L - 1 : 1) * int64_t{sizeof(float)}));
   if (ws) *ws = w;

@@ -227,7 +227,7 @@ struct RoundScratch {
   float *topk_logq;        // [batch, L, K]
   float *row_stats;        // [batch, L, 3]: lse, maxprob, entropy
   float *edge_rows;        // [batch, L, K, K] edge scores: [depth][parent id rank][child id rank]
-  uint8_t *id_rank;        // [batch, L, K] rank of each candidate's token id in its depth
+  int32_t *cand_by_rank;   // [batch, L, K] each depth's candidate tokens in token-id order
   uint8_t *positive;       // [batch, L] 1 if some edge score of that depth is > 0
   float *adj_cos;          // [batch, max(L - 1, 1)] adjacent hidden-state cosines
 };

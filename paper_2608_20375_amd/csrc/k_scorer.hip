@@ -207,7 +207,7 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
             const float *__restrict__ topk_logq, const int32_t *__restrict__ root_token,
             const float *__restrict__ P, const float *__restrict__ Q,
             const float *__restrict__ depth_emb, ScorerParams sp,
-            float *__restrict__ edge_rows, uint8_t *__restrict__ id_rank,
+            float *__restrict__ edge_rows, int32_t *__restrict__ cand_by_rank,
             uint8_t *__restrict__ positive,
             float *__restrict__ edge_out, uint32_t *__restrict__ error_flag, SabaArgs sa,
             SabaParams sp_saba) {
@@ -261,7 +261,7 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
 #pragma unroll 8
     for (int c2 = 0; c2 < K; ++c2) r += s_tok[c2] < tc;
     s_idr[lane] = r;
-    id_rank[row * K + lane] = static_cast<uint8_t>(r);
+    cand_by_rank[row * K + r] = tc;
     int rp = 0;
     if (l > 0) {
       const int32_t tp = s_ptok[lane];
@@ -409,7 +409,7 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graf
   hipLaunchKernelGGL(edge_kernel<SEG>, grid, block, lds, stream, d.num_pos, K, m,            \
                      static_cast<int64_t>(d.vocab), mdiv4, ws.topk_ids, ws.topk_logq,       \
                      root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
-                     ctx->scorer, ws.edge_rows, ws.id_rank,                                 \
+                     ctx->scorer, ws.edge_rows, ws.cand_by_rank,                            \
                      ws.positive, edge_out, ctx->error_flag, sa, ctx->saba)
   if (K <= 1) GRAFT_EDGE(1);
   else if (K <= 2) GRAFT_EDGE(2);

@@ -45,8 +45,7 @@ constexpr int kStageRows = 4096;   // edge-row floats staged in LDS (all of a se
 struct SelectArgs {
   int L, K, n_max, words;
   const float *edge_rows;       // [B, L, K, K] edge scores, [depth][parent id rank][child id rank]
-  const int32_t *topk_ids;      // [B, L, K]
-  const uint8_t *id_rank;       // [B, L, K] rank of each candidate's token id in its depth
+  const int32_t *cand_by_rank;  // [B, L, K] each depth's candidate tokens in token-id order
   const uint8_t *positive;      // [B, L] some edge score of that depth is > 0
   const int32_t *base_pos;
   const int32_t *budget;        // [B] from the edge stage
@@ -1056,12 +1055,9 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
     budget0 = a.budget[b];
     pos0 = tid < L && a.positive[static_cast<int64_t>(b) * L + tid] != 0;
   }
-  // candidates and their rank by token id
-  for (int i = tid; i < L * K; i += kSelThreads) {
-    const int32_t tok = a.topk_ids[static_cast<int64_t>(b) * L * K + i];
-    const int r = a.id_rank[static_cast<int64_t>(b) * L * K + i];
-    s.cand[(i / K) * K + (r < K ? r : K - 1)] = tok;
-  }
+  // each depth's candidate tokens in token-id order (written by the edge stage)
+  for (int i = tid; i < L * K; i += kSelThreads)
+    s.cand[i] = a.cand_by_rank[static_cast<int64_t>(b) * L * K + i];
   // waves 1.. stage the edge rows (16-byte loads, all issued before the
   // stores) while wave 0 computes the budget: all of them when they fit, else
   // those of the first depths (as many whole depths as the stage holds)
@@ -1209,8 +1205,7 @@ hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_rou
   a.n_max = d.max_nodes;
   a.words = (d.max_nodes + 63) / 64;
   a.edge_rows = ws.edge_rows;
-  a.topk_ids = ws.topk_ids;
-  a.id_rank = ws.id_rank;
+  a.cand_by_rank = ws.cand_by_rank;
   a.positive = ws.positive;
   a.base_pos = in->base_pos;
   a.budget = out->budget;
