@@ -221,11 +221,10 @@ GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host 
  * graft_build_tree, and the same kernels, but the round's intermediates
  * (split-row partials, candidates, row statistics, edge rows, candidate
  * tables in token-id order, positive flags, hidden-state cosines) live in a
- * static device array of
- * GRAFT_STATIC_SCRATCH_BYTES per GPU instead of the context's workspace; the
- * context still provides the scorer's projections, SABA parameters, the
- * history ring and the device status.  The bytes needed grow with the batch:
- * 256-byte aligned parts of B*L*K*(4 + 4 + 1) + B*L*(12 + 1) + B*L*K*K*4 +
+ * static device array of GRAFT_STATIC_SCRATCH_BYTES per GPU instead of the
+ * context's workspace; the context still provides the scorer's projections,
+ * SABA parameters, the history ring and the device status.  The bytes needed grow with the batch:
+ * 256-byte aligned parts of B*L*K*(4 + 4 + 4) + B*L*(12 + 1) + B*L*K*K*4 +
  * 4*B*max(L - 1, 1) bytes, plus 8*(3 + K) bytes per split-row partial when
  * rows are split (fewer than about 1024 rows).  A batch whose need exceeds
  * the array returns GRAFT_ERR_UNSUPPORTED before anything is enqueued.  The
