@@ -230,13 +230,27 @@ __device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, do
   if (whole) return unordered_f64(s.thkey);
   // exact ranks inside the boundary bin (only the dead bit of p_info changes
   // here, and the comparisons read the other bits)
+  // rank = members with a higher score (independent loads, unrolled) plus,
+  // only when some member has the same score, those the full order puts first
   const int g = s.sc[kG];
   for (int j = tid; j < g; j += kSelThreads) {
     const int e = s.map[j];
-    int rank = 0;
-    for (int q = 0; q < g; ++q) rank += (q != j) && pool_before(s, K, s.map[q], e);
+    const double ve = s.p_score[e];
+    int rank = 0, same = 0;
+#pragma unroll 8
+    for (int q = 0; q < g; ++q) {
+      const double vq = s.p_score[s.map[q]];
+      rank += vq > ve;
+      same += vq == ve;
+    }
+    if (same > 1) {
+      for (int q = 0; q < g; ++q) {
+        const int eq = s.map[q];
+        rank += (q != j) && s.p_score[eq] == ve && pool_before(s, K, eq, e);
+      }
+    }
     if (rank >= need) atomicOr(&s.p_info[e], kDead);
-    if (rank == need - 1) s.theta = s.p_score[e];
+    if (rank == need - 1) s.theta = ve;
   }
   __syncthreads();
   return s.theta;
