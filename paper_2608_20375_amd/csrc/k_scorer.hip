@@ -200,8 +200,10 @@ __device__ __forceinline__ float seg_sum(float v) {
 // rounded up to a power of two), kRows = 64 / SEG parents at a time: lane c of
 // a run keeps child c's row in registers, reads the parent's row from LDS (one
 // address for the whole run), and forms the dot product, the centering over
-// the parent's children and the score.
-template <int SEG>
+// the parent's children and the score.  With m % 4 == 0 a row is KQ groups of
+// four (KQ = m / 4 rounded up to a power of two; the child's groups past m / 4
+// are zero), all of a parent row's loads issued before its products.
+template <int SEG, int KQ>
 __global__ void __launch_bounds__(kEdgeThreads)
 edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__restrict__ topk_ids,
             const float *__restrict__ topk_logq, const int32_t *__restrict__ root_token,
@@ -319,32 +321,37 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   const int64_t base = row * K * K;
   bool pos = false;
   const int m4 = m >> 2;
-  // the child's row, 16 bytes a register group (m % 4 == 0) or a float each
-  float4 cr[kMaxScoreDim / 4];
+  // the child's row, 16 bytes a register group (m % 4 == 0; groups past m / 4
+  // hold zeros) or a float each
+  float4 cr[KQ];
   if ((m & 3) == 0) {
     const float4 *c4 = reinterpret_cast<const float4 *>(s_chd + cc * mp);
 #pragma unroll
-    for (int q = 0; q < kMaxScoreDim / 4; ++q)
-      if (q < m4) cr[q] = c4[q];
+    for (int q = 0; q < KQ; ++q) cr[q] = c4[q < m4 ? q : 0];
+#pragma unroll
+    for (int q = 0; q < KQ; ++q)
+      if (q >= m4) cr[q] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   const float lq = s_lq[cc];
+  const int col = s_idr[cc];   // the child's column in selection's rows
   for (int p0 = 0; p0 < n_par; p0 += kRows) {
     const int p = p0 + lane / SEG;
     const bool valid = p < n_par && c < K;
     const int pp = p < n_par ? p : 0;
+    const int prow = s_pidr[pp];
     const float *pv = s_par + pp * mp;
     float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
     if ((m & 3) == 0) {
       const float4 *p4 = reinterpret_cast<const float4 *>(pv);
+      float4 x[KQ];
 #pragma unroll
-      for (int q = 0; q < kMaxScoreDim / 4; ++q) {
-        if (q < m4) {
-          const float4 x = p4[q], y = cr[q];
-          a0 = __builtin_fmaf(x.x, y.x, a0);
-          a1 = __builtin_fmaf(x.y, y.y, a1);
-          a2 = __builtin_fmaf(x.z, y.z, a2);
-          a3 = __builtin_fmaf(x.w, y.w, a3);
-        }
+      for (int q = 0; q < KQ; ++q) x[q] = p4[q < m4 ? q : 0];
+#pragma unroll
+      for (int q = 0; q < KQ; ++q) {
+        a0 = __builtin_fmaf(x[q].x, cr[q].x, a0);
+        a1 = __builtin_fmaf(x[q].y, cr[q].y, a1);
+        a2 = __builtin_fmaf(x[q].z, cr[q].z, a2);
+        a3 = __builtin_fmaf(x[q].w, cr[q].w, a3);
       }
     } else {
       const float *cv = s_chd + cc * mp;
@@ -358,7 +365,7 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
     if (valid) {
       // selection's copy is indexed by token-id rank (parent row, child
       // column); the exported table keeps the candidates' rank order
-      edge_rows[base + s_pidr[p] * K + s_idr[c]] = S;
+      edge_rows[base + prow * K + col] = S;
       if (edge_out) edge_out[base + p * K + c] = S;
     }
     pos |= valid && S > 0.f;
@@ -405,12 +412,21 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graf
                      sizeof(int32_t) * 6 * K;
   const FastDiv mdiv4 = make_fastdiv(static_cast<uint32_t>(m >= 4 ? m / 4 : 1));
   const dim3 grid(batch * d.num_pos), block(kEdgeThreads);
-#define GRAFT_EDGE(SEG)                                                                        \
-  hipLaunchKernelGGL(edge_kernel<SEG>, grid, block, lds, stream, d.num_pos, K, m,            \
+#define GRAFT_EDGE_KQ(SEG, KQ)                                                                 \
+  hipLaunchKernelGGL((edge_kernel<SEG, KQ>), grid, block, lds, stream, d.num_pos, K, m,      \
                      static_cast<int64_t>(d.vocab), mdiv4, ws.topk_ids, ws.topk_logq,       \
                      root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
                      ctx->scorer, ws.edge_rows, ws.cand_by_rank,                            \
                      ws.positive, edge_out, ctx->error_flag, sa, ctx->saba)
+  // groups of four per score row (the scalar path, m % 4 != 0, takes 2)
+  const int m4 = (m & 3) == 0 ? m / 4 : 0;
+#define GRAFT_EDGE(SEG)                                                                        \
+  do {                                                                                         \
+    if (m4 <= 2) GRAFT_EDGE_KQ(SEG, 2);                                                        \
+    else if (m4 <= 4) GRAFT_EDGE_KQ(SEG, 4);                                                   \
+    else if (m4 <= 8) GRAFT_EDGE_KQ(SEG, 8);                                                   \
+    else GRAFT_EDGE_KQ(SEG, 16);                                                               \
+  } while (0)
   if (K <= 1) GRAFT_EDGE(1);
   else if (K <= 2) GRAFT_EDGE(2);
   else if (K <= 4) GRAFT_EDGE(4);
@@ -419,6 +435,7 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graf
   else if (K <= 32) GRAFT_EDGE(32);
   else GRAFT_EDGE(64);
 #undef GRAFT_EDGE
+#undef GRAFT_EDGE_KQ
   return hipGetLastError();
 }
 
