@@ -45,26 +45,18 @@ projection_kernel(const float *__restrict__ emb, const float *__restrict__ gp,
 constexpr int kEdgeThreads = 64;   // one wave per (sequence, depth)
 constexpr int kGather = 8;         // projection loads (16 bytes) in flight per lane
 
-// Division by a runtime divisor d <= 64 of numerators below 2^26: a shift for
-// powers of two, else the high half of n * ceil(2^32 / d), which is exact in
-// that range (the error term n * (M d - 2^32) / 2^32 stays below 1).
+// Division by a runtime divisor d <= 64 of numerators n below 2^26, without a
+// branch: the high half of n * ceil(2^32 / d) in 64 bits.  Exact in that
+// range: with ceil(2^32 / d) = (2^32 + e) / d, 0 <= e < d, the quotient is
+// n / d plus n e / (d 2^32) < 2^-6 <= 1/d, which never reaches the next
+// integer.
 struct FastDiv {
-  uint32_t d, m, shift;
-  int pow2;
+  uint64_t m;
   __device__ __forceinline__ uint32_t div(uint32_t n) const {
-    return pow2 ? (n >> shift) : __umulhi(n, m);
+    return static_cast<uint32_t>((static_cast<uint64_t>(n) * m) >> 32);
   }
 };
-FastDiv make_fastdiv(uint32_t d) {
-  FastDiv f{d, 0u, 0u, 0};
-  if ((d & (d - 1)) == 0) {
-    f.pow2 = 1;
-    while ((1u << f.shift) < d) ++f.shift;
-  } else {
-    f.m = static_cast<uint32_t>(((1ull << 32) + d - 1) / d);
-  }
-  return f;
-}
+FastDiv make_fastdiv(uint32_t d) { return FastDiv{((1ull << 32) + d - 1) / d}; }
 
 // SABA inputs and outputs of one round (Sec. "State-Aware Budget Allocation").
 struct SabaArgs {
@@ -278,16 +270,24 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
     const int m4 = m >> 2;
     const int nq = K * m4, total = nq + n_par * m4;
     for (int base = 0; base < total; base += kGather * kEdgeThreads) {
-      float4 v[kGather];
+      // the batch's token ids first (LDS), then its projection loads
+      int32_t tok[kGather], j4s[kGather];
+      bool child[kGather];
 #pragma unroll
       for (int k = 0; k < kGather; ++k) {
         int t = base + k * kEdgeThreads + lane;
         t = t < total ? t : total - 1;
-        const int tt = t < nq ? t : t - nq;
-        const int r = static_cast<int>(mdiv4.div(static_cast<uint32_t>(tt))), j4 = tt - r * m4;
-        const float *src = t < nq ? Q + static_cast<int64_t>(s_cid[r]) * m
-                                  : P + static_cast<int64_t>(s_pid[r]) * m;
-        v[k] = reinterpret_cast<const float4 *>(src)[j4];
+        child[k] = t < nq;
+        const int tt = child[k] ? t : t - nq;
+        const int r = static_cast<int>(mdiv4.div(static_cast<uint32_t>(tt)));
+        j4s[k] = tt - r * m4;
+        tok[k] = child[k] ? s_cid[r] : s_pid[r];
+      }
+      float4 v[kGather];
+#pragma unroll
+      for (int k = 0; k < kGather; ++k) {
+        const float *src = (child[k] ? Q : P) + static_cast<int64_t>(tok[k]) * m;
+        v[k] = reinterpret_cast<const float4 *>(src)[j4s[k]];
       }
 #pragma unroll
       for (int k = 0; k < kGather; ++k) {
