@@ -173,8 +173,14 @@ __device__ __forceinline__ void hist_boundary(SelMem &s, int n_keep) {
   const int inc = wave_incl_scan(sum);
   if (lane == kWave - 1) s.wsum[wave] = inc;
   __syncthreads();
+  // the waves before this one: a fixed-count loop, so that the eight LDS
+  // reads are issued together
   int run = inc - sum;
-  for (int w = 0; w < wave; ++w) run += s.wsum[w];
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    const int v = s.wsum[w];
+    run += w < wave ? v : 0;
+  }
 #pragma unroll
   for (int j = 0; j < kBinsPer; ++j) {
     if (run < n_keep && n_keep <= run + c[j]) {
@@ -777,19 +783,29 @@ __device__ __forceinline__ int select_parallel_k(SelMem &s, const SelectArgs &a,
 // index.
 __device__ void canon_levels(SelMem &s, int n) {
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  const int per = (n + kSelThreads - 1) / kSelThreads;
+  const int per = (n + kSelThreads - 1) / kSelThreads;   // <= kPerThread
   const int lo = tid * per, hi = lo + per < n ? lo + per : n;
-  int cnt = 0;
-  for (int i = lo; i < hi; ++i) cnt += alive(s.p_info[i]) ? 1 : 0;
+  // the thread's entries' alive bits, every LDS read issued before any is used
+  uint32_t bits = 0;
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int i = lo + k < hi ? lo + k : 0;
+    const uint32_t info = s.p_info[i];
+    bits |= (lo + k < hi && alive(info)) ? 1u << k : 0u;
+  }
+  const int cnt = __popc(bits);
   const int inc = wave_incl_scan(cnt);
   if (lane == kWave - 1) s.wsum[wave] = inc;
   __syncthreads();
   int run = inc - cnt;
-  for (int w = 0; w < wave; ++w) run += s.wsum[w];
-  for (int i = lo; i < hi; ++i) {
-    const bool a = alive(s.p_info[i]);
-    s.map[i] = run;
-    run += a ? 1 : 0;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    const int v = s.wsum[w];
+    run += w < wave ? v : 0;
+  }
+  for (int k = 0; lo + k < hi; ++k) {
+    s.map[lo + k] = run;
+    run += (bits >> k) & 1u;
   }
   __syncthreads();
 }
