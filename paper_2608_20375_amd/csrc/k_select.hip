@@ -544,6 +544,40 @@ __device__ __forceinline__ double entry_append_cached(SelMem &s, int x, int K, i
   return append_row<KV>(s, v, kv, theta, dst, x, d, s.p_score[x], (dst << 8) | c);
 }
 
+// Smallest of the wave's fp64 values into s.lomin (as an ordered key; +inf is
+// neutral): DPP steps inside each row of 16 lanes, then one LDS atomic per row
+// (no cross-row lane exchange, whose LDS round trips would serialise).
+__device__ __forceinline__ void lomin_update(SelMem &s, double v) {
+  uint64_t k = v < INFINITY ? ordered_f64(v) : ~0ull;
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) {
+    const uint64_t ok = xor_lane_u64(k, o);
+    k = ok < k ? ok : k;
+  }
+  if ((lane_id() & 15) == 0 && k != ~0ull) atomicMin(&s.lomin, k);
+}
+
+// Largest and smallest float of the wave, in every lane: DPP steps inside the
+// rows of 16 lanes, then the four row results read as scalars.
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __uint_as_float(xor_lane(__float_as_uint(v), o)));
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+__device__ __forceinline__ float wave_min_f32(float v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v = fminf(v, __uint_as_float(xor_lane(__float_as_uint(v), o)));
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fminf(fminf(a, b), fminf(c, d));
+}
+
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
 // alive unexpanded entry lies in [x_lo, n).  rs: where the edge rows are read
 // (LdsRows, SplitRows).
@@ -569,12 +603,8 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
   // the depth-1 row's largest and smallest scores, in every wave (K <= 64)
   const float r0 = lane < K ? rs.at(lane) : 0.f;
-  float r_hi = lane < K ? r0 : -INFINITY, r_lo = lane < K ? r0 : INFINITY;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    r_hi = fmaxf(r_hi, __uint_as_float(xor_lane(__float_as_uint(r_hi), o)));
-    r_lo = fminf(r_lo, __uint_as_float(xor_lane(__float_as_uint(r_lo), o)));
-  }
+  const float r_hi = wave_max_f32(lane < K ? r0 : -INFINITY);
+  const float r_lo = wave_min_f32(lane < K ? r0 : INFINITY);
   if (tid == 0) s.lomin = ordered_f64(static_cast<double>(r_lo));
   __syncthreads();
   // every prefix scores at most its depth-1 ancestor, so at most the best
@@ -596,12 +626,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       const double v = static_cast<double>(rs.at(j / K)) + static_cast<double>(rs.at(pairs + j));
       pmin = v < pmin ? v : pmin;
     }
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const double ov = xor_lane_f64(pmin, o);
-      pmin = ov < pmin ? ov : pmin;
-    }
-    if (lane == 0 && pmin < INFINITY) atomicMin(&s.lomin, ordered_f64(pmin));
+    lomin_update(s, pmin);
     __syncthreads();
     const double lo = unordered_f64(s.lomin);
     const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
@@ -652,14 +677,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
     }
     const int inc = wave_incl_scan(sum);
     if (lane == kWave - 1) s.wsum[wave] = inc;
-    if (theta == -INFINITY) {
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const double ov = xor_lane_f64(vmin, o);
-        vmin = ov < vmin ? ov : vmin;
-      }
-      if (lane == 0) atomicMin(&s.lomin, ordered_f64(vmin));
-    }
+    if (theta == -INFINITY) lomin_update(s, vmin);
     __syncthreads();
     int base = 0, added = 0;
     for (int w = 0; w < kSelWaves; ++w) {
@@ -738,14 +756,7 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
     }
     // the smallest appended score (needed only while theta is unset): one LDS
     // atomic per wave
-    if (theta == -INFINITY) {
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const double ov = xor_lane_f64(amin, o);
-        amin = ov < amin ? ov : amin;
-      }
-      if (lane == 0 && amin < INFINITY) atomicMin(&s.lomin, ordered_f64(amin));
-    }
+    if (theta == -INFINITY) lomin_update(s, amin);
     __syncthreads();
     n += grown;
     n_alive += grown;
