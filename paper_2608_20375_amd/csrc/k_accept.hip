@@ -18,6 +18,7 @@ namespace graft {
 namespace {
 
 constexpr int kAccThreads = 256;
+static_assert(kMaxNodes % kAccThreads == 0 && kMaxL + 1 <= kAccThreads, "staging slots");
 
 // One workgroup per sequence.  Every thread issues its loads of the tree
 // (parents, tokens and, in per-node mode, the targets of all max_nodes slots;
@@ -36,13 +37,30 @@ accept_kernel(int n_max, int L, int window, const int32_t *__restrict__ n_nodes,
   const int64_t ob = static_cast<int64_t>(b) * n_max;
   const int n_raw = n_nodes[b];
   const int t_root = target_node ? target_root[b] : 0;
-  for (int i = tid; i < n_max; i += kAccThreads) {
-    s_par[i] = parents[ob + i];
-    s_tok[i] = tokens[ob + i];
-    if (target_node) s_tgt[i] = target_node[ob + i];
+  // a fixed number of slots per thread (indices clamped to the arrays), so
+  // that all the loads are issued before the first store
+  constexpr int kPer = kMaxNodes / kAccThreads;
+  int32_t vp[kPer], vt[kPer], vg[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = tid + k * kAccThreads;
+    const int64_t ic = ob + (i < n_max ? i : n_max - 1);
+    vp[k] = parents[ic];
+    vt[k] = tokens[ic];
+    vg[k] = target_node ? target_node[ic] : 0;
   }
-  if (!target_node)
-    for (int i = tid; i <= L; i += kAccThreads) s_tgt[i] = target_depth[static_cast<int64_t>(b) * (L + 1) + i];
+  // per-depth targets: L + 1 <= kMaxL + 1 entries, one per thread
+  const int32_t vd = (!target_node && tid <= L) ? target_depth[static_cast<int64_t>(b) * (L + 1) + tid] : 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = tid + k * kAccThreads;
+    if (i < n_max) {
+      s_par[i] = vp[k];
+      s_tok[i] = vt[k];
+      if (target_node) s_tgt[i] = vg[k];
+    }
+  }
+  if (!target_node && tid <= L) s_tgt[tid] = vd;
   __syncthreads();
   if (tid >= kWave) return;
   const int n = n_raw < n_max ? (n_raw < 0 ? 0 : n_raw) : n_max;
