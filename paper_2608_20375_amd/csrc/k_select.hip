@@ -73,7 +73,7 @@ struct SelMem {
   uint32_t p_info[kPoolCap];
   int32_t map[kPoolCap];
   int32_t aux[kPoolCap + 1];
-  int32_t run[kPoolCap];   // sibling run of each entry: first index << 8 | length
+  int32_t run[kPoolCap];   // run of each entry's children: first index << 8 | length
   union {
     struct {
       int32_t hist[kBins + 1];
@@ -91,6 +91,7 @@ struct SelMem {
   int32_t dcnt[kMaxL];   // nodes per depth
   int32_t doff[kMaxL];   // first canonical index of each depth
   int32_t wsum[kSelWaves];
+  int32_t first1[kMaxK + 1];   // first child index of each depth-1 entry (first expansion)
   double theta;
   unsigned long long thkey;   // ordered key of theta when a whole bin is kept
   unsigned long long lomin;   // ordered key of the smallest score appended
@@ -98,7 +99,7 @@ struct SelMem {
 };
 
 enum { kNPool = 0, kBudget, kMono, kBstar, kA, kBcnt, kG, kXfit, kMaxDepth, kNSel, kDepthN,
-       kMixed };
+       kMixed, kRootRun };
 
 __device__ __forceinline__ int32_t ptoken(const SelMem &s, int K, uint32_t info) {
   return s.cand[(pi_depth(info) - 1) * K + pi_rank(info)];
@@ -290,8 +291,15 @@ __device__ int pool_compact(SelMem &s, int n, int *x_lo) {
       keep_to[k] = s.aux[i];
     }
   }
+  int root_run = 0;
+  if (threadIdx.x == 0) {
+    const int32_t rv = s.sc[kRootRun];
+    const int r0 = rv >> 8, r1 = r0 + (rv & 255);
+    root_run = (s.aux[r0] << 8) | (s.aux[r1] - s.aux[r0]);
+  }
   *x_lo = s.aux[*x_lo];
   __syncthreads();
+  if (threadIdx.x == 0) s.sc[kRootRun] = root_run;
 #pragma unroll
   for (int k = 0; k < kPerThread; ++k)
     if (keep_to[k] >= 0) {
@@ -497,7 +505,8 @@ __device__ __forceinline__ double prune_bound(SelMem &s, const RS &rs, int K, in
 template <class RS>
 __device__ __forceinline__ double entry_append(SelMem &s, const RS &rs, int x, int K, int kv,
                                                int KVP, double theta, int dst, int c) {
-  const int32_t runv = (dst << 8) | c;
+  s.run[x] = (dst << 8) | c;
+  const int32_t runv = 0;   // a new entry has no children yet
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
   const float *row = rs.row((d * K + pi_rank(info)) * K);
@@ -541,7 +550,8 @@ __device__ __forceinline__ double entry_append_cached(SelMem &s, int x, int K, i
                                                       const float4 (&v)[KV]) {
   const uint32_t info = s.p_info[x];
   const int d = pi_depth(info);
-  return append_row<KV>(s, v, kv, theta, dst, x, d, s.p_score[x], (dst << 8) | c);
+  s.run[x] = (dst << 8) | c;   // x's children; a new entry has none yet
+  return append_row<KV>(s, v, kv, theta, dst, x, d, s.p_score[x], 0);
 }
 
 // Smallest of the wave's fp64 values into s.lomin (as an ordered key; +inf is
@@ -598,14 +608,17 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   for (int r = tid; r < K; r += kSelThreads) {
     s.p_score[r] = static_cast<double>(rs.at(r));
     s.p_info[r] = pinfo(-1, 1, r);
-    s.run[r] = K;   // the depth-1 run starts at 0
+    s.run[r] = 0;
   }
   for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
   // the depth-1 row's largest and smallest scores, in every wave (K <= 64)
   const float r0 = lane < K ? rs.at(lane) : 0.f;
   const float r_hi = wave_max_f32(lane < K ? r0 : -INFINITY);
   const float r_lo = wave_min_f32(lane < K ? r0 : INFINITY);
-  if (tid == 0) s.lomin = ordered_f64(static_cast<double>(r_lo));
+  if (tid == 0) {
+    s.lomin = ordered_f64(static_cast<double>(r_lo));
+    s.sc[kRootRun] = K;   // the depth-1 entries: first index 0, K of them
+  }
   __syncthreads();
   // every prefix scores at most its depth-1 ancestor, so at most the best
   // depth-1 prefix, which is never dropped
@@ -642,6 +655,63 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
       theta = edge - 1e-9 * (fabs(edge) + fabs(hi) + 1.0);
     }
     pruned = true;
+  }
+  if (L > 1 && K + K * K <= kPoolCap) {
+    // The first expansion, of the K depth-1 entries, spread over their K * K
+    // (parent, child) pairs (a few per thread) rather than over the K parents.
+    // It never takes the prune step (the first bound above is that step; with
+    // K + K * K <= N the children are within N; with N < K theta comes from
+    // the exact selection here) and always fits in the pool.
+    if (n_alive > n_target) {
+      theta = pool_select(s, K, n, n_target, unordered_f64(s.lomin), hi);
+      n_alive = n_target;
+    }
+    const int pairs = K * K;   // pair j: child j % K of depth-1 entry j / K, row rs[K * K + j]
+    const int pp = (pairs + kSelThreads - 1) / kSelThreads;
+    const int j0 = tid * pp < pairs ? tid * pp : pairs;
+    const int j1 = j0 + pp < pairs ? j0 + pp : pairs;
+    int sum = 0;
+    double vmin = INFINITY;
+    for (int j = j0; j < j1; ++j) {
+      const int r = j / K;
+      const double sc = s.p_score[r] + static_cast<double>(rs.at(pairs + j));
+      if (alive(s.p_info[r]) && sc >= theta) {
+        ++sum;
+        vmin = sc < vmin ? sc : vmin;
+      }
+    }
+    const int inc = wave_incl_scan(sum);
+    if (lane == kWave - 1) s.wsum[wave] = inc;
+    if (theta == -INFINITY) lomin_update(s, vmin);
+    __syncthreads();
+    int base = 0, added = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+      const int v = s.wsum[w];
+      base += w < wave ? v : 0;
+      added += v;
+    }
+    // this thread's children in pool order from its offset; the owner of an
+    // entry's first pair records where the entry's children start
+    int dst = K + base + inc - sum;
+    for (int j = j0; j < j1; ++j) {
+      const int r = j / K, c = j - r * K;
+      if (c == 0) s.first1[r] = dst;
+      const double sc = s.p_score[r] + static_cast<double>(rs.at(pairs + j));
+      if (alive(s.p_info[r]) && sc >= theta) {
+        s.p_score[dst] = sc;
+        s.p_info[dst] = pinfo(r, 2, c);
+        s.run[dst] = 0;
+        ++dst;
+      }
+    }
+    if (j0 < j1 && j1 == pairs) s.first1[K] = dst;
+    __syncthreads();
+    if (tid < K) s.run[tid] = (s.first1[tid] << 8) | (s.first1[tid + 1] - s.first1[tid]);
+    n += added;
+    n_alive += added;
+    x_lo = K;
+    pruned = false;
   }
   for (;;) {
     if (n_alive > n_target) {
@@ -847,7 +917,7 @@ __device__ void canon_preorder(SelMem &s, int L, int K, int n, int n_sel) {
     const uint32_t info = s.p_info[i];
     if (!alive(info)) continue;
     const int p = pi_parent(info), mine = pi_rank(info);
-    const int32_t rv = s.run[i];
+    const int32_t rv = p < 0 ? s.sc[kRootRun] : s.run[p];   // i's siblings
     const int lo = rv >> 8, hi = lo + (rv & 255);
     int left = 0;
     for (int j0 = lo; j0 < hi; j0 += 16) {
