@@ -633,13 +633,20 @@ def test_first_expansion_bound_budget_edges(L, K, V, n_max):
     ctx.close()
 
 
-def test_flat_scores_force_pool_compaction():
+@pytest.mark.parametrize("K", [16, 64])
+def test_flat_scores_force_pool_compaction(K):
     """Uniform logits and a zero scorer make every edge score equal (and a few
-    tie levels in the second sequence): the first expansion overflows the
-    pool, partial expansions and tie ranking follow, and a later expansion
-    only fits after the dead entries are compacted (their sibling runs are
-    remapped).  The trees must still match the oracle bit for bit."""
-    w = S.workload(0, batch=2, V=3000, L=4, K=64, n_max=1024, fixed_budget=1024)
+    tie levels in the second sequence).  K = 64: the first expansion overflows
+    the pool, partial expansions and tie ranking follow, and a later expansion
+    only fits after the dead entries are compacted (the runs of children are
+    remapped).  K = 16: the first expansion runs over (parent, child) pairs and
+    fills the depth-1 entries' runs; the prune bound admits all 4,096 depth-3
+    children, which do not fit, so 239 of the 256 depth-2 entries are
+    expanded; the exact selection ranks 3,824 tied entries; the children of
+    the last 17 depth-2 entries fit only after the pool is compacted; the
+    preorder numbering reads the remapped runs.  The trees must still match
+    the oracle bit for bit."""
+    w = S.workload(0, batch=2, V=3000, L=4, K=K, n_max=1024, fixed_budget=1024)
     inp = S.gen_round(w, with_targets=False)
     flat = np.zeros((w.L, w.V), np.float32)
     g = np.random.default_rng(9)
