@@ -76,7 +76,7 @@ struct SelMem {
   int32_t run[kPoolCap];   // run of each entry's children: first index << 8 | length
   union {
     struct {
-      int32_t hist[kBins + 1];
+      alignas(16) int32_t hist[kBins + 1];
       int32_t pcnt[kBins + 1];
     } b;
     struct {                        // serial selector only
@@ -99,7 +99,7 @@ struct SelMem {
 };
 
 enum { kNPool = 0, kBudget, kMono, kBstar, kA, kBcnt, kG, kXfit, kMaxDepth, kNSel, kDepthN,
-       kMixed, kRootRun };
+       kMixed, kRootRun, kRHi };
 
 __device__ __forceinline__ int32_t ptoken(const SelMem &s, int K, uint32_t info) {
   return s.cand[(pi_depth(info) - 1) * K + pi_rank(info)];
@@ -151,6 +151,7 @@ __device__ int block_scan(SelMem &s, int32_t *data, int n) {
 
 constexpr int kBinsPer = kBins / kSelThreads;   // bins per thread in the scan
 static_assert(kBins == kBinsPer * kSelThreads && kBinsPer == 4, "4 bins per thread");
+static_assert(kBins % (4 * kWave) == 0, "the histogram clears as int4 stores by one wave");
 // Histogram slot of a bin: bin 4 t + j of thread t's run is stored at
 // j * kSelThreads + t, so the scan's reads (thread t, run position j) hit
 // consecutive words.
@@ -205,7 +206,7 @@ __device__ __forceinline__ int score_bin(double v, double hi, double scale) {
 // n_keep alive entries, all with scores in [lo, hi], and hist[] cleared (it
 // is left cleared).
 __device__ double pool_select(SelMem &s, int K, int n, int n_keep, double lo, double hi) {
-  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int tid = threadIdx.x;
   const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
   for (int i = tid; i < n; i += kSelThreads) {
     const bool live = alive(s.p_info[i]);
@@ -462,7 +463,7 @@ __device__ __forceinline__ Counted entry_count(const SelMem &s, const RS &rs, in
 template <class RS>
 __device__ __forceinline__ double prune_bound(SelMem &s, const RS &rs, int K, int kv, int KVP, int n, int x_lo,
                               int i0, int per, int n_keep, double theta, double lo, double hi) {
-  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int tid = threadIdx.x;
   const double scale = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
   for (int i = tid; i < n; i += kSelThreads) {
     const bool live = alive(s.p_info[i]);
@@ -588,6 +589,31 @@ __device__ __forceinline__ float wave_min_f32(float v) {
   return fminf(fminf(a, b), fminf(c, d));
 }
 
+// The parallel selector's starting state, set up by wave 0 while the other
+// waves stage the edge rows: the K depth-1 entries in token-id order (r0: the
+// depth-1 row, one score per lane, K <= 64), the root's run, lomin at the
+// smallest depth-1 score, the largest one in sc[kRHi] (float bits), and a
+// cleared histogram.  Harmless when the serial selector runs instead: it
+// rewrites the pool from index 0 and uses the union as its heap.
+__device__ __forceinline__ void select_setup(SelMem &s, int K, float r0) {
+  const int lane = lane_id();
+  int4 *h4 = reinterpret_cast<int4 *>(s.u.b.hist);
+#pragma unroll
+  for (int k = 0; k < kBins / 4 / kWave; ++k) h4[lane + k * kWave] = make_int4(0, 0, 0, 0);
+  if (lane < K) {
+    s.p_score[lane] = static_cast<double>(r0);
+    s.p_info[lane] = pinfo(-1, 1, lane);
+    s.run[lane] = 0;
+  }
+  const float r_hi = wave_max_f32(lane < K ? r0 : -INFINITY);
+  const float r_lo = wave_min_f32(lane < K ? r0 : INFINITY);
+  if (lane == 0) {
+    s.lomin = ordered_f64(static_cast<double>(r_lo));
+    s.sc[kRootRun] = K;   // the depth-1 entries: first index 0, K of them
+    s.sc[kRHi] = __float_as_int(r_hi);
+  }
+}
+
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
 // alive unexpanded entry lies in [x_lo, n).  rs: where the edge rows are read
 // (LdsRows, SplitRows).
@@ -605,24 +631,11 @@ __device__ __forceinline__ int select_parallel(SelMem &s, const SelectArgs &a, c
   constexpr int kCache = KVT == 0 ? 0 : KVT <= 8 ? 2 : 1;
   constexpr int KVC = KVT > 0 ? KVT : 1;
   float4 cache[kCache > 0 ? kCache : 1][KVC];
-  for (int r = tid; r < K; r += kSelThreads) {
-    s.p_score[r] = static_cast<double>(rs.at(r));
-    s.p_info[r] = pinfo(-1, 1, r);
-    s.run[r] = 0;
-  }
-  for (int i = tid; i < kBins; i += kSelThreads) s.u.b.hist[i] = 0;
-  // the depth-1 row's largest and smallest scores, in every wave (K <= 64)
-  const float r0 = lane < K ? rs.at(lane) : 0.f;
-  const float r_hi = wave_max_f32(lane < K ? r0 : -INFINITY);
-  const float r_lo = wave_min_f32(lane < K ? r0 : INFINITY);
-  if (tid == 0) {
-    s.lomin = ordered_f64(static_cast<double>(r_lo));
-    s.sc[kRootRun] = K;   // the depth-1 entries: first index 0, K of them
-  }
-  __syncthreads();
-  // every prefix scores at most its depth-1 ancestor, so at most the best
-  // depth-1 prefix, which is never dropped
-  const double hi = static_cast<double>(r_hi);
+  // The depth-1 entries, the cleared histogram, lomin and the root run were
+  // set up with the staging (select_setup).  Every prefix scores at most its
+  // depth-1 ancestor, so at most the best depth-1 prefix, which is never
+  // dropped.
+  const double hi = static_cast<double>(__int_as_float(s.sc[kRHi]));
   double theta = -INFINITY;
   bool pruned = false;
   int n = K, n_alive = K, x_lo = 0;
@@ -1162,9 +1175,11 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   // wave 0: the budget (computed by the edge stage) and the sign flags
   int budget0 = 0;
   bool pos0 = false;
+  float r0 = 0.f;   // the depth-1 row, one score per lane
   if (tid < kWave) {
     budget0 = a.budget[b];
     pos0 = tid < L && a.positive[static_cast<int64_t>(b) * L + tid] != 0;
+    r0 = ss[tid < K ? tid : 0];
   }
   // each depth's candidate tokens in token-id order (written by the edge stage)
   for (int i = tid; i < L * K; i += kSelThreads)
@@ -1196,6 +1211,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
 
   // ---------------- budget and sign flags ----------------
   if (tid < kWave) {
+    select_setup(s, K, r0);
     const bool mono = __ballot(pos0) == 0ull;
     if (tid == 0) {
       s.sc[kBudget] = budget0;
