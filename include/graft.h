@@ -209,6 +209,19 @@ GRAFT_API int graft_get_history(graft_ctx *ctx, int32_t batch, int32_t *ring, in
 GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host */,
                      const graft_tree_out *out /* host */, graft_stream_t stream);
 
+/* Where steps 2 and 3 run (an execution choice; the results are the same
+ * bits either way).  With enable != 0 (the default of a new context) the
+ * selection kernel computes a sequence's edge scores and its budget itself
+ * whenever the edge rows and the projection rows fit its on-chip memory:
+ * num_pos * top_k^2 <= 4096, score_dim 16 or 32, and
+ * L K (2 score_dim + 11) <= 24576 with L = num_pos, K = top_k; the round
+ * then launches no separate edge stage.  With enable == 0
+ * the edge stage always runs.  *active (host, may be NULL) receives 1 when
+ * the fused path is taken for this context's sizes and installed scorer, else
+ * 0.  Host only, no device work; the scorer's score_dim counts, so call it
+ * after graft_set_scorer to read *active. */
+GRAFT_API int graft_set_fusion(graft_ctx *ctx, int32_t enable, int32_t *active /* host */);
+
 /* Size of the library's static scratch array used by graft_build_tree_static:
  * 24 MiB, the per-round intermediates of a batch of 128 sequences at L = 32
  * and K = 32 (about 18 MB).  Each GPU the library runs on holds one copy until
@@ -314,7 +327,8 @@ GRAFT_API int graft_synth_node_targets(graft_ctx *ctx, int32_t batch, uint64_t s
  * separately): timing-only HIP events (no system-scope fence) are recorded on
  * the call's stream around every stage, 0 = logits pass, 1 = hidden-state
  * cosines, edge scoring and the SABA budget, 2 = selection, emission and mask,
- * 3 = acceptance.  graft_profile_end synchronizes the events, writes
+ * 3 = acceptance (with the fused path of graft_set_fusion, edge scoring and
+ * the budget are timed in stage 2).  graft_profile_end synchronizes the events, writes
  * the summed milliseconds stage_ms[4] and the number of timed launches
  * stage_calls[4] (host arrays), and disarms.  Not for concurrent use. */
 GRAFT_API int graft_profile_begin(graft_ctx *ctx, int32_t max_calls);

@@ -21,7 +21,7 @@ _lib = None
 
 EXPORTED_SYMBOLS = (
     "graft_create", "graft_destroy", "graft_set_scorer", "graft_set_saba", "graft_set_history",
-    "graft_get_history",
+    "graft_get_history", "graft_set_fusion",
     "graft_build_tree", "graft_build_tree_static", "graft_accept", "graft_get_device_status",
     "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end", "graft_status_string", "graft_last_error",
     "graft_mask_to_bias", "graft_commit_accepted", "graft_tdes_create", "graft_tdes_destroy",
@@ -127,6 +127,7 @@ def lib():
         L.graft_set_saba.argtypes = [vp, C.POINTER(SabaDesc)]
         L.graft_set_history.argtypes = [vp, i32, vp, vp]
         L.graft_get_history.argtypes = [vp, i32, vp, vp, vp]
+        L.graft_set_fusion.argtypes = [vp, i32, C.POINTER(C.c_int32)]
         L.graft_build_tree.argtypes = [vp, C.POINTER(RoundIn), C.POINTER(TreeOut), vp]
         L.graft_build_tree_static.argtypes = [vp, C.POINTER(RoundIn), C.POINTER(TreeOut), vp]
         L.graft_accept.argtypes = [vp, i32, vp, vp, vp, C.POINTER(Targets), vp, vp, vp, i32, vp]
@@ -155,7 +156,7 @@ def lib():
         L.graft_last_error.argtypes = []
         L.graft_last_error.restype = C.c_char_p
         for n in ("graft_create", "graft_set_scorer", "graft_set_saba", "graft_set_history",
-                  "graft_get_history",
+                  "graft_get_history", "graft_set_fusion",
                   "graft_build_tree", "graft_build_tree_static", "graft_accept",
                   "graft_get_device_status",
                   "graft_synth_node_targets", "graft_profile_begin", "graft_profile_end",
@@ -293,6 +294,15 @@ class Context:
         d = SabaDesc(C.cast(arr, C.c_void_p), len(budgets), (C.c_float * 4)(*map(float, phi)),
                      float(tau_min), float(c0), float(c1), float(c2))
         _check(lib().graft_set_saba(self._h, C.byref(d)), "graft_set_saba")
+
+    def set_fusion(self, enable=True):
+        """Lets the selection kernel compute the edge scores and the budget
+        itself when the rows fit its stage (graft_set_fusion); returns True
+        when that path is taken for this context."""
+        active = C.c_int32(0)
+        _check(lib().graft_set_fusion(self._h, 1 if enable else 0, C.byref(active)),
+               "graft_set_fusion")
+        return bool(active.value)
 
     def set_history(self, init):
         _need(init, "init", (1,), self.dims.hist_window)

@@ -162,7 +162,7 @@ int build_tree_with(graft_ctx *ctx, const graft_round_in *in, const graft_tree_o
       return hip_fail(e, what);
     }
   }
-  e = graft::launch_edge_scores(ctx, ws, in, out, s);
+  if (!graft::edges_fused(ctx)) e = graft::launch_edge_scores(ctx, ws, in, out, s);
   if (e != hipSuccess) {
     snprintf(what, sizeof what, "%s: edge scores and budget", who);
     return hip_fail(e, what);
@@ -220,6 +220,7 @@ int graft_create(const graft_dims *dims, graft_ctx **out) {
   graft_ctx *c = new (std::nothrow) graft_ctx();
   if (!c) return fail(GRAFT_ERR_OUT_OF_MEMORY, "graft_create: host allocation failed");
   c->dims = d;
+  c->fuse_edges = true;
   (void)hipGetDevice(&c->device);
   const size_t B = d.max_batch;
   const int64_t ws_bytes =
@@ -252,6 +253,13 @@ void graft_destroy(graft_ctx *ctx) {
   if (!ctx) return;
   (void)hipDeviceSynchronize();
   free_ctx(ctx);
+}
+
+int graft_set_fusion(graft_ctx *ctx, int32_t enable, int32_t *active) {
+  if (!ctx) return fail(GRAFT_ERR_INVALID_ARG, "graft_set_fusion: NULL context");
+  ctx->fuse_edges = enable != 0;
+  if (active) *active = ctx->has_scorer && graft::edges_fused(ctx) ? 1 : 0;
+  return GRAFT_OK;
 }
 
 int graft_set_scorer(graft_ctx *ctx, const graft_scorer_desc *desc, graft_stream_t stream) {

@@ -255,6 +255,7 @@ struct graft_ctx {
   float *depth_emb;        // [L, m] or nullptr
   graft::ScorerParams scorer;
   bool has_scorer;
+  bool fuse_edges;         // graft_set_fusion (default on)
   graft::SabaParams saba;
   bool has_saba;
   // history ring
@@ -293,6 +294,9 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graf
                               const graft_tree_out *out, hipStream_t stream);
 hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
                          const graft_tree_out *out, hipStream_t stream);
+// True when the selection kernel computes the edge scores and the budget
+// itself (the rows fit its LDS stage), so the round launches no edge stage.
+bool edges_fused(const graft_ctx *ctx);
 hipError_t launch_accept(graft_ctx *ctx, int batch, const int32_t *n_nodes,
                          const int32_t *tokens, const int32_t *parents,
                          const graft_targets *t, int32_t *acc_len, int32_t *acc_nodes,

@@ -13,12 +13,12 @@
 //   so selection appends a parent's children in canonical order by filtering
 //   the row against its threshold, with no ranking; the exported table keeps
 //   the candidates' logit-rank order.
-// The K x m x K contraction is at most 64 x 64 x 64 per (sequence, depth):
-// VALU work, each lane keeping one child's projection in registers and
-// reading the parents' rows from LDS as broadcasts; there is no dense tile to
-// feed MFMA.  The depth-1 block of each sequence also computes its SABA
-// budget.
+// The K x m x K contraction of a (sequence, depth), at most 64 x 64 x 64, runs
+// on fp32 matrix cores in 16 x 16 tiles (edge_tiles); the depth-1 block of
+// each sequence also computes its SABA budget.
 #include "graft_internal.h"
+#include "edge_mfma.h"
+#include "saba_device.h"
 
 namespace graft {
 namespace {
@@ -58,144 +58,14 @@ struct FastDiv {
 };
 FastDiv make_fastdiv(uint32_t d) { return FastDiv{((1ull << 32) + d - 1) / d}; }
 
-// SABA inputs and outputs of one round (Sec. "State-Aware Budget Allocation").
-struct SabaArgs {
-  const float *row_stats;       // [B, L, 3]: lse, maxprob, entropy
-  const float *hist;            // [B] caller's hist_t, or nullptr: the device ring
-  const int32_t *hist_ring;     // [B, window]
-  const int32_t *prefix_len;    // [B] or nullptr (0)
-  const int32_t *fixed_budget;  // [B]: budgets given by the caller, or nullptr: SABA
-  const float *adj_cos;         // [B, L - 1] adjacent hidden-state cosines, or nullptr
-  int window;
-  int32_t *budget;              // [B] out
-  float *saba_state;            // [B, 4] out (conf, ent or degen, hist, tau) or nullptr
-};
-
-// B_t of sequence b by one wave: conf is the mean of the rows' top-1
-// probability; the second feature is degen = mean_d r_d + (r_{L-1} - r_1)
-// over the adjacent hidden-state cosines when they are given, else the mean
-// row entropy standing in for it; hist is the caller's value or the ring's
-// mean; tau = max(phi . [1, conf, feature, hist], tau_min); U(B) = (1 -
-// exp(-B/tau)) / (c0 + c1 B + c2 B prefix) (eqs. saba-gain, saba-cost) for
-// every grid budget, one lane each in fp64; B_t = the smallest budget with the
-// largest U (eq. saba-objective).
-// The budget's inputs, one wave's lanes; loaded before the edge work so that
-// their latency overlaps it.
-struct SabaIn {
-  float f_conf, f_ent, f_r, f_hist;
-  int32_t ring, prefix_i, fixed, grid;
-};
-__device__ __forceinline__ SabaIn saba_load(const SabaArgs &a, const SabaParams &sp, int b, int L) {
-  const int lane = lane_id();
-  SabaIn in;
-  const float *rs = a.row_stats + (static_cast<int64_t>(b) * L + (lane < L ? lane : 0)) * 3;
-  in.f_conf = rs[1];
-  in.f_ent = rs[2];
-  const int np = L - 1;
-  in.f_r = (a.adj_cos && lane < np) ? a.adj_cos[static_cast<int64_t>(b) * np + lane] : 0.f;
-  in.f_hist = a.hist ? a.hist[b] : 0.f;
-  in.ring = (!a.hist && lane < a.window) ? a.hist_ring[static_cast<int64_t>(b) * a.window + lane] : 0;
-  in.prefix_i = a.prefix_len ? a.prefix_len[b] : 0;
-  in.fixed = a.fixed_budget ? a.fixed_budget[b] : 0;
-  in.grid = lane < sp.n_grid ? sp.grid[lane] : 0;
-  return in;
-}
-
-__device__ void saba_budget(const SabaArgs &a, const SabaParams &sp, int b, int L, const SabaIn &in) {
-  const int lane = lane_id();
-  const float f_conf = in.f_conf, f_ent = in.f_ent, f_r = in.f_r, f_hist = in.f_hist;
-  const int32_t ring = in.ring, prefix_i = in.prefix_i, fixed = in.fixed, grid = in.grid;
-  const int np = L - 1;
-  double hist;
-  if (a.hist) {
-    hist = static_cast<double>(f_hist);
-  } else {
-    int64_t v = ring;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1)
-      v += static_cast<int64_t>(xor_lane_u64(static_cast<uint64_t>(v), o));
-    hist = static_cast<double>(v) / static_cast<double>(a.window);
-  }
-  double conf = lane < L ? static_cast<double>(f_conf) : 0.0;
-  double ent = lane < L ? static_cast<double>(f_ent) : 0.0;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    conf += xor_lane_f64(conf, o);
-    ent += xor_lane_f64(ent, o);
-  }
-  conf /= static_cast<double>(L);
-  ent /= static_cast<double>(L);
-  if (a.adj_cos) {
-    // degen from the cosines r_1 .. r_{L-1} (lanes 0 .. L-2); 0 without a pair
-    double r = lane < np ? static_cast<double>(f_r) : 0.0;
-    const double r_first = static_cast<double>(__shfl(f_r, 0));
-    const double r_last = static_cast<double>(__shfl(f_r, np > 0 ? np - 1 : 0));
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) r += xor_lane_f64(r, o);
-    ent = np > 0 ? r / static_cast<double>(np) + (r_last - r_first) : 0.0;
-  }
-  double tau = 0.0;
-  int budget;
-  if (!a.fixed_budget) {
-    tau = static_cast<double>(sp.phi[0]) + static_cast<double>(sp.phi[1]) * conf +
-          static_cast<double>(sp.phi[2]) * ent + static_cast<double>(sp.phi[3]) * hist;
-    if (tau < static_cast<double>(sp.tau_min)) tau = static_cast<double>(sp.tau_min);
-    const double prefix = static_cast<double>(prefix_i);
-    // the first maximum: largest U, ties (and a non-number U) to the smaller index
-    double u = -INFINITY;
-    if (lane < sp.n_grid) {
-      const double B = static_cast<double>(grid);
-      u = (1.0 - exp(-B / tau)) / (static_cast<double>(sp.c0) + static_cast<double>(sp.c1) * B +
-                                   static_cast<double>(sp.c2) * B * prefix);
-      if (!(u == u)) u = -INFINITY;
-    }
-    int best = lane;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const double ou = xor_lane_f64(u, o);
-      const int ob = static_cast<int>(xor_lane(static_cast<uint32_t>(best), o));
-      if (ou > u || (ou == u && ob < best)) {
-        u = ou;
-        best = ob;
-      }
-    }
-    budget = __builtin_amdgcn_readlane(grid, best < sp.n_grid ? best : 0);
-  } else {
-    budget = fixed;
-  }
-  if (lane == 0) {
-    a.budget[b] = budget;
-    if (a.saba_state) {
-      a.saba_state[b * 4 + 0] = static_cast<float>(conf);
-      a.saba_state[b * 4 + 1] = static_cast<float>(ent);
-      a.saba_state[b * 4 + 2] = static_cast<float>(hist);
-      a.saba_state[b * 4 + 3] = static_cast<float>(tau);
-    }
-  }
-}
-
-// Sum over each run of SEG consecutive lanes, in every lane of the run.
-template <int SEG>
-__device__ __forceinline__ float seg_sum(float v) {
-#pragma unroll
-  for (int stride = 1; stride < SEG; stride <<= 1)
-    v += __uint_as_float(xor_lane(__float_as_uint(v), stride));
-  return v;
-}
-
 // One wave per (sequence b, depth l).  Dynamic LDS: parents [K][mp],
 // children [K][mp] (rows of m floats padded to a multiple of 4 plus 4: 16-byte
 // aligned rows that start on different banks), depth embedding [m], log q [K],
 // token ids [K], their ranks by id [K], clamped child and parent ids [K],
-// parent tokens [K] and their ranks by id [K].
-// The (parent, child) pairs are processed SEG lanes per parent (SEG = K
-// rounded up to a power of two), kRows = 64 / SEG parents at a time: lane c of
-// a run keeps child c's row in registers, reads the parent's row from LDS (one
-// address for the whole run), and forms the dot product, the centering over
-// the parent's children and the score.  With m % 4 == 0 a row is KQ groups of
-// four (KQ = m / 4 rounded up to a power of two; the child's groups past m / 4
-// are zero), all of a parent row's loads issued before its products.
-template <int SEG, int KQ>
+// parent tokens [K] and their ranks by id [K].  The scores come from
+// edge_tiles<MK, NT> when m = 4 MK is a multiple of 16 (NT column tiles of
+// 16 children), else from edge_passes<KQ> (KQ >= ceil(m / 4)).
+template <int MK, int NT, int KQ>
 __global__ void __launch_bounds__(kEdgeThreads)
 edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__restrict__ topk_ids,
             const float *__restrict__ topk_logq, const int32_t *__restrict__ root_token,
@@ -312,64 +182,19 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   }
   __syncthreads();
 
-  // per parent p (SEG lanes, child c = lane % SEG):
-  //   f = s * <P[p] + u, Q[c] + u> / sqrt(m),  S = log q(c) + beta * (f - mean_c f)
   const float fscale = sp.scale / sqrtf(static_cast<float>(m));
-  constexpr int kRows = kEdgeThreads / SEG;
-  const int c = lane & (SEG - 1);
-  const int cc = c < K ? c : 0;
   const int64_t base = row * K * K;
-  bool pos = false;
-  const int m4 = m >> 2;
-  // the child's row, 16 bytes a register group (m % 4 == 0; groups past m / 4
-  // hold zeros) or a float each
-  float4 cr[KQ];
-  if ((m & 3) == 0) {
-    const float4 *c4 = reinterpret_cast<const float4 *>(s_chd + cc * mp);
-#pragma unroll
-    for (int q = 0; q < KQ; ++q) cr[q] = c4[q < m4 ? q : 0];
-#pragma unroll
-    for (int q = 0; q < KQ; ++q)
-      if (q >= m4) cr[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  const float lq = s_lq[cc];
-  const int col = s_idr[cc];   // the child's column in selection's rows
-  for (int p0 = 0; p0 < n_par; p0 += kRows) {
-    const int p = p0 + lane / SEG;
-    const bool valid = p < n_par && c < K;
-    const int pp = p < n_par ? p : 0;
-    const int prow = s_pidr[pp];
-    const float *pv = s_par + pp * mp;
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-    if ((m & 3) == 0) {
-      const float4 *p4 = reinterpret_cast<const float4 *>(pv);
-      float4 x[KQ];
-#pragma unroll
-      for (int q = 0; q < KQ; ++q) x[q] = p4[q < m4 ? q : 0];
-#pragma unroll
-      for (int q = 0; q < KQ; ++q) {
-        a0 = __builtin_fmaf(x[q].x, cr[q].x, a0);
-        a1 = __builtin_fmaf(x[q].y, cr[q].y, a1);
-        a2 = __builtin_fmaf(x[q].z, cr[q].z, a2);
-        a3 = __builtin_fmaf(x[q].w, cr[q].w, a3);
-      }
-    } else {
-      const float *cv = s_chd + cc * mp;
-#pragma unroll 4
-      for (int j = 0; j < m; ++j) a0 = __builtin_fmaf(pv[j], cv[j], a0);
-    }
-    const float f = fscale * ((a0 + a1) + (a2 + a3));
-    float mean = 0.f;
-    if (sp.center) mean = seg_sum<SEG>(valid ? f : 0.f) / static_cast<float>(K);
-    const float S = (lq + sp.beta * (f - mean)) + 0.0f;   // -0 -> +0
-    if (valid) {
-      // selection's copy is indexed by token-id rank (parent row, child
-      // column); the exported table keeps the candidates' rank order
-      edge_rows[base + prow * K + col] = S;
-      if (edge_out) edge_out[base + p * K + c] = S;
-    }
-    pos |= valid && S > 0.f;
-  }
+  // selection's copy is indexed by token-id rank (parent row, child column);
+  // the exported table keeps the candidates' rank order
+  const int32_t *prank = l == 0 ? nullptr : s_pidr;
+  float *out = edge_out ? edge_out + base : nullptr;
+  bool pos;
+  if constexpr (MK > 0)
+    pos = edge_tiles<MK, NT>(s_par, s_chd, mp, n_par, K, fscale, sp.beta, sp.center, s_lq, s_idr,
+                             prank, edge_rows + base, out);
+  else
+    pos = edge_passes<KQ>(s_par, s_chd, mp, n_par, K, m, fscale, sp.beta, sp.center, s_lq, s_idr,
+                          prank, edge_rows + base, out);
   if (edge_out && l == 0)
     for (int i = K + lane; i < K * K; i += kEdgeThreads) edge_out[base + i] = 0.f;
   const bool any_pos = __ballot(pos) != 0ull;
@@ -396,46 +221,38 @@ hipError_t launch_edge_scores(graft_ctx *ctx, const RoundScratch &ws, const graf
   const int batch = in->batch;
   const int32_t *root_token = in->root_token;
   float *edge_out = out->edge_scores;
-  SabaArgs sa;
-  sa.row_stats = ws.row_stats;
-  sa.hist = in->hist;
-  sa.hist_ring = ctx->hist_ring;
-  sa.prefix_len = in->prefix_len;
-  sa.fixed_budget = in->fixed_budget;
-  sa.adj_cos = in->hidden ? ws.adj_cos : nullptr;
-  sa.window = d.hist_window;
-  sa.budget = out->budget;
-  sa.saba_state = out->saba_state;
+  const SabaArgs sa = saba_args(ctx, ws, in, out);
   const int K = d.top_k, m = ctx->scorer.score_dim;
   const size_t mp = ((m + 3) & ~3) + 4;
   const size_t lds = sizeof(float) * (2 * static_cast<size_t>(K) * mp + K + m) +
                      sizeof(int32_t) * 6 * K;
   const FastDiv mdiv4 = make_fastdiv(static_cast<uint32_t>(m >= 4 ? m / 4 : 1));
   const dim3 grid(batch * d.num_pos), block(kEdgeThreads);
-#define GRAFT_EDGE_KQ(SEG, KQ)                                                                 \
-  hipLaunchKernelGGL((edge_kernel<SEG, KQ>), grid, block, lds, stream, d.num_pos, K, m,      \
+#define GRAFT_EDGE(MK, NT, KQ)                                                                 \
+  hipLaunchKernelGGL((edge_kernel<MK, NT, KQ>), grid, block, lds, stream, d.num_pos, K, m,   \
                      static_cast<int64_t>(d.vocab), mdiv4, ws.topk_ids, ws.topk_logq,       \
                      root_token, ctx->proj_parent, ctx->proj_child, ctx->depth_emb,           \
                      ctx->scorer, ws.edge_rows, ws.cand_by_rank,                            \
                      ws.positive, edge_out, ctx->error_flag, sa, ctx->saba)
-  // groups of four per score row (the scalar path, m % 4 != 0, takes 2)
-  const int m4 = (m & 3) == 0 ? m / 4 : 0;
-#define GRAFT_EDGE(SEG)                                                                        \
+#define GRAFT_EDGE_TILES(MK)                                                                   \
   do {                                                                                         \
-    if (m4 <= 2) GRAFT_EDGE_KQ(SEG, 2);                                                        \
-    else if (m4 <= 4) GRAFT_EDGE_KQ(SEG, 4);                                                   \
-    else if (m4 <= 8) GRAFT_EDGE_KQ(SEG, 8);                                                   \
-    else GRAFT_EDGE_KQ(SEG, 16);                                                               \
+    if (K <= 16) GRAFT_EDGE(MK, 1, 0);                                                         \
+    else if (K <= 32) GRAFT_EDGE(MK, 2, 0);                                                    \
+    else GRAFT_EDGE(MK, 4, 0);                                                                 \
   } while (0)
-  if (K <= 1) GRAFT_EDGE(1);
-  else if (K <= 2) GRAFT_EDGE(2);
-  else if (K <= 4) GRAFT_EDGE(4);
-  else if (K <= 8) GRAFT_EDGE(8);
-  else if (K <= 16) GRAFT_EDGE(16);
-  else if (K <= 32) GRAFT_EDGE(32);
-  else GRAFT_EDGE(64);
+  // matrix-core tiles when m is a multiple of 16, else VALU passes with
+  // ceil(m / 4) groups of four per row
+  const int mk = (m + 3) / 4;
+  if (m == 16) GRAFT_EDGE_TILES(4);
+  else if (m == 32) GRAFT_EDGE_TILES(8);
+  else if (m == 48) GRAFT_EDGE_TILES(12);
+  else if (m == 64) GRAFT_EDGE_TILES(16);
+  else if (mk <= 2) GRAFT_EDGE(0, 1, 2);
+  else if (mk <= 4) GRAFT_EDGE(0, 1, 4);
+  else if (mk <= 8) GRAFT_EDGE(0, 1, 8);
+  else GRAFT_EDGE(0, 1, 16);
+#undef GRAFT_EDGE_TILES
 #undef GRAFT_EDGE
-#undef GRAFT_EDGE_KQ
   return hipGetLastError();
 }
 

@@ -30,7 +30,18 @@
 // Emission: canonical numbering (depth ascending, token path ascending), token
 //   ids, parent indices, position ids base_pos + depth, path scores, and the
 //   ancestor-or-self bitset rows.
+//
+// Fused edge scores: when a sequence's edge rows fit the LDS stage, the
+//   workgroup computes them itself (eqs. tdes-bitower, tdes-center,
+//   tdes-score, the edge stage's arithmetic in the same order, so the rows
+//   are the same bits) and one of its waves computes the SABA budget; the round
+//   then has no separate edge kernel, whose launch and round trips through
+//   device memory cost more than the work.
+#include <cstddef>
+
+#include "edge_mfma.h"
 #include "graft_internal.h"
+#include "saba_device.h"
 
 namespace graft {
 namespace {
@@ -41,6 +52,24 @@ constexpr int kPoolCap = 4096;
 constexpr int kPerThread = kPoolCap / kSelThreads;
 constexpr int kBins = 2048;
 constexpr int kStageRows = 4096;   // edge-row floats staged in LDS (all of a sequence's, or its first depths')
+
+// Inputs of the fused edge scores (fused != 0), as the edge stage takes them.
+struct EdgeIn {
+  int fused;
+  int m;                        // score dim, a multiple of 4
+  int64_t V;
+  uint64_t mdiv4;               // ceil(2^32 / (m / 4)): t / (m / 4) as a multiply-shift
+  uint64_t kdiv;                // ceil(2^32 / K)
+  const int32_t *topk_ids;      // [B, L, K] candidates, rank order
+  const float *topk_logq;       // [B, L, K]
+  const int32_t *root_token;    // [B]
+  const float *P, *Q;           // [V, m] parent and child projections
+  const float *depth_emb;       // [L, m] or nullptr
+  ScorerParams sp;
+  float *edge_out;              // [B, L, K, K] exported table (rank order) or nullptr
+  SabaArgs sa;
+  SabaParams saba;
+};
 
 struct SelectArgs {
   int L, K, n_max, words;
@@ -53,6 +82,7 @@ struct SelectArgs {
   uint64_t *mask;
   double *node_scores;
   uint32_t *error_flag;
+  EdgeIn e;
 };
 
 // Pool entry info: parent + 1 (13 bits) | depth - 1 (6) | rank of the token id
@@ -92,6 +122,7 @@ struct SelMem {
   int32_t doff[kMaxL];   // first canonical index of each depth
   int32_t wsum[kSelWaves];
   int32_t first1[kMaxK + 1];   // first child index of each depth-1 entry (first expansion)
+  int32_t epos[kSelWaves];     // fused edge scores: some score of the wave's depths is > 0
   double theta;
   unsigned long long thkey;   // ordered key of theta when a whole bin is kept
   unsigned long long lomin;   // ordered key of the smallest score appended
@@ -1165,14 +1196,155 @@ __device__ void canon_by_depth(SelMem &s, int K, int n) {
   }
 }
 
-__global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
-  __shared__ SelMem s;
-  const int b = blockIdx.x;
+// The fused path's scratch, in the pool arrays (p_score .. run), which
+// selection first uses after the edge phase: the child rows and the parent
+// rows of every depth (L*K rows each of m floats padded to m + 4: 16-byte
+// aligned rows that start on different banks), then the candidates' token
+// ids, log q and ranks by id (L*K each).
+constexpr int kFusedScratchFloats = 24576;   // 96 KiB
+static_assert(offsetof(SelMem, p_score) == 0 &&
+                  kFusedScratchFloats * sizeof(float) <= offsetof(SelMem, u),
+              "the fused scratch lies within the pool arrays");
+constexpr int kGatherThreads = kSelThreads - kWave;   // waves 0-6 gather, wave 7 budgets
+constexpr int kGatherTasks = 10;   // projection loads (16 bytes) in flight per thread
+
+// n / d for n < 2^26 and d <= 64 with mul = ceil(2^32 / d) (exact there:
+// the error term n e / (d 2^32), e < d, stays below 1 / d).
+__device__ __forceinline__ int fast_div(int n, uint64_t mul) {
+  return static_cast<int>((static_cast<uint64_t>(n) * mul) >> 32);
+}
+
+// Fused edge scores of sequence b (eqs. tdes-bitower, tdes-center,
+// tdes-score), in three phases over the whole workgroup: the candidates'
+// token ids and log q; their ranks by id within each depth (selection's row
+// and column order) and every projection row the depth needs (the child
+// rows g_c + u_d of the K candidates, the parent rows g_p + u_d of the
+// previous depth's candidates, or of the root at depth 1), all loads of a
+// batch issued before any store; then wave w takes depths w, w + 8, ... and
+// forms the scores with the edge stage's matrix-core tiles (edge_tiles<MK,
+// NT>, score dim m = 4 MK of 16 or 32), writing them straight into the LDS
+// rows.  The last wave computes the budget while the others gather.  Leaves
+// s.rows, s.cand, s.epos, s.sc[kBudget] and s.sc[kMixed];
+// the caller sets up the selector after a barrier (the scratch overlaps the
+// pool).
+template <int MK, int NT>
+__device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int b) {
+  const EdgeIn &e = a.e;
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int L = a.L, K = a.K, LK = L * K, m = e.m, m4 = m >> 2, mp4 = m4 + 1;
+  const int64_t V = e.V;
+  float4 *chd = reinterpret_cast<float4 *>(s.p_score);   // rows (l, c), then parent rows (l, p)
+  float4 *par = chd + LK * mp4;
+  int32_t *tokr = reinterpret_cast<int32_t *>(par + LK * mp4);
+  float *lqr = reinterpret_cast<float *>(tokr + LK);
+  int32_t *rnk = reinterpret_cast<int32_t *>(lqr + LK);
+  const bool saba_wave = wave == kSelWaves - 1;
+  SabaIn saba_in{};
+  if (saba_wave) saba_in = saba_load(e.sa, e.saba, b, L);
+  int32_t root = e.root_token[b];
+  if (root < 0 || root >= V) {
+    if (tid == 0) atomicOr(a.error_flag, 1u);
+    root = 0;
+  }
+  const int64_t cb = static_cast<int64_t>(b) * LK;
+  for (int i = tid; i < LK; i += kSelThreads) {
+    tokr[i] = e.topk_ids[cb + i];
+    lqr[i] = e.topk_logq[cb + i];
+  }
+  __syncthreads();
+  // ranks: the depth's K <= 16 NT tokens read as int4 groups, all loads
+  // issued before the comparisons (groups past K reread the first and are
+  // masked)
+  for (int i = tid; i < LK; i += kSelThreads) {
+    const int base = fast_div(i, e.kdiv) * K;
+    const int32_t t = tokr[i];
+    int4 tv[4 * NT];
+    if ((K & 3) == 0) {
+#pragma unroll
+      for (int q = 0; q < 4 * NT; ++q)
+        tv[q] = reinterpret_cast<const int4 *>(tokr + base)[4 * q < K ? q : 0];
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4 * NT; ++q) {
+        const int c = 4 * q;
+        tv[q] = make_int4(tokr[base + (c < K ? c : 0)], tokr[base + (c + 1 < K ? c + 1 : 0)],
+                          tokr[base + (c + 2 < K ? c + 2 : 0)], tokr[base + (c + 3 < K ? c + 3 : 0)]);
+      }
+    }
+    int r = 0;
+#pragma unroll
+    for (int q = 0; q < 4 * NT; ++q) {
+      const int c = 4 * q;
+      r += (c < K && tv[q].x < t) + (c + 1 < K && tv[q].y < t) + (c + 2 < K && tv[q].z < t) +
+           (c + 3 < K && tv[q].w < t);
+    }
+    rnk[i] = r;
+    s.cand[base + r] = t;
+  }
+  // the projection rows: 2 L K rows of m4 groups of four, gathered by waves
+  // 0-6 while wave 7 computes the budget; ids outside [0, V) (only with
+  // non-finite logits) are clamped for the gathers
+  const float4 *P4 = reinterpret_cast<const float4 *>(e.P);
+  const float4 *Q4 = reinterpret_cast<const float4 *>(e.Q);
+  const float4 *U4 = e.sp.has_depth_emb ? reinterpret_cast<const float4 *>(e.depth_emb) : nullptr;
+  const int n_tasks = 2 * LK * m4;
+  if (saba_wave) {
+    const int budget = saba_budget(e.sa, e.saba, b, L, saba_in);
+    if (lane == 0) s.sc[kBudget] = budget;
+  }
+  for (int j0 = 0; !saba_wave && j0 < n_tasks; j0 += kGatherTasks * kGatherThreads) {
+    float4 v[kGatherTasks], u[kGatherTasks];
+    int32_t dst[kGatherTasks];
+#pragma unroll
+    for (int k = 0; k < kGatherTasks; ++k) {
+      int j = j0 + k * kGatherThreads + tid;
+      j = j < n_tasks ? j : n_tasks - 1;
+      const int row = fast_div(j, e.mdiv4);
+      const int j4 = j - row * m4;
+      const bool child = row < LK;
+      const int rr = child ? row : row - LK;
+      const int l = fast_div(rr, e.kdiv);
+      int32_t tok = child ? tokr[rr] : (l == 0 ? root : tokr[rr - K]);
+      tok = (tok < 0 || tok >= V) ? 0 : tok;
+      v[k] = (child ? Q4 : P4)[static_cast<int64_t>(tok) * m4 + j4];
+      u[k] = U4 ? U4[l * m4 + j4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      dst[k] = row * mp4 + j4;
+    }
+#pragma unroll
+    for (int k = 0; k < kGatherTasks; ++k)
+      if (j0 + k * kGatherThreads + tid < n_tasks)
+        chd[dst[k]] = make_float4(v[k].x + u[k].x, v[k].y + u[k].y, v[k].z + u[k].z,
+                                  v[k].w + u[k].w);
+  }
+  __syncthreads();
+
+  const float fscale = e.sp.scale / sqrtf(static_cast<float>(m));
+  const int ld = 4 * mp4;
+  bool pos = false;
+  for (int l = wave; l < L; l += kSelWaves) {
+    const int64_t base = (static_cast<int64_t>(b) * L + l) * K * K;
+    pos |= edge_tiles<MK, NT>(reinterpret_cast<const float *>(par + l * K * mp4),
+                              reinterpret_cast<const float *>(chd + l * K * mp4), ld,
+                              l == 0 ? 1 : K, K, fscale, e.sp.beta, e.sp.center, lqr + l * K,
+                              rnk + l * K, l == 0 ? nullptr : rnk + (l - 1) * K,
+                              s.rows + l * K * K, e.edge_out ? e.edge_out + base : nullptr);
+    if (e.edge_out && l == 0)
+      for (int i2 = K + lane; i2 < K * K; i2 += kWave) e.edge_out[base + i2] = 0.f;
+  }
+  const bool any_pos = __ballot(pos) != 0ull;
+  if (lane == 0) s.epos[wave] = any_pos ? 1 : 0;
+  if (tid == 0) s.sc[kMixed] = 0;
+}
+
+// The inputs the edge stage left in device memory for sequence b: wave 0
+// reads the budget and the sign flags and sets up the parallel selector from
+// the depth-1 row; waves 1.. stage the edge rows (16-byte loads, all issued
+// before the stores): all of them when they fit, else those of the first
+// depths (n_stage floats, as many whole depths as the stage holds).
+__device__ __forceinline__ void load_edge_stage(SelMem &s, const SelectArgs &a, int b,
+                                                const float *ss, int n_stage) {
   const int tid = threadIdx.x;
   const int L = a.L, K = a.K;
-  const float *ss = a.edge_rows + static_cast<int64_t>(b) * L * K * K;
-
-  // wave 0: the budget (computed by the edge stage) and the sign flags
   int budget0 = 0;
   bool pos0 = false;
   float r0 = 0.f;   // the depth-1 row, one score per lane
@@ -1184,11 +1356,6 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   // each depth's candidate tokens in token-id order (written by the edge stage)
   for (int i = tid; i < L * K; i += kSelThreads)
     s.cand[i] = a.cand_by_rank[static_cast<int64_t>(b) * L * K + i];
-  // waves 1.. stage the edge rows (16-byte loads, all issued before the
-  // stores) while wave 0 computes the budget: all of them when they fit, else
-  // those of the first depths (as many whole depths as the stage holds)
-  const int n_stage = (L * K * K <= kStageRows ? L : kStageRows / (K * K)) * K * K;
-  const bool staged = n_stage == L * K * K;
   constexpr int kStageThreads = kSelThreads - kWave;
   if (tid >= kWave && ((L * K * K) % 4 != 0 || n_stage % 4 != 0)) {
     for (int i = tid - kWave; i < n_stage; i += kStageThreads) s.rows[i] = ss[i];
@@ -1208,8 +1375,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
     for (int k = 0; k < kF4; ++k)
       if (t + k * kStageThreads < nf4) reinterpret_cast<float4 *>(s.rows)[t + k * kStageThreads] = vf[k];
   }
-
-  // ---------------- budget and sign flags ----------------
+  // wave 0: the budget, the sign flags and the selector's starting state
   if (tid < kWave) {
     select_setup(s, K, r0);
     const bool mono = __ballot(pos0) == 0ull;
@@ -1219,12 +1385,52 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
       s.sc[kMixed] = 0;
     }
   }
+}
+
+// FUSED: the edge scores and the budget are computed here (a.e), else read
+// from the edge stage; two instantiations, so that the unfused kernel carries
+// none of the fused code.
+template <bool FUSED>
+__global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
+  __shared__ SelMem s;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int L = a.L, K = a.K;
+  const float *ss = a.edge_rows + static_cast<int64_t>(b) * L * K * K;
+
+  constexpr bool fused = FUSED;
+  const int n_stage = (L * K * K <= kStageRows ? L : kStageRows / (K * K)) * K * K;
+  const bool staged = fused || n_stage == L * K * K;   // the fused path stages every row
+  if constexpr (fused) {
+    // the edge stage's tile shapes: m = 4 MK in {16, 32}, NT column tiles of 16
+    if (a.e.m == 16) {
+      if (K <= 16) fused_edges<4, 1>(s, a, b);
+      else if (K <= 32) fused_edges<4, 2>(s, a, b);
+      else fused_edges<4, 4>(s, a, b);
+    } else {
+      if (K <= 16) fused_edges<8, 1>(s, a, b);
+      else if (K <= 32) fused_edges<8, 2>(s, a, b);
+      else fused_edges<8, 4>(s, a, b);
+    }
+    __syncthreads();   // the scratch overlaps the pool the setup writes
+    if (tid < kWave) select_setup(s, K, tid < K ? s.rows[tid] : 0.f);
+  } else {
+    load_edge_stage(s, a, b, ss, n_stage);
+  }
   __syncthreads();
 
   // ---------------- selection ----------------
   int n_target = s.sc[kBudget] < a.n_max ? s.sc[kBudget] : a.n_max;
   if (n_target < 0) n_target = 0;
-  const bool mono = s.sc[kMono] != 0;
+  bool mono;
+  if constexpr (fused) {
+    int any = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) any |= s.epos[w];
+    mono = any == 0;
+  } else {
+    mono = s.sc[kMono] != 0;
+  }
   if (mono) {
     if (n_target > 0) {
       const int n_pool = staged ? select_parallel_k(s, a, LdsRows{s.rows}, n_target)
@@ -1323,6 +1529,13 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
 
 }  // namespace
 
+bool edges_fused(const graft_ctx *ctx) {
+  const graft_dims &d = ctx->dims;
+  const int L = d.num_pos, K = d.top_k, m = ctx->scorer.score_dim;
+  return ctx->fuse_edges && (m == 16 || m == 32) && L * K * K <= kStageRows &&
+         2 * L * K * (m + 4) + 3 * L * K <= kFusedScratchFloats;
+}
+
 hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
                          const graft_tree_out *out, hipStream_t stream) {
   const graft_dims &d = ctx->dims;
@@ -1343,7 +1556,30 @@ hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_rou
   a.mask = out->mask;
   a.node_scores = out->node_scores;
   a.error_flag = ctx->error_flag;
-  hipLaunchKernelGGL(select_kernel, dim3(in->batch), dim3(kSelThreads), 0, stream, a);
+  EdgeIn &e = a.e;
+  e = EdgeIn{};
+  e.fused = edges_fused(ctx) ? 1 : 0;
+  if (e.fused) {
+    const int m = ctx->scorer.score_dim, m4 = m / 4;
+    e.m = m;
+    e.V = d.vocab;
+    e.mdiv4 = ((1ull << 32) + static_cast<uint64_t>(m4) - 1) / static_cast<uint64_t>(m4);
+    e.kdiv = ((1ull << 32) + static_cast<uint64_t>(d.top_k) - 1) / static_cast<uint64_t>(d.top_k);
+    e.topk_ids = ws.topk_ids;
+    e.topk_logq = ws.topk_logq;
+    e.root_token = in->root_token;
+    e.P = ctx->proj_parent;
+    e.Q = ctx->proj_child;
+    e.depth_emb = ctx->depth_emb;
+    e.sp = ctx->scorer;
+    e.edge_out = out->edge_scores;
+    e.sa = saba_args(ctx, ws, in, out);
+    e.saba = ctx->saba;
+  }
+  if (e.fused)
+    hipLaunchKernelGGL(select_kernel<true>, dim3(in->batch), dim3(kSelThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(select_kernel<false>, dim3(in->batch), dim3(kSelThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -445,9 +445,10 @@ EDGE_SHAPES = [
     # K, score dim m, embedding dim
     (1, 8, 16),       # K = 1: one lane per parent run, 64 parents a pass
     (5, 30, 32),      # m % 4 != 0: the element-wise gathers instead of 16-byte ones
-    (13, 20, 32),     # K = 13 in runs of 16 lanes (3 idle lanes per parent), 4 parents a pass
-    (33, 64, 64),     # K = 33 in one 64-lane run per parent (31 idle lanes), m = 64
-    (64, 64, 64),     # the largest K and m: every lane a child, one parent a pass
+    (13, 20, 32),     # m = 20 (VALU passes): K = 13 in runs of 16 lanes, 4 parents a pass
+    (33, 64, 64),     # K = 33, m = 64: three column tiles of the matrix-core path, one partial
+    (20, 48, 32),     # m = 48: twelve k-slots a lane, two column tiles
+    (64, 64, 64),     # the largest K and m: four parent tiles by four column tiles
 ]
 
 
@@ -463,6 +464,53 @@ def test_edge_score_shapes(K, m, E, mode):
     g = WL.gpu_round(ctx, w, inp, torch)
     end_to_end_check(w, g, inp, results)
     staged_check(w, g, sc, sp, inp, range(w.batch))
+    assert ctx.device_status() == 0
+    ctx.close()
+
+
+# Sizes at which the selection kernel computes the edge scores and the budget
+# itself (graft_set_fusion): workload id, overrides, scorer mode, hidden dim
+FUSION_CASES = [
+    (0, {}, "literal", 0),                  # L = 8, K = 4: one depth a wave, fixed budgets
+    (2, {}, "paper", 0),                    # K = 8, m = 16, SABA, centered scores
+    (3, {"batch": 16}, "literal", 0),       # K = 16, m = 32: two depths a wave
+    (3, {"batch": 8}, "paper", 64),         # SABA on the hidden-state degeneration signal
+    (0, dict(batch=3, L=5, V=3000, K=13, n_max=128, fixed_budget=100, emb_dim=32, rank=16),
+     "paper", 0),                           # K = 13: a partial 16 x 16 tile, m = 16
+    (0, dict(batch=2, L=4, V=3000, K=24, n_max=256, fixed_budget=200, emb_dim=32, rank=16),
+     "paper", 0),                           # K = 24: two column tiles, the second partial
+    (0, dict(batch=2, L=1, V=3000, K=64, n_max=64, fixed_budget=64, emb_dim=32, rank=32),
+     "literal", 0),                         # K = 64: four column tiles, one depth
+    (0, dict(batch=3, L=12, V=3000, K=1, n_max=16, fixed_budget=12, emb_dim=16, rank=16),
+     "literal", 0),                         # K = 1, L = 12: waves 0-3 take two depths
+]
+
+
+@pytest.mark.parametrize("case", range(len(FUSION_CASES) + 1))
+def test_fused_edges_match_edge_stage(case):
+    """The fused path (edge scores and budget inside the selection kernel)
+    and the separate edge stage give the same bits for every output; the
+    last case has positive edge scores, so both run the serial selector."""
+    if case < len(FUSION_CASES):
+        wid, kw, mode, hd = FUSION_CASES[case]
+        w = S.workload(wid, **kw)
+        inp, sc, sp, _ = WL.audited_round(w, 0, mode, seqs=[], hidden_dim=hd or None)
+    else:
+        w = S.workload(0, batch=2, V=3000, L=5, K=3, n_max=64, fixed_budget=40)
+        inp, sc, sp, _ = WL.audited_round(w, 0, "paper", seqs=[])
+        sc["beta"] = 400.0
+        sp = None
+    _say("fusion case", case, w)
+    ctx = WL.gpu_context(w, sc, sp, torch)
+    assert ctx.set_fusion(True)
+    fused = WL.gpu_round(ctx, w, inp, torch)
+    assert not ctx.set_fusion(False)
+    staged = WL.gpu_round(ctx, w, inp, torch)
+    if case == len(FUSION_CASES):
+        assert (fused["edge_scores"] > 0).any()
+    for k, v in fused.items():
+        if not k.startswith("_"):
+            assert np.array_equal(v, staged[k]), k
     assert ctx.device_status() == 0
     ctx.close()
 
