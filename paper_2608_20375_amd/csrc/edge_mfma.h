@@ -30,93 +30,125 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
-// Matrix-core tiles.  Lane (i = lane % 16, g = lane / 16) feeds parent row
-// 16 tp + i and child row 16 tc + i at k = g * MK + t (t < MK, m = 4 MK: two or
-// more 16-byte loads per row) and receives f of parents 16 tp + 4 g + r
-// (r < 4) with child 16 tc + i.  NT >= ceil(K / 16) column tiles (those past
-// K hold zeros); a parent's mean sums each column tile's row (row16_sum),
-// combines the tiles as (t0 + t1) + (t2 + t3) and scales by fl(1 / K).
-template <int MK, int NT>
-__device__ __forceinline__ bool edge_tiles(const float *par, const float *chd, int ld, int n_par,
-                                           int K, float fscale, float beta, int center,
-                                           const float *lq, const int32_t *col,
-                                           const int32_t *prank, float *rows, float *out) {
+// One (sequence, depth) for edge_tiles: its parent and child rows, number of
+// parents, log q and column of each child, row of each parent (prank ==
+// nullptr: 0), and the outputs.
+struct EdgeJob {
+  const float *par, *chd;
+  int n_par;
+  const float *lq;
+  const int32_t *col, *prank;
+  float *rows, *out;
+};
+
+// Matrix-core tiles for ND jobs of the same K, interleaved (independent
+// accumulator chains; each job's arithmetic is the same as alone).  Lane
+// (i = lane % 16, g = lane / 16) feeds parent row 16 tp + i and child row
+// 16 tc + i at k = g * MK + t (t < MK, m = 4 MK: two or more 16-byte loads per
+// row) and receives f of parents 16 tp + 4 g + r (r < 4) with child 16 tc + i.
+// NT >= ceil(K / 16) column tiles (those past K hold zeros); a parent's mean
+// sums each column tile's row (row16_sum), combines the tiles as
+// (t0 + t1) + (t2 + t3) and scales by fl(1 / K).
+template <int MK, int NT, int ND>
+__device__ __forceinline__ bool edge_tiles(const EdgeJob (&job)[ND], int ld, int K, float fscale,
+                                           float beta, int center) {
   static_assert(MK % 4 == 0 && (NT == 1 || NT == 2 || NT == 4), "tile shape");
   constexpr int V4 = MK / 4;
   const int lane = lane_id(), i = lane & 15, g = lane >> 4;
-  const int n_tp = (n_par + 15) >> 4;
   // the children's operands of every column tile, kept across parent tiles
-  float4 bv[NT][V4];
-  float lqv[NT];
-  int32_t colv[NT];
+  float4 bv[ND][NT][V4];
+  float lqv[ND][NT];
+  int32_t colv[ND][NT];
+  int n_tp = 0;
 #pragma unroll
-  for (int tc = 0; tc < NT; ++tc) {
-    const int c = tc * 16 + i;
-    const int cc = c < K ? c : 0;
-    const float4 *src = reinterpret_cast<const float4 *>(chd + cc * ld + g * MK);
+  for (int d = 0; d < ND; ++d) {
+    const int nt = (job[d].n_par + 15) >> 4;
+    n_tp = nt > n_tp ? nt : n_tp;
 #pragma unroll
-    for (int t = 0; t < V4; ++t) bv[tc][t] = src[t];
-    lqv[tc] = lq[cc];
-    colv[tc] = col[cc];
+    for (int tc = 0; tc < NT; ++tc) {
+      const int c = tc * 16 + i;
+      const int cc = c < K ? c : 0;
+      const float4 *src = reinterpret_cast<const float4 *>(job[d].chd + cc * ld + g * MK);
+#pragma unroll
+      for (int t = 0; t < V4; ++t) bv[d][tc][t] = src[t];
+      lqv[d][tc] = job[d].lq[cc];
+      colv[d][tc] = job[d].col[cc];
+    }
   }
 #pragma unroll
-  for (int tc = 0; tc < NT; ++tc)
-    if (tc * 16 + i >= K)
+  for (int d = 0; d < ND; ++d)
 #pragma unroll
-      for (int t = 0; t < V4; ++t) bv[tc][t] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int tc = 0; tc < NT; ++tc)
+      if (tc * 16 + i >= K)
+#pragma unroll
+        for (int t = 0; t < V4; ++t) bv[d][tc][t] = make_float4(0.f, 0.f, 0.f, 0.f);
   const float inv_k = 1.0f / static_cast<float>(K);
   bool pos = false;
   for (int tp = 0; tp < n_tp; ++tp) {
     const int pa = tp * 16 + i;
-    const float4 *src = reinterpret_cast<const float4 *>(par + (pa < n_par ? pa : 0) * ld + g * MK);
-    float4 av[V4];
+    float4 av[ND][V4];
+    int32_t prow[ND][4];
 #pragma unroll
-    for (int t = 0; t < V4; ++t) av[t] = src[t];
-    int32_t prow[4];
+    for (int d = 0; d < ND; ++d) {
+      const int np = job[d].n_par;
+      const float4 *src =
+          reinterpret_cast<const float4 *>(job[d].par + (pa < np ? pa : 0) * ld + g * MK);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int p = tp * 16 + 4 * g + r;
-      prow[r] = prank ? prank[p < n_par ? p : 0] : 0;
-    }
-    if (pa >= n_par)
+      for (int t = 0; t < V4; ++t) av[d][t] = src[t];
 #pragma unroll
-      for (int t = 0; t < V4; ++t) av[t] = make_float4(0.f, 0.f, 0.f, 0.f);
-    mfma_f32x4 acc[NT];
-#pragma unroll
-    for (int tc = 0; tc < NT; ++tc) {
-      acc[tc] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int t = 0; t < V4; ++t) {
-        acc[tc] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].x, bv[tc][t].x, acc[tc], 0, 0, 0);
-        acc[tc] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].y, bv[tc][t].y, acc[tc], 0, 0, 0);
-        acc[tc] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].z, bv[tc][t].z, acc[tc], 0, 0, 0);
-        acc[tc] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t].w, bv[tc][t].w, acc[tc], 0, 0, 0);
+      for (int r = 0; r < 4; ++r) {
+        const int p = tp * 16 + 4 * g + r;
+        prow[d][r] = job[d].prank ? job[d].prank[p < np ? p : 0] : 0;
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int p = tp * 16 + 4 * g + r;
-      const bool pok = p < n_par;
-      float f[NT];
+    for (int d = 0; d < ND; ++d)
+      if (pa >= job[d].n_par)
 #pragma unroll
-      for (int tc = 0; tc < NT; ++tc) f[tc] = fscale * acc[tc][r];
-      float mean = 0.f;
-      if (center) {
-        float rs[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < V4; ++t) av[d][t] = make_float4(0.f, 0.f, 0.f, 0.f);
+    mfma_f32x4 acc[ND][NT];
 #pragma unroll
-        for (int tc = 0; tc < NT; ++tc) rs[tc] = row16_sum(tc * 16 + i < K ? f[tc] : 0.f);
-        mean = ((rs[0] + rs[1]) + (rs[2] + rs[3])) * inv_k;
-      }
+    for (int tc = 0; tc < NT; ++tc)
 #pragma unroll
-      for (int tc = 0; tc < NT; ++tc) {
-        const int c = tc * 16 + i;
-        const bool valid = pok && c < K;
-        const float S = (lqv[tc] + beta * (f[tc] - mean)) + 0.0f;   // -0 -> +0
-        if (valid) {
-          rows[prow[r] * K + colv[tc]] = S;
-          if (out) out[p * K + c] = S;
+      for (int d = 0; d < ND; ++d) acc[d][tc] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < V4; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int tc = 0; tc < NT; ++tc)
+#pragma unroll
+          for (int d = 0; d < ND; ++d)
+            acc[d][tc] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[d][t][q], bv[d][tc][t][q],
+                                                               acc[d][tc], 0, 0, 0);
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      if (tp * 16 >= job[d].n_par) continue;   // this job has no parent tile tp
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int p = tp * 16 + 4 * g + r;
+        const bool pok = p < job[d].n_par;
+        float f[NT];
+#pragma unroll
+        for (int tc = 0; tc < NT; ++tc) f[tc] = fscale * acc[d][tc][r];
+        float mean = 0.f;
+        if (center) {
+          float rs[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int tc = 0; tc < NT; ++tc) rs[tc] = row16_sum(tc * 16 + i < K ? f[tc] : 0.f);
+          mean = ((rs[0] + rs[1]) + (rs[2] + rs[3])) * inv_k;
         }
-        pos |= valid && S > 0.f;
+#pragma unroll
+        for (int tc = 0; tc < NT; ++tc) {
+          const int c = tc * 16 + i;
+          const bool valid = pok && c < K;
+          const float S = (lqv[d][tc] + beta * (f[tc] - mean)) + 0.0f;   // -0 -> +0
+          if (valid) {
+            job[d].rows[prow[d][r] * K + colv[d][tc]] = S;
+            if (job[d].out) job[d].out[p * K + c] = S;
+          }
+          pos |= valid && S > 0.f;
+        }
       }
     }
   }

@@ -189,10 +189,10 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   const int32_t *prank = l == 0 ? nullptr : s_pidr;
   float *out = edge_out ? edge_out + base : nullptr;
   bool pos;
-  if constexpr (MK > 0)
-    pos = edge_tiles<MK, NT>(s_par, s_chd, mp, n_par, K, fscale, sp.beta, sp.center, s_lq, s_idr,
-                             prank, edge_rows + base, out);
-  else
+  if constexpr (MK > 0) {
+    const EdgeJob job[1] = {{s_par, s_chd, n_par, s_lq, s_idr, prank, edge_rows + base, out}};
+    pos = edge_tiles<MK, NT, 1>(job, mp, K, fscale, sp.beta, sp.center);
+  } else
     pos = edge_passes<KQ>(s_par, s_chd, mp, n_par, K, m, fscale, sp.beta, sp.center, s_lq, s_idr,
                           prank, edge_rows + base, out);
   if (edge_out && l == 0)

@@ -1320,16 +1320,31 @@ __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int 
 
   const float fscale = e.sp.scale / sqrtf(static_cast<float>(m));
   const int ld = 4 * mp4;
-  bool pos = false;
-  for (int l = wave; l < L; l += kSelWaves) {
+  // the job of depth l
+  auto job_of = [&](int l) {
     const int64_t base = (static_cast<int64_t>(b) * L + l) * K * K;
-    pos |= edge_tiles<MK, NT>(reinterpret_cast<const float *>(par + l * K * mp4),
-                              reinterpret_cast<const float *>(chd + l * K * mp4), ld,
-                              l == 0 ? 1 : K, K, fscale, e.sp.beta, e.sp.center, lqr + l * K,
-                              rnk + l * K, l == 0 ? nullptr : rnk + (l - 1) * K,
-                              s.rows + l * K * K, e.edge_out ? e.edge_out + base : nullptr);
-    if (e.edge_out && l == 0)
-      for (int i2 = K + lane; i2 < K * K; i2 += kWave) e.edge_out[base + i2] = 0.f;
+    return EdgeJob{reinterpret_cast<const float *>(par + l * K * mp4),
+                   reinterpret_cast<const float *>(chd + l * K * mp4),
+                   l == 0 ? 1 : K,
+                   lqr + l * K,
+                   rnk + l * K,
+                   l == 0 ? nullptr : rnk + (l - 1) * K,
+                   s.rows + l * K * K,
+                   e.edge_out ? e.edge_out + base : nullptr};
+  };
+  bool pos = false;
+  int l = wave;
+  for (; l + kSelWaves < L; l += 2 * kSelWaves) {   // two depths at a time, interleaved
+    const EdgeJob jobs[2] = {job_of(l), job_of(l + kSelWaves)};
+    pos |= edge_tiles<MK, NT, 2>(jobs, ld, K, fscale, e.sp.beta, e.sp.center);
+  }
+  if (l < L) {
+    const EdgeJob jobs[1] = {job_of(l)};
+    pos |= edge_tiles<MK, NT, 1>(jobs, ld, K, fscale, e.sp.beta, e.sp.center);
+  }
+  if (e.edge_out && wave == 0) {   // depth 1 has one parent row; the others are 0
+    const int64_t base = static_cast<int64_t>(b) * L * K * K;
+    for (int i2 = K + lane; i2 < K * K; i2 += kWave) e.edge_out[base + i2] = 0.f;
   }
   const bool any_pos = __ballot(pos) != 0ull;
   if (lane == 0) s.epos[wave] = any_pos ? 1 : 0;
