@@ -570,8 +570,8 @@ __device__ __forceinline__ void block_merge(uint64_t *buf, const int *cnt, const
 
 template <int CAP>
 __global__ void __launch_bounds__(kThreads, 4)
-logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, int K, int batch,
-                   int L, double *__restrict__ part_stats, uint64_t *__restrict__ part_keys,
+logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, int K,
+                   double *__restrict__ part_stats, uint64_t *__restrict__ part_keys,
                    RowOut out) {
   __shared__ uint64_t s_buf[kWaves][CAP];
   __shared__ double s_stats[kWaves][3];
@@ -579,12 +579,7 @@ logits_pass_kernel(const uint16_t *__restrict__ logits, int64_t V, int splits, i
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = lane_id();
-  // depth-major rows: with a batch that is a multiple of the 8 XCDs (blocks
-  // go to XCDs round-robin), every row of sequence b is processed on the XCD
-  // that the later kernels run sequence b on, so they find its candidates and
-  // statistics in that XCD's L2
-  const int rb = static_cast<int>(blockIdx.x) / splits;
-  const int64_t row = static_cast<int64_t>(rb % batch) * L + rb / batch;
+  const int64_t row = blockIdx.x / splits;
   const int split = blockIdx.x % splits;
 
   const uint16_t *rowp = logits + row * V;
@@ -823,13 +818,13 @@ hipError_t launch_logits_pass(graft_ctx *ctx, const RoundScratch &ws, int batch,
   const int64_t V = d.vocab;
   if (d.top_k <= 32) {
     hipLaunchKernelGGL(logits_pass_kernel<128>, grid, dim3(kThreads), 0, stream, logits, V,
-                       splits, d.top_k, batch, d.num_pos, ws.part_stats, ws.part_keys, o);
+                       splits, d.top_k, ws.part_stats, ws.part_keys, o);
     if (splits > 1)
       hipLaunchKernelGGL(merge_kernel<128>, dim3(rows), dim3(kWave), 0, stream, splits, d.top_k,
                          ws.part_stats, ws.part_keys, o);
   } else {
     hipLaunchKernelGGL(logits_pass_kernel<256>, grid, dim3(kThreads), 0, stream, logits, V,
-                       splits, d.top_k, batch, d.num_pos, ws.part_stats, ws.part_keys, o);
+                       splits, d.top_k, ws.part_stats, ws.part_keys, o);
     if (splits > 1)
       hipLaunchKernelGGL(merge_kernel<256>, dim3(rows), dim3(kWave), 0, stream, splits, d.top_k,
                          ws.part_stats, ws.part_keys, o);
