@@ -1474,17 +1474,20 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   const int64_t ob = static_cast<int64_t>(b) * a.n_max;
   const int32_t base = a.base_pos[b];
   int32_t *cpar = s.u.b.hist;       // canonical parents, for the mask
+  int32_t *gpar = s.u.b.pcnt;       // canonical grandparents
   for (int i = tid; i < n; i += kSelThreads) {
     const uint32_t info = s.p_info[i];
     if (!alive(info)) continue;
     const int c = s.map[i];
     const int p = pi_parent(info);
     const int cp = p < 0 ? -1 : s.map[p];
+    const int pp = p < 0 ? -1 : pi_parent(s.p_info[p]);
     a.tokens[ob + c] = ptoken(s, K, info);
     a.parents[ob + c] = cp;
     a.pos_ids[ob + c] = base + pi_depth(info);
     if (a.node_scores) a.node_scores[ob + c] = s.p_score[i];
     cpar[c] = cp;
+    gpar[c] = pp < 0 ? -1 : s.map[pp];
   }
   for (int c = n_sel + tid; c < a.n_max; c += kSelThreads) {
     a.tokens[ob + c] = -1;
@@ -1497,7 +1500,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
   // ---------------- ancestor mask ----------------
   // Each wave takes 64 rows at a time, one per lane: a single walk up the
   // canonical parents (which precede their children, so the indices
-  // decrease) emits the row's words from the highest down into LDS (rows
+  // decrease), two levels per LDS round trip (parent and grandparent read
+  // together), emits the row's words from the highest down into LDS (rows
   // padded by one word against bank conflicts); the wave then copies the 64
   // rows out with consecutive lanes on consecutive words.  The pool arrays
   // are free by now and hold the staging rows.
@@ -1513,16 +1517,22 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
       int w = words - 1;
       if (r < n_sel) {
         for (; w > (r >> 6); --w) my[w] = 0ull;
-        uint64_t bits = 0;
+        uint64_t bits = 1ull << (r & 63);
         for (int j = r;;) {
-          bits |= 1ull << (j & 63);
-          const int pj = cpar[j];
-          if (pj < 0 || pj >= j) break;
-          for (; (pj >> 6) < w; --w) {
+          const int p1 = cpar[j], p2 = gpar[j];
+          if (p1 < 0 || p1 >= j) break;
+          for (; (p1 >> 6) < w; --w) {
             my[w] = bits;
             bits = 0;
           }
-          j = pj;
+          bits |= 1ull << (p1 & 63);
+          if (p2 < 0 || p2 >= p1) break;
+          for (; (p2 >> 6) < w; --w) {
+            my[w] = bits;
+            bits = 0;
+          }
+          bits |= 1ull << (p2 & 63);
+          j = p2;
         }
         my[w--] = bits;
       }
