@@ -214,7 +214,7 @@ GRAFT_API int graft_build_tree(graft_ctx *ctx, const graft_round_in *in /* host 
  * selection kernel computes a sequence's edge scores and its budget itself
  * whenever the edge rows and the projection rows fit its on-chip memory:
  * num_pos * top_k^2 <= 4096, score_dim 16 or 32, and
- * L K (2 score_dim + 11) <= 24576 with L = num_pos, K = top_k; the round
+ * L K <= 512 and L K (2 score_dim + 10) <= 24576 with L = num_pos, K = top_k; the round
  * then launches no separate edge stage.  With enable == 0
  * the edge stage always runs.  *active (host, may be NULL) receives 1 when
  * the fused path is taken for this context's sizes and installed scorer, else

@@ -1199,8 +1199,8 @@ __device__ void canon_by_depth(SelMem &s, int K, int n) {
 // The fused path's scratch, in the pool arrays (p_score .. run), which
 // selection first uses after the edge phase: the child rows and the parent
 // rows of every depth (L*K rows each of m floats padded to m + 4: 16-byte
-// aligned rows that start on different banks), then the candidates' token
-// ids, log q and ranks by id (L*K each).
+// aligned rows that start on different banks), then the candidates' log q
+// and ranks by id (L*K each).
 constexpr int kFusedScratchFloats = 24576;   // 96 KiB
 static_assert(offsetof(SelMem, p_score) == 0 &&
                   kFusedScratchFloats * sizeof(float) <= offsetof(SelMem, u),
@@ -1215,18 +1215,19 @@ __device__ __forceinline__ int fast_div(int n, uint64_t mul) {
 }
 
 // Fused edge scores of sequence b (eqs. tdes-bitower, tdes-center,
-// tdes-score), in three phases over the whole workgroup: the candidates'
-// token ids and log q; their ranks by id within each depth (selection's row
-// and column order) and every projection row the depth needs (the child
-// rows g_c + u_d of the K candidates, the parent rows g_p + u_d of the
-// previous depth's candidates, or of the root at depth 1), all loads of a
-// batch issued before any store; then wave w takes depths w, w + 8, ... and
-// forms the scores with the edge stage's matrix-core tiles (edge_tiles<MK,
-// NT>, score dim m = 4 MK of 16 or 32), writing them straight into the LDS
-// rows.  The last wave computes the budget while the others gather.  Leaves
-// s.rows, s.cand, s.epos, s.sc[kBudget] and s.sc[kMixed];
-// the caller sets up the selector after a barrier (the scratch overlaps the
-// pool).
+// tdes-score), in two phases over the whole workgroup.  First, with no
+// barrier between the two round trips: each thread's candidate (tid < L K),
+// its log q and its depth's tokens, for its rank by id within the depth
+// (selection's row and column order); and every projection row the depths
+// need (the child rows g_c + u_d of the K candidates, the parent rows g_p + u_d
+// of the previous depth's candidates, or of the root at depth 1), gathered by
+// waves 0-6 from token ids read straight from device memory, all loads of a
+// batch issued before any store, while wave 7 computes the budget.  Then wave
+// w takes depths w, w + 8, ... and forms the scores with the edge stage's
+// matrix-core tiles (edge_tiles<MK, NT>, score dim m = 4 MK of 16 or 32, two
+// depths interleaved), writing them straight into the LDS rows.  Leaves
+// s.rows, s.cand, s.epos, s.sc[kBudget] and s.sc[kMixed]; the caller sets up
+// the selector after a barrier (the scratch overlaps the pool).
 template <int MK, int NT>
 __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int b) {
   const EdgeIn &e = a.e;
@@ -1235,8 +1236,7 @@ __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int 
   const int64_t V = e.V;
   float4 *chd = reinterpret_cast<float4 *>(s.p_score);   // rows (l, c), then parent rows (l, p)
   float4 *par = chd + LK * mp4;
-  int32_t *tokr = reinterpret_cast<int32_t *>(par + LK * mp4);
-  float *lqr = reinterpret_cast<float *>(tokr + LK);
+  float *lqr = reinterpret_cast<float *>(par + LK * mp4);
   int32_t *rnk = reinterpret_cast<int32_t *>(lqr + LK);
   const bool saba_wave = wave == kSelWaves - 1;
   SabaIn saba_in{};
@@ -1246,40 +1246,28 @@ __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int 
     if (tid == 0) atomicOr(a.error_flag, 1u);
     root = 0;
   }
+  // Every load first: this thread's candidate (tid < L K <= 512), its log q
+  // and the K tokens of its depth (for its rank by id), then the gather tasks'
+  // tokens and projection rows, all from device memory, so that no barrier
+  // separates the two round trips.
   const int64_t cb = static_cast<int64_t>(b) * LK;
-  for (int i = tid; i < LK; i += kSelThreads) {
-    tokr[i] = e.topk_ids[cb + i];
-    lqr[i] = e.topk_logq[cb + i];
-  }
-  __syncthreads();
-  // ranks: the depth's K <= 16 NT tokens read as int4 groups, all loads
-  // issued before the comparisons (groups past K reread the first and are
-  // masked)
-  for (int i = tid; i < LK; i += kSelThreads) {
-    const int base = fast_div(i, e.kdiv) * K;
-    const int32_t t = tokr[i];
-    int4 tv[4 * NT];
-    if ((K & 3) == 0) {
+  const int32_t *ids = e.topk_ids + cb;
+  const int ci = tid < LK ? tid : 0;
+  const int cbase = fast_div(ci, e.kdiv) * K;
+  const int32_t ct = ids[ci];
+  const float clq = e.topk_logq[cb + ci];
+  int4 tv[4 * NT];   // groups past K reread the first and are masked
+  if ((K & 3) == 0) {
 #pragma unroll
-      for (int q = 0; q < 4 * NT; ++q)
-        tv[q] = reinterpret_cast<const int4 *>(tokr + base)[4 * q < K ? q : 0];
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4 * NT; ++q) {
-        const int c = 4 * q;
-        tv[q] = make_int4(tokr[base + (c < K ? c : 0)], tokr[base + (c + 1 < K ? c + 1 : 0)],
-                          tokr[base + (c + 2 < K ? c + 2 : 0)], tokr[base + (c + 3 < K ? c + 3 : 0)]);
-      }
-    }
-    int r = 0;
+    for (int q = 0; q < 4 * NT; ++q)
+      tv[q] = reinterpret_cast<const int4 *>(ids + cbase)[4 * q < K ? q : 0];
+  } else {
 #pragma unroll
     for (int q = 0; q < 4 * NT; ++q) {
       const int c = 4 * q;
-      r += (c < K && tv[q].x < t) + (c + 1 < K && tv[q].y < t) + (c + 2 < K && tv[q].z < t) +
-           (c + 3 < K && tv[q].w < t);
+      tv[q] = make_int4(ids[cbase + (c < K ? c : 0)], ids[cbase + (c + 1 < K ? c + 1 : 0)],
+                        ids[cbase + (c + 2 < K ? c + 2 : 0)], ids[cbase + (c + 3 < K ? c + 3 : 0)]);
     }
-    rnk[i] = r;
-    s.cand[base + r] = t;
   }
   // the projection rows: 2 L K rows of m4 groups of four, gathered by waves
   // 0-6 while wave 7 computes the budget; ids outside [0, V) (only with
@@ -1288,33 +1276,50 @@ __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int 
   const float4 *Q4 = reinterpret_cast<const float4 *>(e.Q);
   const float4 *U4 = e.sp.has_depth_emb ? reinterpret_cast<const float4 *>(e.depth_emb) : nullptr;
   const int n_tasks = 2 * LK * m4;
-  if (saba_wave) {
-    const int budget = saba_budget(e.sa, e.saba, b, L, saba_in);
-    if (lane == 0) s.sc[kBudget] = budget;
-  }
   for (int j0 = 0; !saba_wave && j0 < n_tasks; j0 += kGatherTasks * kGatherThreads) {
-    float4 v[kGatherTasks], u[kGatherTasks];
-    int32_t dst[kGatherTasks];
+    int32_t tok[kGatherTasks], dst[kGatherTasks], j4s[kGatherTasks], ls[kGatherTasks];
+    bool chd_row[kGatherTasks];
 #pragma unroll
     for (int k = 0; k < kGatherTasks; ++k) {
       int j = j0 + k * kGatherThreads + tid;
       j = j < n_tasks ? j : n_tasks - 1;
       const int row = fast_div(j, e.mdiv4);
-      const int j4 = j - row * m4;
-      const bool child = row < LK;
-      const int rr = child ? row : row - LK;
-      const int l = fast_div(rr, e.kdiv);
-      int32_t tok = child ? tokr[rr] : (l == 0 ? root : tokr[rr - K]);
-      tok = (tok < 0 || tok >= V) ? 0 : tok;
-      v[k] = (child ? Q4 : P4)[static_cast<int64_t>(tok) * m4 + j4];
-      u[k] = U4 ? U4[l * m4 + j4] : make_float4(0.f, 0.f, 0.f, 0.f);
-      dst[k] = row * mp4 + j4;
+      j4s[k] = j - row * m4;
+      chd_row[k] = row < LK;
+      const int rr = chd_row[k] ? row : row - LK;
+      ls[k] = fast_div(rr, e.kdiv);
+      tok[k] = chd_row[k] ? ids[rr] : (ls[k] == 0 ? root : ids[rr - K]);
+      dst[k] = row * mp4 + j4s[k];
+    }
+    float4 v[kGatherTasks], u[kGatherTasks];
+#pragma unroll
+    for (int k = 0; k < kGatherTasks; ++k) {
+      const int32_t t = (tok[k] < 0 || tok[k] >= V) ? 0 : tok[k];
+      v[k] = (chd_row[k] ? Q4 : P4)[static_cast<int64_t>(t) * m4 + j4s[k]];
+      u[k] = U4 ? U4[ls[k] * m4 + j4s[k]] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int k = 0; k < kGatherTasks; ++k)
       if (j0 + k * kGatherThreads + tid < n_tasks)
         chd[dst[k]] = make_float4(v[k].x + u[k].x, v[k].y + u[k].y, v[k].z + u[k].z,
                                   v[k].w + u[k].w);
+  }
+  // ranks by token id within each depth (selection's row and column order)
+  if (tid < LK) {
+    int r = 0;
+#pragma unroll
+    for (int q = 0; q < 4 * NT; ++q) {
+      const int c = 4 * q;
+      r += (c < K && tv[q].x < ct) + (c + 1 < K && tv[q].y < ct) + (c + 2 < K && tv[q].z < ct) +
+           (c + 3 < K && tv[q].w < ct);
+    }
+    rnk[tid] = r;
+    lqr[tid] = clq;
+    s.cand[cbase + r] = ct;
+  }
+  if (saba_wave) {
+    const int budget = saba_budget(e.sa, e.saba, b, L, saba_in);
+    if (lane == 0) s.sc[kBudget] = budget;
   }
   __syncthreads();
 
@@ -1558,7 +1563,7 @@ bool edges_fused(const graft_ctx *ctx) {
   const graft_dims &d = ctx->dims;
   const int L = d.num_pos, K = d.top_k, m = ctx->scorer.score_dim;
   return ctx->fuse_edges && (m == 16 || m == 32) && L * K * K <= kStageRows &&
-         2 * L * K * (m + 4) + 3 * L * K <= kFusedScratchFloats;
+         L * K <= kSelThreads && 2 * L * K * (m + 4) + 2 * L * K <= kFusedScratchFloats;
 }
 
 hipError_t launch_select(graft_ctx *ctx, const RoundScratch &ws, const graft_round_in *in,
