@@ -626,16 +626,22 @@ __device__ __forceinline__ float wave_min_f32(float v) {
 // smallest depth-1 score, the largest one in sc[kRHi] (float bits), and a
 // cleared histogram.  Harmless when the serial selector runs instead: it
 // rewrites the pool from index 0 and uses the union as its heap.
-__device__ __forceinline__ void select_setup(SelMem &s, int K, float r0) {
+// In two parts for the fused path, whose scratch overlaps the pool until a
+// barrier: select_setup_scalars (the histogram, lomin, the root run, the
+// largest score) and select_setup_pool (the K entries).
+__device__ __forceinline__ void select_setup_pool(SelMem &s, int K, float r0) {
   const int lane = lane_id();
-  int4 *h4 = reinterpret_cast<int4 *>(s.u.b.hist);
-#pragma unroll
-  for (int k = 0; k < kBins / 4 / kWave; ++k) h4[lane + k * kWave] = make_int4(0, 0, 0, 0);
   if (lane < K) {
     s.p_score[lane] = static_cast<double>(r0);
     s.p_info[lane] = pinfo(-1, 1, lane);
     s.run[lane] = 0;
   }
+}
+__device__ __forceinline__ void select_setup_scalars(SelMem &s, int K, float r0) {
+  const int lane = lane_id();
+  int4 *h4 = reinterpret_cast<int4 *>(s.u.b.hist);
+#pragma unroll
+  for (int k = 0; k < kBins / 4 / kWave; ++k) h4[lane + k * kWave] = make_int4(0, 0, 0, 0);
   const float r_hi = wave_max_f32(lane < K ? r0 : -INFINITY);
   const float r_lo = wave_min_f32(lane < K ? r0 : INFINITY);
   if (lane == 0) {
@@ -643,6 +649,10 @@ __device__ __forceinline__ void select_setup(SelMem &s, int K, float r0) {
     s.sc[kRootRun] = K;   // the depth-1 entries: first index 0, K of them
     s.sc[kRHi] = __float_as_int(r_hi);
   }
+}
+__device__ __forceinline__ void select_setup(SelMem &s, int K, float r0) {
+  select_setup_pool(s, K, r0);
+  select_setup_scalars(s, K, r0);
 }
 
 // Parallel exact top-N for sequences whose edge scores are all <= 0.  Every
@@ -1226,8 +1236,10 @@ __device__ __forceinline__ int fast_div(int n, uint64_t mul) {
 // w takes depths w, w + 8, ... and forms the scores with the edge stage's
 // matrix-core tiles (edge_tiles<MK, NT>, score dim m = 4 MK of 16 or 32, two
 // depths interleaved), writing them straight into the LDS rows.  Leaves
-// s.rows, s.cand, s.epos, s.sc[kBudget] and s.sc[kMixed]; the caller sets up
-// the selector after a barrier (the scratch overlaps the pool).
+// s.rows, s.cand, s.epos, s.sc[kBudget], s.sc[kMixed] and the selector's
+// scalars (select_setup_scalars, by wave 0, which scored depth 1); the caller
+// writes the depth-1 pool entries after a barrier (the scratch overlaps the
+// pool).
 template <int MK, int NT>
 __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int b) {
   const EdgeIn &e = a.e;
@@ -1354,6 +1366,14 @@ __device__ __forceinline__ void fused_edges(SelMem &s, const SelectArgs &a, int 
   const bool any_pos = __ballot(pos) != 0ull;
   if (lane == 0) s.epos[wave] = any_pos ? 1 : 0;
   if (tid == 0) s.sc[kMixed] = 0;
+  if (wave == 0) {
+    // wave 0 scored depth 1: the selector's scalars now, its pool entries
+    // after the barrier
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    select_setup_scalars(s, K, lane < K ? s.rows[lane] : 0.f);
+  }
 }
 
 // The inputs the edge stage left in device memory for sequence b: wave 0
@@ -1433,7 +1453,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(SelectArgs a) {
       else fused_edges<8, 4>(s, a, b);
     }
     __syncthreads();   // the scratch overlaps the pool the setup writes
-    if (tid < kWave) select_setup(s, K, tid < K ? s.rows[tid] : 0.f);
+    if (tid < kWave) select_setup_pool(s, K, tid < K ? s.rows[tid] : 0.f);
   } else {
     load_edge_stage(s, a, b, ss, n_stage);
   }
