@@ -55,6 +55,13 @@ def test_create_rejects_bad_dims_before_touching_the_device():
     assert L.graft_create(None, C.byref(h)) == 1
 
 
+def test_set_fusion_rejects_a_null_context():
+    L = G.lib()
+    active = C.c_int32(7)
+    assert L.graft_set_fusion(None, 1, C.byref(active)) == 1
+    assert active.value == 7   # untouched on error
+
+
 PROBE = r"""
 #include <stddef.h>
 #include <stdio.h>
