@@ -483,6 +483,11 @@ FUSION_CASES = [
      "literal", 0),                         # K = 64: four column tiles, one depth
     (0, dict(batch=3, L=12, V=3000, K=1, n_max=16, fixed_budget=12, emb_dim=16, rank=16),
      "literal", 0),                         # K = 1, L = 12: waves 0-3 take two depths
+    (0, dict(batch=2, L=64, V=3000, K=8, n_max=256, fixed_budget=200, emb_dim=32, rank=16),
+     "paper", 0),                           # L K = 512: every thread ranks a candidate, the
+                                            # budget wave included; eight depths a wave
+    (0, dict(batch=2, L=40, V=3000, K=8, n_max=256, fixed_budget=200, emb_dim=32, rank=32),
+     "literal", 0),                         # 5120 projection loads: two gather batches
 ]
 
 
