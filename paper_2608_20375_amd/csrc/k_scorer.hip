@@ -190,8 +190,18 @@ edge_kernel(int L, int K, int m, int64_t V, FastDiv mdiv4, const int32_t *__rest
   float *out = edge_out ? edge_out + base : nullptr;
   bool pos;
   if constexpr (MK > 0) {
-    const EdgeJob job[1] = {{s_par, s_chd, n_par, s_lq, s_idr, prank, edge_rows + base, out}};
-    pos = edge_tiles<MK, NT, 1>(job, mp, K, fscale, sp.beta, sp.center);
+    if (n_par > 16) {
+      // the parents in two halves of whole 16-row tiles, their chains interleaved
+      const int h = ((n_par + 31) / 32) * 16;
+      const EdgeJob job[2] = {
+          {s_par, s_chd, h, s_lq, s_idr, prank, edge_rows + base, out},
+          {s_par + h * mp, s_chd, n_par - h, s_lq, s_idr, prank + h, edge_rows + base,
+           out ? out + h * K : nullptr}};
+      pos = edge_tiles<MK, NT, 2>(job, mp, K, fscale, sp.beta, sp.center);
+    } else {
+      const EdgeJob job[1] = {{s_par, s_chd, n_par, s_lq, s_idr, prank, edge_rows + base, out}};
+      pos = edge_tiles<MK, NT, 1>(job, mp, K, fscale, sp.beta, sp.center);
+    }
   } else
     pos = edge_passes<KQ>(s_par, s_chd, mp, n_par, K, m, fscale, sp.beta, sp.center, s_lq, s_idr,
                           prank, edge_rows + base, out);
